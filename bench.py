@@ -1,0 +1,217 @@
+#!/usr/bin/env python3
+"""Benchmark of the TwinQuant dual-component W4A4 linear layer on one MI355X.
+
+One step = one forward of the LLaMA3-8B q_proj/o_proj-shaped layer
+(K = N = 4096, rank 64, group 64) for each token count M in {1, 16, 128, 2048}:
+activation quantization (tq_quant_act) followed by the fused layer
+(tq_dual_gemm), four layer calls in all.  Inputs are seeded synthetic tensors
+resident in HBM before timing starts; the packed weights are replicated over
+>= 1 GiB of distinct copies and every call uses the next copy, so decode-sized
+calls read their weights from HBM rather than from the 256 MB last-level cache.
+
+Prints one JSON line: effective TFLOPS (2*M*N*K summed over the step / step
+time), per-M microseconds per layer next to an fp16 GEMM of the same shape
+(torch.matmul -> hipBLASLt), the roofline position of the dominant kernel
+(tq_dual_gemm at M = 2048, timed with HIP events on its own stream) and the
+CPU oracle timed on the host as a reported baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "dual-component W4A4 linear: µs/layer & TFLOPS (M=1..4096) vs fp16 GEMM"
+WORKLOAD = "llama3-8b-qo"
+MS = (1, 16, 128, 2048)
+K = N = 4096
+RANK = 64
+GROUP = 64
+FP8_MFMA_PEAK_TFLOPS = 5000.0   # MI355X dense fp8 matrix peak (5.0 PFLOP/s)
+HBM_PEAK_GBS = 8000.0
+ROTATE_BYTES = 1 << 30
+
+
+def alg_ops(m, n=N, k=K, r=RANK):
+    return 2.0 * m * (n * k + k * r + r * n)
+
+
+def alg_bytes(m, n=N, k=K, r=RANK, g=GROUP):
+    gr = min(g, r)
+    return (n * k / 2 + 2 * n * k / g + k * r / 2 + 2 * r * k / g + r * n / 2 + 2 * n * r / gr
+            + m * k / 2 + 2 * m * k / g + 2 * m * n)
+
+
+def cpu_baseline(data):
+    """The oracle as it stands, on the host cores, over the step's four layer
+    calls (every token of every M), repeated to at least 10 s of work."""
+    import oracle
+    oracle.lib()
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    flops = 0.0
+    t0 = time.perf_counter()
+    reps = 0
+    while True:
+        for m in MS:
+            d = data[m]
+            oracle.layer(d["X"], d["W_res"], d["L1"], d["L2"], GROUP)
+            flops += 2.0 * m * N * K
+        reps += 1
+        if time.perf_counter() - t0 >= 10.0 or reps >= 5:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": flops / dt / 1e12, "unit": "TFLOPS", "cores": threads, "kind": "oracle",
+            "sample": f"the full step (M={','.join(map(str, MS))}, every token) x{reps}, "
+                      f"{dt:.1f} s on the host, weight quantization included in each call"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the layer runs on a single MI355X "
+              "(multi-GPU sharding is a design note, not built)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2606_01556_amd as tq
+    from tq_synth import WORKLOADS, weights, activations
+
+    wl = WORKLOADS[WORKLOAD]
+    layer = wl.layers[0]
+    w = weights(wl, layer)
+    data = {m: {"X": activations(wl, m, K), **w} for m in MS}
+
+    dev = torch.device("cuda")
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        lay = tq.Layer(torch.from_numpy(w["W_res"]).to(dev), torch.from_numpy(w["L1"]).to(dev),
+                       torch.from_numpy(w["L2"]).to(dev), stream=stream)
+        desc = lay.desc
+        ncopy = max(2, int(np.ceil(ROTATE_BYTES / desc.packed_bytes)))
+        copies = [lay.packed] + [lay.packed.clone() for _ in range(ncopy - 1)]
+        X = {m: torch.from_numpy(data[m]["X"]).to(dev) for m in MS}
+        act = {m: tq.empty_act(m, K) for m in MS}
+        Y = {m: torch.empty((m, N), dtype=torch.float16, device=dev) for m in MS}
+        WT = torch.from_numpy(w["W_res"]).to(dev).t().contiguous()   # [K, N] fp16
+        nwt = max(2, int(np.ceil(ROTATE_BYTES / (WT.numel() * 2))))
+        WTs = [WT] + [WT.clone() for _ in range(nwt - 1)]
+    torch.cuda.synchronize()
+    s = stream.cuda_stream
+    dom_m = MS[-1]
+    call = [0]
+
+    def layer_call(m, ev=None):
+        xc, xs = act[m]
+        tq.quant_act(X[m], xc, xs, stream=s)
+        p = copies[call[0] % ncopy]
+        call[0] += 1
+        if ev is not None:
+            ev[0].record(stream)
+        tq.dual_gemm(desc, p, xc, xs, m, Y[m], stream=s)
+        if ev is not None:
+            ev[1].record(stream)
+
+    def step(evs=None):
+        for m in MS:
+            layer_call(m, evs if m == dom_m else None)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # ---- timed region: exactly `steps` steps ----
+    evpairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for i in range(args.steps):
+        step(evpairs[i])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    ms_step = t_start.elapsed_time(t_end) / args.steps
+    dom_us = 1e3 * float(np.mean([a.elapsed_time(b) for a, b in evpairs]))
+
+    # ---- per-M detail (outside the timed region) ----
+    def timed(fn, reps=50):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        for _ in range(3):
+            fn()
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return 1e3 * e0.elapsed_time(e1) / reps
+
+    per_m = []
+    for m in MS:
+        xc, xs = act[m]
+        us_layer = timed(lambda: layer_call(m))
+        us_quant = timed(lambda: tq.quant_act(X[m], xc, xs, stream=s))
+
+        def g():
+            p = copies[call[0] % ncopy]
+            call[0] += 1
+            tq.dual_gemm(desc, p, xc, xs, m, Y[m], stream=s)
+        us_gemm = timed(g)
+        def f16():
+            wt = WTs[call[0] % nwt]
+            call[0] += 1
+            torch.matmul(X[m], wt)
+        with torch.cuda.stream(stream):
+            us_fp16 = timed(f16)
+        per_m.append({
+            "M": m, "us_layer": round(us_layer, 3), "us_dual_gemm": round(us_gemm, 3),
+            "us_quant_act": round(us_quant, 3),
+            "tflops_nominal": round(2.0 * m * N * K / us_layer / 1e6, 2),
+            "tops_algorithmic_gemm": round(alg_ops(m) / us_gemm / 1e6, 2),
+            "gbs_algorithmic_gemm": round(alg_bytes(m) / us_gemm / 1e3, 1),
+            "hbm_frac_gemm": round(alg_bytes(m) / us_gemm / 1e3 / HBM_PEAK_GBS, 3),
+            "fp16_gemm_us": round(us_fp16, 3),
+            "speedup_vs_fp16": round(us_fp16 / us_layer, 3),
+        })
+
+    flops_step = sum(2.0 * m * N * K for m in MS)
+    achieved = alg_ops(dom_m) / dom_us / 1e6        # TFLOP/s (fp8 matrix-core ops)
+    out = {
+        "metric": METRIC,
+        "value": round(flops_step / (ms_step * 1e-3) / 1e12, 3),
+        "unit": "TFLOPS",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "int4",
+        "data": "synthetic",
+        "config": {"workload": "LLaMA3-8B q_proj/o_proj shape: K=N=4096, rank 64, group 64; "
+                               "one step = one layer call at each M in (1, 16, 128, 2048)",
+                   "K": K, "N": N, "rank": RANK, "group": GROUP, "M": list(MS),
+                   "weight_copies_rotated": ncopy,
+                   "compute": "int4 codes as exact fp8-e4m3 matrix-core operands, fp32 accumulate"},
+        "per_m": per_m,
+        "roofline": {"kernel": f"tq_dual_gemm M={dom_m}", "bound": "mfma",
+                     "achieved": round(achieved, 1), "peak": FP8_MFMA_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / FP8_MFMA_PEAK_TFLOPS, 4),
+                     "traffic": None, "avg_launch_us": round(dom_us, 3),
+                     "ops_per_launch": alg_ops(dom_m)},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(data)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

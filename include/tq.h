@@ -1,0 +1,154 @@
+/*
+ * tq.h -- C ABI of the TwinQuant dual-component W4A4 linear layer for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The layer (paper "TwinQuant: Learnable Subspace Decomposition for 4-Bit
+ * LLM Quantization", Sec. 4.1 Eq. 4/6 and Sec. 4.3) is
+ *
+ *     Y = Q(X) [ Q(L1) Q(L2) + Q(W_res)^T ]
+ *
+ * X [m,k] activations, W_res [n,k] the 4-bit residual component R' (stored
+ * like a PyTorch Linear weight, Y = X W_res^T), L1 = U' [k,r] and
+ * L2 = V' [r,n] the low-rank factors.  Q is the symmetric 4-bit group
+ * quantizer of Sec. 2 Eq. (1): codes q in [-7, 7], one fp16 scale
+ * s = fp16(max|v| / 7) per group of `group` consecutive values along the
+ * reduction axis (Sec. 5.1 uses groups of contiguous elements).  The low-rank
+ * branch is two integer products: H = Q(X) Q(L1) is formed on chip,
+ * re-quantized per token and group of min(group, r) rank columns with an fp32
+ * scale s_H, and multiplied by Q(L2); both branches are merged in one
+ * epilogue with a single rounding to fp16 or bf16 (Sec. 4.3, "fused two-stage
+ * low-rank pipeline" and "on-the-fly scaling with a single epilogue").
+ *
+ * Conventions for every entry point:
+ *  - All array pointers are DEVICE pointers owned by the caller; the library
+ *    never allocates, frees or synchronizes and keeps no global state.
+ *    Device pointers must be 16-byte aligned (TQ_ERR_ALIGN otherwise).
+ *  - `stream` is a hipStream_t (NULL = the default stream).  Work is enqueued
+ *    asynchronously on it; results are visible after the stream completes.
+ *  - Arguments are validated on the host before anything is launched; on any
+ *    error nothing is written and the call returns the error code.  A failed
+ *    launch returns TQ_ERR_HIP.  No C++ exception crosses the ABI.
+ *  - Inputs must be finite; for NaN/Inf inputs results are unspecified (but
+ *    every access stays in bounds).
+ *  - fp16 / bf16 values are passed as their 16-bit IEEE bit patterns.
+ *
+ * TQ4 code word (the packed 4-bit format of activations and of exported
+ * weights).  A little-endian 32-bit word holds 8 consecutive codes c0..c7
+ * (consecutive along the reduction axis) in sign-magnitude form:
+ *     c_i     (i < 4): |c_i| in bits 8i..8i+2,  sign in bit 8i+7
+ *     c_(4+i) (i < 4): |c_(4+i)| in bits 8i+4..8i+6,
+ *                      sign in bit 8*((i+1) mod 4) + 3
+ * A sign bit is 1 for negative codes only (zero is never "-0").  The layout
+ * lets the kernels turn 8 codes into two words of fp8 e4m3 matrix-core
+ * operands with three bit operations (mask, rotate, mask).
+ */
+#ifndef TQ_H
+#define TQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    TQ_OK = 0,
+    TQ_ERR_NULL = 1,    /* a required pointer is NULL                        */
+    TQ_ERR_SHAPE = 2,   /* a size is out of range                            */
+    TQ_ERR_GROUP = 3,   /* group size unsupported or k not a multiple of it  */
+    TQ_ERR_RANK = 4,    /* rank unsupported                                  */
+    TQ_ERR_DTYPE = 5,   /* unknown output dtype                              */
+    TQ_ERR_ALIGN = 6,   /* a device pointer is not 16-byte aligned           */
+    TQ_ERR_BUFFER = 7,  /* descriptor inconsistent / not initialised         */
+    TQ_ERR_HIP = 8      /* the HIP runtime reported an error on launch       */
+} tq_status;
+
+typedef enum { TQ_F16 = 0, TQ_BF16 = 1 } tq_dtype;
+
+/* Geometry of one layer's packed weights.  Filled by tq_weight_desc_init;
+ * treat every field as read-only. */
+typedef struct {
+    int32_t n, k, rank, group;   /* layer sizes; group = quantization group    */
+    int32_t group_r;             /* group along the rank axis = min(group, r)  */
+    int32_t n_pad;               /* n rounded up to 32                         */
+    int32_t r_pad32, r_pad64;    /* r rounded up to 32 and to 64               */
+    int32_t magic;               /* set by tq_weight_desc_init                 */
+    int32_t reserved;
+    uint64_t packed_bytes;       /* size of the packed weight buffer           */
+    uint64_t off_w, off_ws, off_l1, off_l1s, off_l2, off_l2s;  /* section offsets */
+} tq_weight_desc;
+
+/* Validate a layer shape and fill `out` (host only, touches no GPU).
+ *   n >= 1 output features, k input features with k % group == 0,
+ *   group == 64 (the only group size built), rank r in {0, 8, 16, 32, 64,
+ *   128}.  r == 0 is the plain 4-bit linear layer of Sec. 2 Eq. (2).
+ * Errors: TQ_ERR_NULL, TQ_ERR_SHAPE, TQ_ERR_GROUP, TQ_ERR_RANK. */
+tq_status tq_weight_desc_init(int n, int k, int rank, int group, tq_weight_desc *out);
+
+/* Quantize and pack one layer's weights (the offline fold of Sec. 4.1:
+ * U', V', R' are quantized once and stored in 4 bits).
+ *   w_res  [n,k] fp16 row-major   (quantized per row, groups along k)
+ *   l1     [k,r] fp16 row-major   (quantized per column, groups along k)
+ *   l2     [r,n] fp16 row-major   (quantized per column, groups of group_r
+ *                                  along r); l1 and l2 may be NULL iff r == 0
+ *   packed  device buffer of d->packed_bytes bytes, written completely; its
+ *           layout is private to the library (see tq_export_weights).
+ * Errors: TQ_ERR_NULL, TQ_ERR_BUFFER, TQ_ERR_ALIGN, TQ_ERR_HIP. */
+tq_status tq_pack_weights(const tq_weight_desc *d, const void *w_res, const void *l1,
+                          const void *l2, void *packed, void *stream);
+
+/* Per-token, per-group activation quantizer (Sec. 2 Eq. 1; Sec. 4.3: the
+ * activation is quantized once and shared by both branches).
+ *   x         [m,k] fp16 row-major, m >= 0, k % group == 0, group == 64
+ *   x_codes   [m, k/8] TQ4 code words (m*k/2 bytes), row-major
+ *   x_scales  [k/group, m] fp16: the scale of token i, group g is
+ *             x_scales[g*m + i] (group-major, so one group's scales of a
+ *             token tile are contiguous)
+ * m == 0 is a no-op.  Errors: TQ_ERR_NULL, TQ_ERR_SHAPE, TQ_ERR_GROUP,
+ * TQ_ERR_ALIGN, TQ_ERR_HIP. */
+tq_status tq_quant_act(const void *x, int m, int k, int group, void *x_codes,
+                       void *x_scales, void *stream);
+
+/* The fused dual-component layer: residual 4-bit GEMM, low-rank stage 1
+ * (H = Q(X) Q(L1), kept on chip), on-the-fly re-quantization of H, stage 2
+ * (Q_H Q(L2)), and one epilogue that sums both branches and stores Y once.
+ *   packed            buffer written by tq_pack_weights for descriptor d
+ *   x_codes/x_scales  written by tq_quant_act for the same k (m tokens)
+ *   y                 [m,n] output, fp16 or bf16 per y_dtype, row-major
+ * One kernel launch, no workspace, no global intermediate.  m == 0 is a
+ * no-op.  Errors: TQ_ERR_NULL, TQ_ERR_SHAPE, TQ_ERR_BUFFER, TQ_ERR_DTYPE,
+ * TQ_ERR_ALIGN, TQ_ERR_HIP. */
+tq_status tq_dual_gemm(const tq_weight_desc *d, const void *packed, const void *x_codes,
+                       const void *x_scales, int m, void *y, tq_dtype y_dtype, void *stream);
+
+/* Same computation and kernel as tq_dual_gemm, for tests: additionally
+ * copies the on-chip low-rank intermediate of every token out of the kernel.
+ *   h   [m,r] fp32     H before re-quantization
+ *   sh  [m,r/group_r]  fp32 scales s_H
+ *   qh  [m,r] int8     codes Q_H in [-7, 7]
+ * Errors as tq_dual_gemm; additionally TQ_ERR_RANK when r == 0. */
+tq_status tq_dual_gemm_debug(const tq_weight_desc *d, const void *packed, const void *x_codes,
+                             const void *x_scales, int m, void *y, tq_dtype y_dtype,
+                             void *h, void *sh, void *qh, void *stream);
+
+/* Copy the packed weights out in the canonical layout (for tests/debug):
+ *   w_codes  [n, k/8] TQ4 words      w_scales  [n, k/group] fp16
+ *   l1_codes [r, k/8] TQ4 words (row j = column j of L1, along k)
+ *   l1_scales[r, k/group] fp16
+ *   l2_codes [n, r/8] TQ4 words (row c = column c of L2, along r)
+ *   l2_scales[n, r/group_r] fp16
+ * The l1/l2 pointers may be NULL iff r == 0.
+ * Errors: TQ_ERR_NULL, TQ_ERR_BUFFER, TQ_ERR_ALIGN, TQ_ERR_HIP. */
+tq_status tq_export_weights(const tq_weight_desc *d, const void *packed, void *w_codes,
+                            void *w_scales, void *l1_codes, void *l1_scales, void *l2_codes,
+                            void *l2_scales, void *stream);
+
+/* Static description of a status code; never NULL. */
+const char *tq_status_string(tq_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TQ_H */

@@ -1,0 +1,193 @@
+"""TwinQuant dual-component W4A4 linear layer on AMD MI355X (gfx950).
+
+Thin Python binding of ``libtq.so`` (C ABI in ``include/tq.h``).  Every step of
+the layer runs in the library's HIP kernels; this module only marshals
+arguments (device pointers from torch tensors, the current HIP stream) and
+turns non-zero status codes into exceptions.  It never computes the layer
+itself and has no CPU fallback: if the library is missing it raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtq.so")
+GROUP = 64
+
+TQ_F16, TQ_BF16 = 0, 1
+STATUS = {0: "TQ_OK", 1: "TQ_ERR_NULL", 2: "TQ_ERR_SHAPE", 3: "TQ_ERR_GROUP", 4: "TQ_ERR_RANK",
+          5: "TQ_ERR_DTYPE", 6: "TQ_ERR_ALIGN", 7: "TQ_ERR_BUFFER", 8: "TQ_ERR_HIP"}
+
+
+class TQError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        super().__init__(f"{where}: {STATUS.get(code, code)} ({lib().tq_status_string(code).decode()})")
+
+
+class WeightDesc(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int32), ("k", ctypes.c_int32), ("rank", ctypes.c_int32),
+                ("group", ctypes.c_int32), ("group_r", ctypes.c_int32), ("n_pad", ctypes.c_int32),
+                ("r_pad32", ctypes.c_int32), ("r_pad64", ctypes.c_int32), ("magic", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("packed_bytes", ctypes.c_uint64),
+                ("off_w", ctypes.c_uint64), ("off_ws", ctypes.c_uint64), ("off_l1", ctypes.c_uint64),
+                ("off_l1s", ctypes.c_uint64), ("off_l2", ctypes.c_uint64), ("off_l2s", ctypes.c_uint64)]
+
+
+EXPORTS = ("tq_weight_desc_init", "tq_pack_weights", "tq_quant_act", "tq_dual_gemm",
+           "tq_dual_gemm_debug", "tq_export_weights", "tq_status_string")
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libtq.so (built by ``paper_2606_01556_amd.build``); raise if absent."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2606_01556_amd.build` (there is no fallback)")
+        L = ctypes.CDLL(LIB_PATH)
+        P, I = ctypes.c_void_p, ctypes.c_int
+        D = ctypes.POINTER(WeightDesc)
+        L.tq_weight_desc_init.argtypes = [I, I, I, I, D]
+        L.tq_pack_weights.argtypes = [D, P, P, P, P, P]
+        L.tq_quant_act.argtypes = [P, I, I, I, P, P, P]
+        L.tq_dual_gemm.argtypes = [D, P, P, P, I, P, I, P]
+        L.tq_dual_gemm_debug.argtypes = [D, P, P, P, I, P, I, P, P, P, P]
+        L.tq_export_weights.argtypes = [D, P, P, P, P, P, P, P, P]
+        L.tq_status_string.argtypes = [I]
+        L.tq_status_string.restype = ctypes.c_char_p
+        for name in EXPORTS[:-1]:
+            getattr(L, name).restype = I
+        _lib = L
+    return _lib
+
+
+def _check(code: int, where: str):
+    if code != 0:
+        raise TQError(code, where)
+
+
+def _ptr(t):
+    """Device pointer of a torch tensor (or an int address, or None)."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+# ------------------------------------------------------------------ C ABI
+def weight_desc_init(n: int, k: int, rank: int, group: int = GROUP) -> WeightDesc:
+    d = WeightDesc()
+    _check(lib().tq_weight_desc_init(n, k, rank, group, ctypes.byref(d)), "tq_weight_desc_init")
+    return d
+
+
+def pack_weights(desc: WeightDesc, w_res, l1, l2, packed, stream=None):
+    _check(lib().tq_pack_weights(ctypes.byref(desc), _ptr(w_res), _ptr(l1), _ptr(l2), _ptr(packed),
+                                 _stream(stream)), "tq_pack_weights")
+
+
+def quant_act(x, x_codes, x_scales, group: int = GROUP, stream=None):
+    m, k = x.shape
+    _check(lib().tq_quant_act(_ptr(x), m, k, group, _ptr(x_codes), _ptr(x_scales), _stream(stream)),
+           "tq_quant_act")
+
+
+def dual_gemm(desc: WeightDesc, packed, x_codes, x_scales, m: int, y, bf16: bool = False, stream=None):
+    _check(lib().tq_dual_gemm(ctypes.byref(desc), _ptr(packed), _ptr(x_codes), _ptr(x_scales), m,
+                              _ptr(y), TQ_BF16 if bf16 else TQ_F16, _stream(stream)), "tq_dual_gemm")
+
+
+def dual_gemm_debug(desc: WeightDesc, packed, x_codes, x_scales, m: int, y, h, sh, qh,
+                    bf16: bool = False, stream=None):
+    _check(lib().tq_dual_gemm_debug(ctypes.byref(desc), _ptr(packed), _ptr(x_codes), _ptr(x_scales), m,
+                                    _ptr(y), TQ_BF16 if bf16 else TQ_F16, _ptr(h), _ptr(sh), _ptr(qh),
+                                    _stream(stream)), "tq_dual_gemm_debug")
+
+
+def export_weights(desc: WeightDesc, packed, w_codes, w_scales, l1_codes=None, l1_scales=None,
+                   l2_codes=None, l2_scales=None, stream=None):
+    _check(lib().tq_export_weights(ctypes.byref(desc), _ptr(packed), _ptr(w_codes), _ptr(w_scales),
+                                   _ptr(l1_codes), _ptr(l1_scales), _ptr(l2_codes), _ptr(l2_scales),
+                                   _stream(stream)), "tq_export_weights")
+
+
+# ------------------------------------------------------------------ buffers
+def empty_packed(desc: WeightDesc, device="cuda"):
+    import torch
+    return torch.empty(int(desc.packed_bytes), dtype=torch.uint8, device=device)
+
+
+def empty_act(m: int, k: int, device="cuda"):
+    """(x_codes [m, k/8] int32 TQ4 words, x_scales [k/64, m] fp16)."""
+    import torch
+    return (torch.empty((m, k // 8), dtype=torch.int32, device=device),
+            torch.empty((k // GROUP, max(m, 1)), dtype=torch.float16, device=device))
+
+
+class Layer:
+    """One packed layer: descriptor + packed device buffer (device memory from torch)."""
+
+    def __init__(self, w_res, l1=None, l2=None, group: int = GROUP, stream=None):
+        n, k = w_res.shape
+        r = 0 if l1 is None else l1.shape[1]
+        self.desc = weight_desc_init(n, k, r, group)
+        self.packed = empty_packed(self.desc, w_res.device)
+        pack_weights(self.desc, w_res.contiguous(), None if l1 is None else l1.contiguous(),
+                     None if l2 is None else l2.contiguous(), self.packed, stream)
+        self.n, self.k, self.rank = n, k, r
+
+    def __call__(self, x, bf16: bool = False, stream=None):
+        import torch
+        m = x.shape[0]
+        xc, xs = empty_act(m, self.k, x.device)
+        y = torch.empty((m, self.n), dtype=torch.bfloat16 if bf16 else torch.float16, device=x.device)
+        quant_act(x.contiguous(), xc, xs, stream=stream)
+        dual_gemm(self.desc, self.packed, xc, xs, m, y, bf16, stream)
+        return y
+
+
+# ------------------------------------------------------------------ format helpers
+def tq4_decode(words) -> np.ndarray:
+    """TQ4 words (uint32/int32 array [..., w]) -> int8 codes [..., 8w] (host side)."""
+    w = np.ascontiguousarray(words).view(np.uint32)
+    out = np.zeros(w.shape + (8,), np.int8)
+    for i in range(4):
+        mag = (w >> (8 * i)) & 7
+        sgn = (w >> (8 * i + 7)) & 1
+        out[..., i] = np.where(sgn == 1, -mag.astype(np.int16), mag).astype(np.int8)
+        mag2 = (w >> (8 * i + 4)) & 7
+        sgn2 = (w >> (8 * ((i + 1) % 4) + 3)) & 1
+        out[..., 4 + i] = np.where(sgn2 == 1, -mag2.astype(np.int16), mag2).astype(np.int8)
+    return out.reshape(w.shape[:-1] + (w.shape[-1] * 8,))
+
+
+def tq4_encode(codes) -> np.ndarray:
+    """int8 codes in [-7, 7], last axis a multiple of 8 -> TQ4 words (uint32)."""
+    c = np.ascontiguousarray(codes).astype(np.int32)
+    assert c.shape[-1] % 8 == 0 and np.all(np.abs(c) <= 7)
+    c = c.reshape(c.shape[:-1] + (c.shape[-1] // 8, 8))
+    mag = np.abs(c).astype(np.uint32)
+    neg = (c < 0).astype(np.uint32)
+    w = np.zeros(c.shape[:-1], np.uint32)
+    for i in range(4):
+        w |= mag[..., i] << (8 * i)
+        w |= neg[..., i] << (8 * i + 7)
+        w |= mag[..., 4 + i] << (8 * i + 4)
+        w |= neg[..., 4 + i] << (8 * ((i + 1) % 4) + 3)
+    return w

@@ -1,0 +1,169 @@
+// C ABI of libtq: argument validation on the host, then one or more kernel
+// launches on the caller's stream.  No allocation, no synchronization, no
+// global state.
+#include <stdint.h>
+
+#include "tq.h"
+#include "tq_kernels.hpp"
+
+namespace {
+
+constexpr int32_t kMagic = 0x54513401;  // "TQ4" + layout version 1
+
+inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+inline uint64_t round_up(uint64_t v, uint64_t a) { return (v + a - 1) / a * a; }
+
+bool desc_ok(const tq_weight_desc *d) {
+  return d != nullptr && d->magic == kMagic && d->group == 64 && d->k % 64 == 0 && d->n >= 1 &&
+         d->n_pad == (int32_t)round_up((uint64_t)d->n, 32) &&
+         d->r_pad32 == (int32_t)round_up((uint64_t)d->rank, 32) &&
+         d->r_pad64 == (int32_t)round_up((uint64_t)d->rank, 64);
+}
+
+tq::Geometry geometry(const tq_weight_desc *d) {
+  tq::Geometry g;
+  g.n = d->n; g.k = d->k; g.r = d->rank; g.gr = d->group_r;
+  g.n_pad = d->n_pad; g.r_pad32 = d->r_pad32; g.r_pad64 = d->r_pad64;
+  g.off_w = d->off_w; g.off_ws = d->off_ws; g.off_l1 = d->off_l1;
+  g.off_l1s = d->off_l1s; g.off_l2 = d->off_l2; g.off_l2s = d->off_l2s;
+  return g;
+}
+
+tq_status hip_status(hipError_t e) { return e == hipSuccess ? TQ_OK : TQ_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+tq_status tq_weight_desc_init(int n, int k, int rank, int group, tq_weight_desc *out) {
+  if (out == nullptr) return TQ_ERR_NULL;
+  if (group != 64) return TQ_ERR_GROUP;
+  if (n < 1 || k < 1 || n > (1 << 24) || k > (1 << 24)) return TQ_ERR_SHAPE;
+  if (k % group != 0) return TQ_ERR_GROUP;
+  if (!(rank == 0 || rank == 8 || rank == 16 || rank == 32 || rank == 64 || rank == 128))
+    return TQ_ERR_RANK;
+  tq_weight_desc d = {};
+  d.n = n; d.k = k; d.rank = rank; d.group = group;
+  d.group_r = rank == 0 ? 0 : (rank < group ? rank : group);
+  d.n_pad = (int32_t)round_up((uint64_t)n, 32);
+  d.r_pad32 = (int32_t)round_up((uint64_t)rank, 32);
+  d.r_pad64 = (int32_t)round_up((uint64_t)rank, 64);
+  d.magic = kMagic;
+  const uint64_t kg = (uint64_t)k / 64;
+  uint64_t off = 0;
+  d.off_w = off;   off = round_up(off + (uint64_t)d.n_pad / 32 * kg * 1024, 256);
+  d.off_ws = off;  off = round_up(off + kg * (uint64_t)d.n_pad * 2, 256);
+  d.off_l1 = off;  off = round_up(off + (uint64_t)d.r_pad32 / 32 * kg * 1024, 256);
+  d.off_l1s = off; off = round_up(off + kg * (uint64_t)d.r_pad32 * 2, 256);
+  d.off_l2 = off;  off = round_up(off + (uint64_t)d.n_pad / 32 * ((uint64_t)d.r_pad64 / 64) * 1024, 256);
+  d.off_l2s = off;
+  const uint64_t rgroups = rank == 0 ? 0 : (uint64_t)rank / (uint64_t)d.group_r;
+  off = round_up(off + rgroups * (uint64_t)d.n_pad * 2, 256);
+  d.packed_bytes = off;
+  *out = d;
+  return TQ_OK;
+}
+
+tq_status tq_pack_weights(const tq_weight_desc *d, const void *w_res, const void *l1,
+                          const void *l2, void *packed, void *stream) {
+  if (d == nullptr || w_res == nullptr || packed == nullptr) return TQ_ERR_NULL;
+  if (!desc_ok(d)) return TQ_ERR_BUFFER;
+  if (d->rank > 0 && (l1 == nullptr || l2 == nullptr)) return TQ_ERR_NULL;
+  if (!aligned16(w_res) || !aligned16(packed) || (d->rank > 0 && (!aligned16(l1) || !aligned16(l2))))
+    return TQ_ERR_ALIGN;
+  return hip_status(tq::launch_pack(geometry(d), static_cast<const uint16_t *>(w_res),
+                                    static_cast<const uint16_t *>(l1),
+                                    static_cast<const uint16_t *>(l2),
+                                    static_cast<uint8_t *>(packed),
+                                    static_cast<hipStream_t>(stream)));
+}
+
+tq_status tq_quant_act(const void *x, int m, int k, int group, void *x_codes, void *x_scales,
+                       void *stream) {
+  if (x == nullptr || x_codes == nullptr || x_scales == nullptr) return TQ_ERR_NULL;
+  if (group != 64) return TQ_ERR_GROUP;
+  if (m < 0 || k < 1 || k > (1 << 24)) return TQ_ERR_SHAPE;
+  if (k % group != 0) return TQ_ERR_GROUP;
+  if (!aligned16(x) || !aligned16(x_codes) || !aligned16(x_scales)) return TQ_ERR_ALIGN;
+  if ((int64_t)m * k >= ((int64_t)1 << 40)) return TQ_ERR_SHAPE;
+  if (m == 0) return TQ_OK;
+  return hip_status(tq::launch_quant_act(static_cast<const uint16_t *>(x), m, k,
+                                         static_cast<uint32_t *>(x_codes),
+                                         static_cast<uint16_t *>(x_scales),
+                                         static_cast<hipStream_t>(stream)));
+}
+
+static tq_status dual_gemm_impl(const tq_weight_desc *d, const void *packed, const void *x_codes,
+                                const void *x_scales, int m, void *y, tq_dtype y_dtype, void *h,
+                                void *sh, void *qh, void *stream) {
+  if (d == nullptr || packed == nullptr || x_codes == nullptr || x_scales == nullptr || y == nullptr)
+    return TQ_ERR_NULL;
+  if (!desc_ok(d)) return TQ_ERR_BUFFER;
+  if (m < 0 || m > (1 << 24)) return TQ_ERR_SHAPE;
+  if (y_dtype != TQ_F16 && y_dtype != TQ_BF16) return TQ_ERR_DTYPE;
+  if (!aligned16(packed) || !aligned16(x_codes) || !aligned16(x_scales) || !aligned16(y))
+    return TQ_ERR_ALIGN;
+  if (h != nullptr && (!aligned16(h) || !aligned16(sh) || !aligned16(qh))) return TQ_ERR_ALIGN;
+  if (m == 0) return TQ_OK;
+  tq::GemmArgs a;
+  a.packed = static_cast<const uint8_t *>(packed);
+  a.geo = geometry(d);
+  a.xc = static_cast<const uint32_t *>(x_codes);
+  a.xs = static_cast<const uint16_t *>(x_scales);
+  a.y = y;
+  a.m = m;
+  a.bf16_out = y_dtype == TQ_BF16;
+  a.dbg_h = static_cast<float *>(h);
+  a.dbg_sh = static_cast<float *>(sh);
+  a.dbg_qh = static_cast<int8_t *>(qh);
+  return hip_status(tq::launch_dual_gemm(a, static_cast<hipStream_t>(stream)));
+}
+
+tq_status tq_dual_gemm(const tq_weight_desc *d, const void *packed, const void *x_codes,
+                       const void *x_scales, int m, void *y, tq_dtype y_dtype, void *stream) {
+  return dual_gemm_impl(d, packed, x_codes, x_scales, m, y, y_dtype, nullptr, nullptr, nullptr,
+                        stream);
+}
+
+tq_status tq_dual_gemm_debug(const tq_weight_desc *d, const void *packed, const void *x_codes,
+                             const void *x_scales, int m, void *y, tq_dtype y_dtype, void *h,
+                             void *sh, void *qh, void *stream) {
+  if (h == nullptr || sh == nullptr || qh == nullptr) return TQ_ERR_NULL;
+  if (d != nullptr && d->rank == 0) return TQ_ERR_RANK;
+  return dual_gemm_impl(d, packed, x_codes, x_scales, m, y, y_dtype, h, sh, qh, stream);
+}
+
+tq_status tq_export_weights(const tq_weight_desc *d, const void *packed, void *w_codes,
+                            void *w_scales, void *l1_codes, void *l1_scales, void *l2_codes,
+                            void *l2_scales, void *stream) {
+  if (d == nullptr || packed == nullptr || w_codes == nullptr || w_scales == nullptr)
+    return TQ_ERR_NULL;
+  if (!desc_ok(d)) return TQ_ERR_BUFFER;
+  if (d->rank > 0 && (!l1_codes || !l1_scales || !l2_codes || !l2_scales)) return TQ_ERR_NULL;
+  if (!aligned16(packed) || !aligned16(w_codes) || !aligned16(w_scales)) return TQ_ERR_ALIGN;
+  if (d->rank > 0 && (!aligned16(l1_codes) || !aligned16(l1_scales) || !aligned16(l2_codes) ||
+                      !aligned16(l2_scales)))
+    return TQ_ERR_ALIGN;
+  return hip_status(tq::launch_export(
+      geometry(d), static_cast<const uint8_t *>(packed), static_cast<uint32_t *>(w_codes),
+      static_cast<uint16_t *>(w_scales), static_cast<uint32_t *>(l1_codes),
+      static_cast<uint16_t *>(l1_scales), static_cast<uint32_t *>(l2_codes),
+      static_cast<uint16_t *>(l2_scales), static_cast<hipStream_t>(stream)));
+}
+
+const char *tq_status_string(tq_status s) {
+  switch (s) {
+    case TQ_OK: return "ok";
+    case TQ_ERR_NULL: return "a required pointer is NULL";
+    case TQ_ERR_SHAPE: return "size out of range";
+    case TQ_ERR_GROUP: return "unsupported group size or k not a multiple of it";
+    case TQ_ERR_RANK: return "unsupported rank";
+    case TQ_ERR_DTYPE: return "unknown output dtype";
+    case TQ_ERR_ALIGN: return "device pointer not 16-byte aligned";
+    case TQ_ERR_BUFFER: return "weight descriptor not initialised or inconsistent";
+    case TQ_ERR_HIP: return "HIP runtime error on launch";
+  }
+  return "unknown status";
+}
+
+}  // extern "C"

@@ -1,0 +1,111 @@
+// Device helpers shared by the TwinQuant HIP kernels (gfx950 / MI355X).
+//
+// Numeric conventions (paper Sec. 2 Eq. 1, Sec. 4.3):
+//  * a group's scale is s = fp16_rne(fp32(max|v|) / 7) (IEEE fp32 division);
+//  * a code is q = clamp(rint(fp32(v) / s), -7, 7), 0 when s == 0;
+//  * codes reach the matrix cores as fp8 e4m3 bytes whose exponent field is
+//    zero: byte = sign << 7 | |q| encodes q * 2^-9 exactly (e4m3 subnormals),
+//    so every product is exact and a 64-term dot product of codes, with both
+//    operand block scales set to 2^9, comes out of the fp32 accumulator as the
+//    exact integer sum.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tq {
+
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kGroup = 64;
+constexpr int kScale2p9 = 127 + 9;  // E8M0 block scale 2^9
+
+// TQ4 word -> two words of fp8 e4m3 bytes (codes 0..3 and 4..7, in order).
+__device__ __forceinline__ void tq4_to_fp8(uint32_t w, uint32_t &lo, uint32_t &hi) {
+  lo = w & 0x87878787u;
+  hi = __builtin_amdgcn_alignbit(w, w, 4) & 0x87878787u;
+}
+
+// 32 codes (4 TQ4 words, natural order) -> one fp8 matrix-core operand.
+__device__ __forceinline__ v8i unpack32(u32x4 raw) {
+  v8i r;
+  uint32_t lo, hi;
+  tq4_to_fp8(raw.x, lo, hi); r[0] = (int)lo; r[1] = (int)hi;
+  tq4_to_fp8(raw.y, lo, hi); r[2] = (int)lo; r[3] = (int)hi;
+  tq4_to_fp8(raw.z, lo, hi); r[4] = (int)lo; r[5] = (int)hi;
+  tq4_to_fp8(raw.w, lo, hi); r[6] = (int)lo; r[7] = (int)hi;
+  return r;
+}
+
+// Eight codes in [-7, 7] -> one TQ4 word.
+__device__ __forceinline__ uint32_t tq4_pack8(const int c[8]) {
+  uint32_t w = 0;
+#pragma unroll
+  for (int i = 0; i < 4; i++) {
+    uint32_t m = (uint32_t)(c[i] < 0 ? -c[i] : c[i]);
+    w |= m << (8 * i);
+    w |= (uint32_t)(c[i] < 0) << (8 * i + 7);
+    uint32_t m2 = (uint32_t)(c[4 + i] < 0 ? -c[4 + i] : c[4 + i]);
+    w |= m2 << (8 * i + 4);
+    w |= (uint32_t)(c[4 + i] < 0) << (8 * ((i + 1) & 3) + 3);
+  }
+  return w;
+}
+
+// fp8 byte of a code (sign-magnitude e4m3 subnormal).
+__device__ __forceinline__ uint32_t code_to_fp8(int q) {
+  return (uint32_t)(q < 0 ? (0x80 | -q) : q);
+}
+
+__device__ __forceinline__ float half_bits_to_float(uint16_t h) {
+  return (float)__builtin_bit_cast(_Float16, h);
+}
+
+__device__ __forceinline__ uint16_t float_to_half_bits(float f) {
+  return __builtin_bit_cast(uint16_t, (_Float16)f);  // v_cvt_f16_f32, round to nearest even
+}
+
+__device__ __forceinline__ uint16_t float_to_bf16_bits(float f) {
+  uint32_t b = __builtin_bit_cast(uint32_t, f);
+  b += 0x7fffu + ((b >> 16) & 1u);  // round to nearest even (finite inputs)
+  return (uint16_t)(b >> 16);
+}
+
+// Scale of a group from its max |v|: fp16(max / 7) and its fp32 value.
+__device__ __forceinline__ float q4_scale(float amax, uint16_t &s16) {
+  float s32 = amax / 7.0f;  // IEEE division (no fast-math anywhere in this library)
+  s16 = float_to_half_bits(s32);
+  return half_bits_to_float(s16);
+}
+
+__device__ __forceinline__ int q4_code(float v, float s) {
+  if (s == 0.0f) return 0;
+  float t = __builtin_rintf(v / s);
+  t = t > 7.0f ? 7.0f : (t < -7.0f ? -7.0f : t);
+  return (int)t;
+}
+
+// Exact integer dot products of 32x32 code tiles over one group of 64:
+// D[i][j] = sum_k A[i][k] * B[k][j].  Operand lane l holds row/column l % 32,
+// k in [32 * (l / 32), +32); result lane l holds column l % 32, rows
+// 8 * (v / 4) + 4 * (l / 32) + v % 4 for v = 0..15.
+__device__ __forceinline__ v16f mfma_codes_32x32x64(v8i a, v8i b) {
+  const v16f z = {0};
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, z, 0, 0, 0, kScale2p9, 0, kScale2p9);
+}
+
+// Same for 16x16 tiles over 128 k: operand lane l holds row/column l % 16,
+// k in [32 * (l / 16), +32); result lane l: column l % 16, rows 4 * (l / 16) + v.
+__device__ __forceinline__ v4f mfma_codes_16x16x128(v8i a, v8i b) {
+  const v4f z = {0};
+  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, z, 0, 0, 0, kScale2p9, 0, kScale2p9);
+}
+
+__device__ __forceinline__ int row_of_32x32(int lane, int v) {
+  return 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+}
+
+}  // namespace tq

@@ -1,0 +1,44 @@
+// Host-side launch interface of the TwinQuant kernels (internal to libtq).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tq {
+
+// Geometry shared by the packing, export and GEMM kernels.
+//  W_res codes: [n_pad/32][k/64] blocks of 1 KiB; block lane L (16 bytes,
+//               4 TQ4 words) holds column 32*t + L%32, k in [32*(L/32), +32)
+//               of the group.  Scales: [k/64][n_pad] fp16.
+//  L1 codes:    the same block format with the rank index as the column:
+//               [r_pad32/32][k/64] blocks.  Scales: [k/64][r_pad32] fp16.
+//  L2 codes:    [n_pad/32][r_pad64/64] blocks, the rank index as the
+//               reduction axis (zero past r).  Scales: [r/group_r][n_pad].
+struct Geometry {
+  int n, k, r, gr, n_pad, r_pad32, r_pad64;
+  uint64_t off_w, off_ws, off_l1, off_l1s, off_l2, off_l2s;
+};
+
+struct GemmArgs {
+  const uint8_t *packed;
+  Geometry geo;
+  const uint32_t *xc;   // [m][k/8] TQ4 words
+  const uint16_t *xs;   // [k/64][m] fp16
+  void *y;              // [m][n]
+  int m;
+  int bf16_out;
+  float *dbg_h;         // optional [m][r]
+  float *dbg_sh;        // optional [m][r/gr]
+  int8_t *dbg_qh;       // optional [m][r]
+};
+
+hipError_t launch_quant_act(const uint16_t *x, int m, int k, uint32_t *codes, uint16_t *scales,
+                            hipStream_t s);
+hipError_t launch_pack(const Geometry &g, const uint16_t *w, const uint16_t *l1,
+                       const uint16_t *l2, uint8_t *packed, hipStream_t s);
+hipError_t launch_export(const Geometry &g, const uint8_t *packed, uint32_t *wc, uint16_t *ws,
+                         uint32_t *l1c, uint16_t *l1s, uint32_t *l2c, uint16_t *l2s,
+                         hipStream_t s);
+hipError_t launch_dual_gemm(const GemmArgs &a, hipStream_t s);
+
+}  // namespace tq

@@ -1,0 +1,227 @@
+// Activation quantizer, weight packing and weight export kernels.
+//
+// Quantizer: paper Sec. 2 Eq. (1) with q_max = 7, one fp16 scale per group of
+// 64 consecutive values along the reduction axis (Sec. 5.1), round half to
+// even, codes clamped to [-7, 7], an all-zero group gets scale 0.
+#include "tq_device.hpp"
+#include "tq_kernels.hpp"
+
+namespace tq {
+
+// ---------------------------------------------------------------------------
+// Activations: one thread per TQ4 word (8 consecutive values); the 8 threads
+// of a group are consecutive lanes of one wavefront and share the group max
+// through three butterfly shuffles.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void quant_act_kernel(const uint16_t *__restrict__ x, int m,
+                                                        int k, uint32_t *__restrict__ codes,
+                                                        uint16_t *__restrict__ scales) {
+  const int64_t words_per_row = k >> 3;
+  const int64_t nwords = (int64_t)m * words_per_row;
+  const int64_t wid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const bool valid = wid < nwords;
+  u32x4 raw = {0, 0, 0, 0};
+  if (valid) raw = *reinterpret_cast<const u32x4 *>(x + wid * 8);
+  float v[8];
+#pragma unroll
+  for (int i = 0; i < 4; i++) {
+    v[2 * i] = half_bits_to_float((uint16_t)(raw[i] & 0xffffu));
+    v[2 * i + 1] = half_bits_to_float((uint16_t)(raw[i] >> 16));
+  }
+  float amax = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 8; i++) amax = fmaxf(amax, fabsf(v[i]));
+  amax = fmaxf(amax, __shfl_xor(amax, 1));
+  amax = fmaxf(amax, __shfl_xor(amax, 2));
+  amax = fmaxf(amax, __shfl_xor(amax, 4));
+  uint16_t s16;
+  const float s = q4_scale(amax, s16);
+  int c[8];
+#pragma unroll
+  for (int i = 0; i < 8; i++) c[i] = q4_code(v[i], s);
+  if (valid) {
+    codes[wid] = tq4_pack8(c);
+    if ((wid & 7) == 0) {
+      const int64_t gi = wid >> 3;
+      const int64_t groups_per_row = k / kGroup;
+      const int64_t row = gi / groups_per_row, g = gi % groups_per_row;
+      scales[g * m + row] = s16;
+    }
+  }
+}
+
+hipError_t launch_quant_act(const uint16_t *x, int m, int k, uint32_t *codes, uint16_t *scales,
+                            hipStream_t s) {
+  const int64_t nwords = (int64_t)m * (k / 8);
+  const int64_t blocks = (nwords + 255) / 256;
+  hipLaunchKernelGGL(quant_act_kernel, dim3((unsigned)blocks), dim3(256), 0, s, x, m, k, codes,
+                     scales);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Weight packing: one thread per (vector, group) -- a vector is a row of
+// W_res, a column of L1 or a column of L2 -- quantizes its group and writes
+// the codes into the two 16-byte lane slots of its block plus the scale.
+// Vectors past the real sizes (padding to 32 columns / 64 ranks) get zero
+// codes and zero scales, so every byte of the packed buffer is written.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void quantize_group_strided(const uint16_t *src, int64_t stride,
+                                                       int len, bool present, uint32_t out[8],
+                                                       uint16_t &s16) {
+  // len <= 64 values starting at src with the given element stride; codes past
+  // len are zero (len is a multiple of 8).
+  float amax = 0.0f;
+  if (present)
+    for (int i = 0; i < len; i++) amax = fmaxf(amax, fabsf(half_bits_to_float(src[i * stride])));
+  const float s = q4_scale(amax, s16);
+  for (int wd = 0; wd < 8; wd++) {
+    int c[8];
+    for (int i = 0; i < 8; i++) {
+      const int e = wd * 8 + i;
+      c[i] = (present && e < len) ? q4_code(half_bits_to_float(src[e * stride]), s) : 0;
+    }
+    out[wd] = tq4_pack8(c);
+  }
+}
+
+// W_res [n][k] rows and L1 [k][r] columns share the block format.
+__global__ __launch_bounds__(256) void pack_kgroups_kernel(const uint16_t *__restrict__ src,
+                                                           int64_t vec_stride, int64_t elem_stride,
+                                                           int nvec, int nvec_pad, int kgroups,
+                                                           uint8_t *__restrict__ codes,
+                                                           uint16_t *__restrict__ scales) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (int64_t)nvec_pad * kgroups) return;
+  const int g = (int)(t % kgroups);
+  const int v = (int)(t / kgroups);
+  const bool present = v < nvec;
+  uint32_t w[8];
+  uint16_t s16;
+  const uint16_t *p = present ? src + (int64_t)v * vec_stride + (int64_t)g * kGroup * elem_stride : src;
+  quantize_group_strided(p, elem_stride, kGroup, present, w, s16);
+  uint8_t *blk = codes + ((int64_t)(v >> 5) * kgroups + g) * 1024;
+  const int c = v & 31;
+  *reinterpret_cast<u32x4 *>(blk + c * 16) = u32x4{w[0], w[1], w[2], w[3]};
+  *reinterpret_cast<u32x4 *>(blk + (32 + c) * 16) = u32x4{w[4], w[5], w[6], w[7]};
+  scales[(int64_t)g * nvec_pad + v] = s16;
+}
+
+// L2 [r][n]: column n along the rank axis, one 64-rank block per thread.
+__global__ __launch_bounds__(256) void pack_l2_kernel(const uint16_t *__restrict__ l2, int n,
+                                                      int n_pad, int r, int gr, int rblocks,
+                                                      uint8_t *__restrict__ codes,
+                                                      uint16_t *__restrict__ scales) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (int64_t)n_pad * rblocks) return;
+  const int rb = (int)(t % rblocks);
+  const int col = (int)(t / rblocks);
+  const bool present = col < n;
+  uint32_t w[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  // groups of gr ranks inside this 64-rank block (gr is 64 or r < 64)
+  const int j0 = rb * 64;
+  const int jend = r < j0 + 64 ? r : j0 + 64;
+  for (int jg = j0; jg < jend; jg += gr) {
+    uint32_t part[8];
+    uint16_t s16;
+    const uint16_t *p = present ? l2 + (int64_t)jg * n + col : l2;
+    quantize_group_strided(p, n, gr, present, part, s16);
+    const int w0 = (jg - j0) / 8;
+    for (int i = 0; i < gr / 8; i++) w[w0 + i] = part[i];
+    scales[(int64_t)(jg / gr) * n_pad + col] = s16;
+  }
+  uint8_t *blk = codes + ((int64_t)(col >> 5) * rblocks + rb) * 1024;
+  const int c = col & 31;
+  *reinterpret_cast<u32x4 *>(blk + c * 16) = u32x4{w[0], w[1], w[2], w[3]};
+  *reinterpret_cast<u32x4 *>(blk + (32 + c) * 16) = u32x4{w[4], w[5], w[6], w[7]};
+}
+
+static unsigned nblocks(int64_t threads) { return (unsigned)((threads + 255) / 256); }
+
+hipError_t launch_pack(const Geometry &g, const uint16_t *w, const uint16_t *l1,
+                       const uint16_t *l2, uint8_t *packed, hipStream_t s) {
+  const int kg = g.k / kGroup;
+  hipLaunchKernelGGL(pack_kgroups_kernel, dim3(nblocks((int64_t)g.n_pad * kg)), dim3(256), 0, s,
+                     w, (int64_t)g.k, (int64_t)1, g.n, g.n_pad, kg, packed + g.off_w,
+                     reinterpret_cast<uint16_t *>(packed + g.off_ws));
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || g.r == 0) return e;
+  hipLaunchKernelGGL(pack_kgroups_kernel, dim3(nblocks((int64_t)g.r_pad32 * kg)), dim3(256), 0,
+                     s, l1, (int64_t)1, (int64_t)g.r, g.r, g.r_pad32, kg, packed + g.off_l1,
+                     reinterpret_cast<uint16_t *>(packed + g.off_l1s));
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int rblocks = g.r_pad64 / 64;
+  hipLaunchKernelGGL(pack_l2_kernel, dim3(nblocks((int64_t)g.n_pad * rblocks)), dim3(256), 0, s,
+                     l2, g.n, g.n_pad, g.r, g.gr, rblocks, packed + g.off_l2,
+                     reinterpret_cast<uint16_t *>(packed + g.off_l2s));
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Export to the canonical layout (tests / debugging).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void export_kgroups_kernel(const uint8_t *__restrict__ codes,
+                                                             const uint16_t *__restrict__ scales,
+                                                             int nvec, int nvec_pad, int kgroups,
+                                                             uint32_t *__restrict__ out_c,
+                                                             uint16_t *__restrict__ out_s) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (int64_t)nvec * kgroups) return;
+  const int g = (int)(t % kgroups);
+  const int v = (int)(t / kgroups);
+  const uint8_t *blk = codes + ((int64_t)(v >> 5) * kgroups + g) * 1024;
+  const int c = v & 31;
+  const u32x4 a = *reinterpret_cast<const u32x4 *>(blk + c * 16);
+  const u32x4 b = *reinterpret_cast<const u32x4 *>(blk + (32 + c) * 16);
+  uint32_t *o = out_c + (int64_t)v * kgroups * 8 + g * 8;
+  o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w;
+  o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
+  out_s[(int64_t)v * kgroups + g] = scales[(int64_t)g * nvec_pad + v];
+}
+
+__global__ __launch_bounds__(256) void export_l2_kernel(const uint8_t *__restrict__ codes,
+                                                        const uint16_t *__restrict__ scales, int n,
+                                                        int n_pad, int r, int gr, int rblocks,
+                                                        uint32_t *__restrict__ out_c,
+                                                        uint16_t *__restrict__ out_s) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (int64_t)n * rblocks) return;
+  const int rb = (int)(t % rblocks);
+  const int col = (int)(t / rblocks);
+  const uint8_t *blk = codes + ((int64_t)(col >> 5) * rblocks + rb) * 1024;
+  const int c = col & 31;
+  const u32x4 a = *reinterpret_cast<const u32x4 *>(blk + c * 16);
+  const u32x4 b = *reinterpret_cast<const u32x4 *>(blk + (32 + c) * 16);
+  const uint32_t w[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+  const int j0 = rb * 64;
+  const int words = ((r < j0 + 64 ? r : j0 + 64) - j0) / 8;
+  uint32_t *o = out_c + (int64_t)col * (r / 8) + j0 / 8;
+  for (int i = 0; i < words; i++) o[i] = w[i];
+  const int ng = r / gr;
+  for (int jg = j0; jg < j0 + words * 8; jg += gr)
+    out_s[(int64_t)col * ng + jg / gr] = scales[(int64_t)(jg / gr) * n_pad + col];
+}
+
+hipError_t launch_export(const Geometry &g, const uint8_t *packed, uint32_t *wc, uint16_t *ws,
+                         uint32_t *l1c, uint16_t *l1s, uint32_t *l2c, uint16_t *l2s,
+                         hipStream_t s) {
+  const int kg = g.k / kGroup;
+  hipLaunchKernelGGL(export_kgroups_kernel, dim3(nblocks((int64_t)g.n * kg)), dim3(256), 0, s,
+                     packed + g.off_w, reinterpret_cast<const uint16_t *>(packed + g.off_ws), g.n,
+                     g.n_pad, kg, wc, ws);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || g.r == 0) return e;
+  hipLaunchKernelGGL(export_kgroups_kernel, dim3(nblocks((int64_t)g.r * kg)), dim3(256), 0, s,
+                     packed + g.off_l1, reinterpret_cast<const uint16_t *>(packed + g.off_l1s),
+                     g.r, g.r_pad32, kg, l1c, l1s);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int rblocks = g.r_pad64 / 64;
+  hipLaunchKernelGGL(export_l2_kernel, dim3(nblocks((int64_t)g.n * rblocks)), dim3(256), 0, s,
+                     packed + g.off_l2, reinterpret_cast<const uint16_t *>(packed + g.off_l2s),
+                     g.n, g.n_pad, g.r, g.gr, rblocks, l2c, l2s);
+  return hipGetLastError();
+}
+
+}  // namespace tq

@@ -1,0 +1,121 @@
+"""CPU tests of the C ABI: the library loads, exports every declared entry
+point, and validates arguments on the host without touching a GPU."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2606_01556_amd as tq
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_symbols():
+    src = open(os.path.join(ROOT, "include", "tq.h")).read()
+    return sorted(set(re.findall(r"\b(tq_[a-z_0-9]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(tq.LIB_PATH):
+        from paper_2606_01556_amd import build
+        build.build()
+    return tq.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    syms = declared_symbols()
+    assert set(syms) == set(tq.EXPORTS)
+    for s in syms:
+        assert hasattr(L, s), s
+
+
+def test_status_strings(L):
+    for code in range(0, 9):
+        assert L.tq_status_string(code)
+    assert L.tq_status_string(1234) == b"unknown status"
+
+
+@pytest.mark.parametrize("n,k,r,g,code", [
+    (512, 512, 16, 64, 0), (4096, 4096, 64, 64, 0), (100, 64, 0, 64, 0), (1, 64, 128, 64, 0),
+    (512, 512, 16, 128, 3), (512, 500, 16, 64, 3), (0, 512, 16, 64, 2), (512, 0, 16, 64, 2),
+    (512, 512, 24, 64, 4), (512, 512, 256, 64, 4), (512, 512, -8, 64, 4),
+])
+def test_desc_init_validation(L, n, k, r, g, code):
+    d = tq.WeightDesc()
+    assert L.tq_weight_desc_init(n, k, r, g, ctypes.byref(d)) == code
+
+
+def test_desc_init_null(L):
+    assert L.tq_weight_desc_init(64, 64, 0, 64, None) == 1
+
+
+def test_desc_sizes(L):
+    d = tq.weight_desc_init(4096, 4096, 64)
+    assert d.n_pad == 4096 and d.r_pad32 == 64 and d.r_pad64 == 64 and d.group_r == 64
+    # codes: n*k/2 + scales 2*n*k/64 + L1 codes k*r/2 + scales + L2 codes + scales
+    expect = 4096 * 4096 // 2 + 2 * 4096 * 64 + 4096 * 64 // 2 + 2 * 64 * 64 + 4096 * 64 // 2 + 2 * 4096
+    assert d.packed_bytes == expect
+    offs = [d.off_w, d.off_ws, d.off_l1, d.off_l1s, d.off_l2, d.off_l2s, d.packed_bytes]
+    assert offs == sorted(offs) and all(o % 256 == 0 for o in offs)
+    d2 = tq.weight_desc_init(100, 128, 16)
+    assert d2.n_pad == 128 and d2.r_pad32 == 32 and d2.r_pad64 == 64 and d2.group_r == 16
+
+
+FAKE = 1 << 20     # 16-byte aligned fake device address; never dereferenced
+
+
+def test_quant_act_validation(L):
+    assert L.tq_quant_act(None, 4, 64, 64, FAKE, FAKE, None) == 1
+    assert L.tq_quant_act(FAKE, 4, 64, 32, FAKE, FAKE, None) == 3
+    assert L.tq_quant_act(FAKE, 4, 100, 64, FAKE, FAKE, None) == 3
+    assert L.tq_quant_act(FAKE, -1, 64, 64, FAKE, FAKE, None) == 2
+    assert L.tq_quant_act(FAKE + 8, 4, 64, 64, FAKE, FAKE, None) == 6
+    assert L.tq_quant_act(FAKE, 0, 64, 64, FAKE, FAKE, None) == 0      # empty: no launch
+
+
+def test_dual_gemm_validation(L):
+    d = tq.weight_desc_init(128, 128, 16)
+    bad = tq.WeightDesc()
+    D = ctypes.byref
+    assert L.tq_dual_gemm(D(d), None, FAKE, FAKE, 4, FAKE, 0, None) == 1
+    assert L.tq_dual_gemm(D(bad), FAKE, FAKE, FAKE, 4, FAKE, 0, None) == 7
+    assert L.tq_dual_gemm(D(d), FAKE, FAKE, FAKE, 4, FAKE, 7, None) == 5
+    assert L.tq_dual_gemm(D(d), FAKE, FAKE, FAKE, -2, FAKE, 0, None) == 2
+    assert L.tq_dual_gemm(D(d), FAKE, FAKE + 4, FAKE, 4, FAKE, 0, None) == 6
+    assert L.tq_dual_gemm(D(d), FAKE, FAKE, FAKE, 0, FAKE, 0, None) == 0
+    d0 = tq.weight_desc_init(128, 128, 0)
+    assert L.tq_dual_gemm_debug(D(d0), FAKE, FAKE, FAKE, 4, FAKE, 0, FAKE, FAKE, FAKE, None) == 4
+    assert L.tq_dual_gemm_debug(D(d), FAKE, FAKE, FAKE, 4, FAKE, 0, None, FAKE, FAKE, None) == 1
+    # a descriptor edited after init is rejected
+    d3 = tq.weight_desc_init(128, 128, 16)
+    d3.n_pad = 64
+    assert L.tq_dual_gemm(D(d3), FAKE, FAKE, FAKE, 4, FAKE, 0, None) == 7
+
+
+def test_pack_export_validation(L):
+    d = tq.weight_desc_init(128, 128, 16)
+    D = ctypes.byref
+    assert L.tq_pack_weights(D(d), FAKE, None, FAKE, FAKE, None) == 1
+    assert L.tq_pack_weights(D(d), FAKE + 2, FAKE, FAKE, FAKE, None) == 6
+    assert L.tq_export_weights(D(d), FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, None) == 1
+    d0 = tq.weight_desc_init(128, 128, 0)
+    assert L.tq_export_weights(D(d0), FAKE, FAKE, FAKE + 1, None, None, None, None, None) == 6
+
+
+def test_tq4_roundtrip():
+    g = np.random.default_rng(0)
+    c = g.integers(-7, 8, size=(5, 64)).astype(np.int8)
+    w = tq.tq4_encode(c)
+    assert w.shape == (5, 8)
+    np.testing.assert_array_equal(tq.tq4_decode(w), c)
+    # the documented bit positions, spelled out for one word
+    one = np.array([[1, -2, 3, -4, 5, -6, 7, 0]], np.int8)
+    word = int(tq.tq4_encode(one)[0, 0])
+    assert word & 0x87 == 0x01
+    assert (word >> 8) & 0x87 == 0x82
+    assert (word >> 4) & 7 == 5 and (word >> 11) & 1 == 0      # c4 = +5, sign in bit 11
+    assert (word >> 12) & 7 == 6 and (word >> 19) & 1 == 1     # c5 = -6, sign in bit 19
+    assert (word >> 28) & 7 == 0 and (word >> 3) & 1 == 0      # c7 = 0, sign in bit 3

@@ -1,0 +1,241 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Bit-exact: activation codes and scales, weight codes and scales (via the
+canonical export), the on-chip low-rank intermediate H, its scales s_H and
+codes Q_H, and -- because every kernel accumulates each output in the same
+ascending-group fma order as the oracle -- the rounded output Y itself.  The
+spec tolerance (relative Frobenius 1e-3, max-abs 1e-2 * rms(Y)) is
+checked as well, against the oracle's fp64 result.
+"""
+import numpy as np
+import pytest
+
+import paper_2606_01556_amd as tq
+from tq_synth import GROUP, WORKLOADS, layer_inputs, random_codes_layer
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+REL_FRO = 1e-3
+MAX_ABS_RMS = 1e-2
+# bf16 output: its unit roundoff (2^-9) is 8x that of fp16 (2^-12), and the
+# rounding of the output alone reaches ~1.1e-3 relative Frobenius error, so the
+# fp16 bounds are scaled by 8 for bf16 results.
+BF16_FACTOR = 8.0
+
+
+def say(*a):
+    print("[case]", *a, flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    tq.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def run_gpu(X, W, L1, L2, bf16=False, debug=True):
+    M, K = X.shape
+    N = W.shape[0]
+    r = 0 if L1 is None else L1.shape[1]
+    lay = tq.Layer(dev(W), None if L1 is None else dev(L1), None if L2 is None else dev(L2))
+    d = lay.desc
+    xd = dev(X)
+    xc, xs = tq.empty_act(M, K)
+    tq.quant_act(xd, xc, xs)
+    y = torch.empty((M, N), dtype=torch.bfloat16 if bf16 else torch.float16, device="cuda")
+    out = {}
+    if r and debug:
+        h = torch.empty((M, r), dtype=torch.float32, device="cuda")
+        sh = torch.empty((M, r // d.group_r), dtype=torch.float32, device="cuda")
+        qh = torch.empty((M, r), dtype=torch.int8, device="cuda")
+        tq.dual_gemm_debug(d, lay.packed, xc, xs, M, y, h, sh, qh, bf16)
+        out.update(H=h, sH=sh, qH=qh)
+    else:
+        tq.dual_gemm(d, lay.packed, xc, xs, M, y, bf16)
+    wc = torch.empty((N, K // 8), dtype=torch.int32, device="cuda")
+    ws = torch.empty((N, K // GROUP), dtype=torch.float16, device="cuda")
+    ex = [wc, ws]
+    if r:
+        l1c = torch.empty((r, K // 8), dtype=torch.int32, device="cuda")
+        l1s = torch.empty((r, K // GROUP), dtype=torch.float16, device="cuda")
+        l2c = torch.empty((N, r // 8), dtype=torch.int32, device="cuda")
+        l2s = torch.empty((N, r // d.group_r), dtype=torch.float16, device="cuda")
+        ex += [l1c, l1s, l2c, l2s]
+    tq.export_weights(d, lay.packed, *ex)
+    torch.cuda.synchronize()
+    out["xq"] = tq.tq4_decode(xc.cpu().numpy())
+    out["xs"] = xs.cpu().numpy()[:, :M].T.copy()
+    out["wq"] = tq.tq4_decode(wc.cpu().numpy())
+    out["ws"] = ws.cpu().numpy()
+    if r:
+        out["l1q"] = tq.tq4_decode(l1c.cpu().numpy()).T.copy()    # [K, r]
+        out["l1s"] = l1s.cpu().numpy().T.copy()                   # [K/G, r]
+        out["l2q"] = tq.tq4_decode(l2c.cpu().numpy()).T.copy()    # [r, N]
+        out["l2s"] = l2s.cpu().numpy().T.copy()                   # [r/Gr, N]
+    out["Y"] = y.float().cpu().numpy()
+    out["Ybits"] = y.view(torch.int16).cpu().numpy().view(np.uint16)
+    for k in ("H", "sH", "qH"):
+        if k in out:
+            out[k] = out[k].cpu().numpy()
+    return out
+
+
+def check_tolerance(Y, ref64, bf16=False):
+    f = BF16_FACTOR if bf16 else 1.0
+    err = Y.astype(np.float64) - ref64
+    rel = np.linalg.norm(err) / max(np.linalg.norm(ref64), 1e-300)
+    rms = np.sqrt(np.mean(ref64 ** 2))
+    assert rel <= f * REL_FRO, f"relative Frobenius error {rel:.3e}"
+    assert np.max(np.abs(err)) <= f * MAX_ABS_RMS * rms + 1e-30, "max-abs error"
+
+
+def full_parity(oracle_mod, X, W, L1, L2, bf16=False):
+    g = run_gpu(X, W, L1, L2, bf16)
+    o = oracle_mod.layer(X, W, L1, L2, GROUP)
+    qx, sx = oracle_mod.quantize(X, GROUP)
+    np.testing.assert_array_equal(g["xq"], qx)
+    np.testing.assert_array_equal(g["xs"].view(np.uint16), sx.view(np.uint16))
+    qw, sw = oracle_mod.quantize(W, GROUP)
+    np.testing.assert_array_equal(g["wq"], qw)
+    np.testing.assert_array_equal(g["ws"].view(np.uint16), sw.view(np.uint16))
+    if L1 is not None:
+        r = L1.shape[1]
+        q1, s1 = oracle_mod.quantize(L1, GROUP, axis=0)
+        np.testing.assert_array_equal(g["l1q"], q1)
+        np.testing.assert_array_equal(g["l1s"].view(np.uint16), s1.view(np.uint16))
+        q2, s2 = oracle_mod.quantize(L2, min(GROUP, r), axis=0)
+        np.testing.assert_array_equal(g["l2q"], q2)
+        np.testing.assert_array_equal(g["l2s"].view(np.uint16), s2.view(np.uint16))
+        np.testing.assert_array_equal(g["H"].view(np.uint32), o["H"].view(np.uint32))
+        np.testing.assert_array_equal(g["sH"].view(np.uint32), o["sH"].view(np.uint32))
+        np.testing.assert_array_equal(g["qH"], o["qH"])
+    if bf16:
+        np.testing.assert_array_equal(g["Ybits"], o["Ybf"])
+    else:
+        np.testing.assert_array_equal(g["Ybits"], o["Y16"].view(np.uint16))
+    check_tolerance(g["Y"], o["Y64"], bf16)
+    return g, o
+
+
+def test_tiny_workload(oracle_mod):
+    say("tiny M=16 K=512 N=512 r=16")
+    d = layer_inputs("tiny", 0, 16)
+    full_parity(oracle_mod, d["X"], d["W_res"], d["L1"], d["L2"])
+
+
+@pytest.mark.parametrize("M,K,N,r", [
+    (1, 64, 32, 8), (5, 128, 96, 16), (17, 192, 100, 32), (33, 256, 64, 64), (70, 128, 160, 128),
+    (130, 320, 288, 64), (257, 128, 40, 0), (3, 64, 8, 0), (16, 512, 256, 128), (200, 256, 512, 32),
+])
+def test_ragged_shapes(oracle_mod, M, K, N, r):
+    say(f"ragged M={M} K={K} N={N} r={r}")
+    d = random_codes_layer(M, K, N, r, seed=M + K + N + r)
+    full_parity(oracle_mod, d["X"], d["W_res"], d["L1"], d["L2"])
+
+
+@pytest.mark.parametrize("M", [4, 100])
+def test_bf16_output(oracle_mod, M):
+    say(f"bf16 M={M}")
+    d = random_codes_layer(M, 256, 96, 64, seed=3)
+    full_parity(oracle_mod, d["X"], d["W_res"], d["L1"], d["L2"], bf16=True)
+
+
+def test_zero_groups(oracle_mod):
+    say("zero groups")
+    d = random_codes_layer(40, 256, 64, 32, seed=5)
+    X = d["X"].copy()
+    X[3, :] = 0
+    X[7, 64:128] = 0
+    W = d["W_res"].copy()
+    W[5, 128:192] = 0
+    L1 = d["L1"].copy()
+    L1[:, 2] = 0
+    g, o = full_parity(oracle_mod, X, W, L1, d["L2"])
+    assert np.all(g["xq"][3] == 0) and np.all(g["xs"][3] == 0)
+    assert np.all(g["qH"][3] == 0) and np.all(g["sH"][3] == 0)
+
+
+def test_integer_accumulators_exact(oracle_mod):
+    """Every group max is 7, so all scales are 1 and Y is the exact integer sum
+    of the code products: the integer accumulators show through unrounded."""
+    say("integer-designed layer")
+    g0 = np.random.default_rng(7)
+    M, K, N, r = 48, 256, 96, 64
+    X = g0.integers(-7, 8, size=(M, K)).astype(np.float64)
+    W = g0.integers(-7, 8, size=(N, K)).astype(np.float64)
+    X[:, ::GROUP] = 7
+    W[:, 1::GROUP] = -7
+    L1 = np.zeros((K, r))
+    L1[0, :] = 7
+    L2 = np.zeros((r, N))
+    L2[0, :] = 7
+    X, W, L1, L2 = (a.astype(np.float16) for a in (X, W, L1, L2))
+    g, o = full_parity(oracle_mod, X, W, L1, L2)
+    Yint = X.astype(np.int64) @ W.astype(np.int64).T
+    H = X.astype(np.int64) @ L1.astype(np.int64)      # = 49 for every entry
+    assert np.all(g["H"] == H)
+    # Q_H = 49 / (49 / 7) = 7 everywhere; only rank 0 of L2 is non-zero (7)
+    np.testing.assert_array_equal(g["Y"].astype(np.float64),
+                                  (Yint + 7 * 7 * 7).astype(np.float16).astype(np.float64))
+
+
+def test_repeatable_bitwise(oracle_mod):
+    say("determinism")
+    d = random_codes_layer(64, 512, 256, 64, seed=11)
+    a = run_gpu(d["X"], d["W_res"], d["L1"], d["L2"], debug=False)
+    b = run_gpu(d["X"], d["W_res"], d["L1"], d["L2"], debug=False)
+    np.testing.assert_array_equal(a["Ybits"], b["Ybits"])
+
+
+# ------------------------------------------------------------------ full-size workloads
+def sampled_parity(oracle_mod, wl_name, layer_idx, M, rank=None, n_rows=6, n_cols=192):
+    d = layer_inputs(wl_name, layer_idx, M, rank=rank)
+    X, W, L1, L2 = d["X"], d["W_res"], d["L1"], d["L2"]
+    N = W.shape[0]
+    g = run_gpu(X, W, L1, L2)
+    rng = np.random.default_rng(M + N)
+    rows = np.unique(np.concatenate([[0, M - 1], rng.integers(0, M, n_rows)]))
+    cols = np.unique(np.concatenate([[0, N - 1], rng.integers(0, N, n_cols)]))
+    o = oracle_mod.layer(X, W, L1, L2, GROUP, rows=rows, cols=cols)
+    np.testing.assert_array_equal(g["Ybits"][np.ix_(rows, cols)], o["Y16"].view(np.uint16))
+    check_tolerance(g["Y"][np.ix_(rows, cols)], o["Y64"])
+    if L1 is not None:
+        np.testing.assert_array_equal(g["qH"][rows], o["qH"])
+        np.testing.assert_array_equal(g["sH"][rows].view(np.uint32), o["sH"].view(np.uint32))
+    # the rows the oracle did not see: finite and of the right scale
+    assert np.all(np.isfinite(g["Y"]))
+
+
+@pytest.mark.parametrize("M", WORKLOADS["llama3-8b-qo"].Ms)
+def test_llama3_8b_qo(oracle_mod, M):
+    say(f"llama3-8b q_proj M={M}")
+    sampled_parity(oracle_mod, "llama3-8b-qo", 0, M)
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("li,M", [(0, 1), (0, 16), (0, 4096), (1, 1), (1, 16), (1, 4096)])
+def test_llama3_8b_mlp(oracle_mod, li, M):
+    say(f"llama3-8b mlp layer={li} M={M}")
+    sampled_parity(oracle_mod, "llama3-8b-mlp", li, M)
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("li,M", [(0, 1), (0, 256), (0, 4096), (4, 256), (5, 1), (8, 4096)])
+def test_qwen3_8b(oracle_mod, li, M):
+    say(f"qwen3-8b layer={li} M={M}")
+    sampled_parity(oracle_mod, "qwen3-8b", li, M)
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("li,M", [(0, 1), (0, 32), (1, 8192)])
+def test_llama3_70b(oracle_mod, li, M):
+    say(f"llama3-70b layer={li} M={M}")
+    sampled_parity(oracle_mod, "llama3-70b", li, M)
