@@ -102,9 +102,10 @@ tq_status tq_pack_weights(const tq_weight_desc *d, const void *w_res, const void
  * activation is quantized once and shared by both branches).
  *   x         [m,k] fp16 row-major, m >= 0, k % group == 0, group == 64
  *   x_codes   [m, k/8] TQ4 code words (m*k/2 bytes), row-major
- *   x_scales  [k/group, m] fp16: the scale of token i, group g is
- *             x_scales[g*m + i] (group-major, so one group's scales of a
- *             token tile are contiguous)
+ *   x_scales  [k/group, m8] fp16 with m8 = m rounded up to a multiple of 8:
+ *             the scale of token i, group g is x_scales[g*m8 + i]
+ *             (group-major, so one group's scales of a token tile are
+ *             contiguous and 16-byte aligned); entries i in [m, m8) are 0
  * m == 0 is a no-op.  Errors: TQ_ERR_NULL, TQ_ERR_SHAPE, TQ_ERR_GROUP,
  * TQ_ERR_ALIGN, TQ_ERR_HIP. */
 tq_status tq_quant_act(const void *x, int m, int k, int group, void *x_codes,

@@ -133,11 +133,16 @@ def empty_packed(desc: WeightDesc, device="cuda"):
     return torch.empty(int(desc.packed_bytes), dtype=torch.uint8, device=device)
 
 
+def scale_stride(m: int) -> int:
+    """Row stride of x_scales: the token count rounded up to a multiple of 8."""
+    return (m + 7) // 8 * 8
+
+
 def empty_act(m: int, k: int, device="cuda"):
-    """(x_codes [m, k/8] int32 TQ4 words, x_scales [k/64, m] fp16)."""
+    """(x_codes [m, k/8] int32 TQ4 words, x_scales [k/64, m8] fp16, m8 = scale_stride(m))."""
     import torch
     return (torch.empty((m, k // 8), dtype=torch.int32, device=device),
-            torch.empty((k // GROUP, max(m, 1)), dtype=torch.float16, device=device))
+            torch.empty((k // GROUP, max(scale_stride(m), 8)), dtype=torch.float16, device=device))
 
 
 class Layer:

@@ -1,64 +1,346 @@
-// Fused dual-component W4A4 layer (paper Sec. 4.3): one kernel computes the
-// residual 4-bit GEMM and the two-stage low-rank branch over the same
-// quantized activation tile, keeps the low-rank intermediate H on chip,
-// re-quantizes it on the fly, and merges both branches in one epilogue.
+// Fused dual-component W4A4 layer (paper Sec. 4.3) for m > 16 tokens: one
+// kernel computes the residual 4-bit GEMM and the two-stage low-rank branch
+// over the same quantized activation tile, keeps the low-rank intermediate H
+// on chip, re-quantizes it on the fly, and merges both branches in one
+// epilogue.
 //
-// Work decomposition (one workgroup = 4 wavefronts, one per SIMD):
+// Work decomposition (one workgroup = 4 wavefronts in a 2x2 grid):
 //  * a workgroup owns BM tokens and a run of consecutive BN-column tiles;
 //  * during the K loop of its first column tile it also accumulates the
 //    stage-1 product H = Q(X) Q(L1) for its BM tokens (all r ranks), then
 //    re-quantizes H into LDS; later column tiles reuse Q_H and s_H from LDS,
 //    so H is formed once per workgroup and never leaves the chip;
-//  * per 64-wide K group, 16-byte slices of packed codes are staged through
-//    double-buffered LDS in matrix-core fragment order, expanded to fp8 with
-//    three bit operations per 8 codes, and multiplied exactly on the matrix
-//    cores (v_mfma_scale_f32_32x32x64_f8f6f4); the exact integer group sums
-//    are scaled by s_x * s_w and accumulated with one fma per group, in
-//    ascending group order (the same order for H, whose codes depend on it).
+//  * K runs in groups of 64.  A 3-deep LDS ring is filled by direct
+//    global->LDS loads (global_load_lds_dwordx4, each wavefront a fixed set
+//    planned once per tile) two groups ahead of use, one workgroup barrier
+//    per group; packed codes arrive in matrix-core fragment order and are
+//    expanded to fp8 with three bit operations per 8 codes;
+//  * per 32x32 output tile and group: one exact fp8 product of codes
+//    (v_mfma_scale_f32_32x32x64_f8f6f4), one fp16 matrix-core outer product
+//    s_x (x) s_w (exact in fp32) and one fma per output, in ascending group
+//    order -- the same order for H, whose codes depend on it.
+#include <stdio.h>
+#include <stdlib.h>
+
 #include "tq_device.hpp"
 #include "tq_kernels.hpp"
 
 namespace tq {
 
-template <int WM, int WN, int TM, int TN, int RT>
+typedef _Float16 v4h __attribute__((ext_vector_type(4)));
+
+// Direct global -> LDS loads (LDS DMA) of 16 / 4 / 2 bytes per lane: the
+// data of a wavefront lands in lane order at the LDS address in M0
+// (wave-uniform), 16 bytes per lane for dwordx4 and 4 bytes per lane for
+// dword and ushort (a 2-byte value occupies the low half of its dword).  Written as inline asm so that the compiler does not
+// guard every LDS access with a full vmcnt(0) wait; the kernel waits for its
+// own loads explicitly (in-order completion, a fixed number per stage).
+__device__ __forceinline__ uint32_t lds_addr(const void *p) {
+  return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)p);
+}
+__device__ __forceinline__ void g2l_16(const void *g, void *lds) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds_addr(lds)), "v"(g)
+               : "memory");
+}
+__device__ __forceinline__ void g2l_4(const void *g, void *lds) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off" ::"s"(lds_addr(lds)), "v"(g)
+               : "memory");
+}
+__device__ __forceinline__ void g2l_2(const void *g, void *lds) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_ushort %1, off" ::"s"(lds_addr(lds)), "v"(g)
+               : "memory");
+}
+
+// exact fp32 outer product of two 32-vectors of fp16 scales, laid out like
+// a 32x32 matrix-core result: operand lanes 0-31 carry the values in k = 0.
+__device__ __forceinline__ v16f outer32(v4h a, v4h b) {
+  const v16f z = {0};
+  return __builtin_amdgcn_mfma_f32_32x32x8f16(a, b, z, 0, 0, 0);
+}
+
+template <int TM, int TN, int RT>
 struct TileCfg {
-  static_assert(WM * WN == 4, "four wavefronts per workgroup");
+  static constexpr int WM = 2, WN = 2;
   static constexpr int BM = WM * TM * 32;
   static constexpr int BN = WN * TN * 32;
-  static constexpr int A_CH = BM * 2;        // 16-byte chunks of one K group
-  static constexpr int B_CH = BN * 2;
-  static constexpr int L_CH = RT * 64;
-  static constexpr int RB = (RT + 1) / 2;    // 64-rank blocks (= rank groups)
-  static constexpr int HT = (RT + WN - 1) / WN;  // H column tiles per wave
-  // LDS layout of one pipeline stage
+  static constexpr int RB = (RT + 1) / 2;        // 64-rank blocks (= rank groups)
+  static constexpr int HT = (RT + WN - 1) / WN;  // H column tiles per wavefront
+  static constexpr int STAGES = 4;   // ring slots; loads run 3 groups ahead
+  // one LDS stage: code blocks of 1 KiB in fragment order (A, B, L1), the
+  // group's fp16 scales (s_x[BM], s_w[BN], s_L1[32*RT]) in one 1 KiB block,
+  // and a dummy block that absorbs padding loads
+  static constexpr int NA = BM / 32, NB = BN / 32;
+  static_assert(BM + BN + 32 * RT <= 512, "one wavefront load carries all scales of a group");
+  static_assert(RT <= 1 || RT % WN == 0, "rank tiles spread evenly over the wavefront columns");
   static constexpr int OFF_A = 0;
-  static constexpr int OFF_B = OFF_A + A_CH * 16;
-  static constexpr int OFF_L = OFF_B + B_CH * 16;
-  static constexpr int OFF_SX = OFF_L + L_CH * 16;
-  static constexpr int OFF_SW = OFF_SX + BM * 4;
-  static constexpr int OFF_SL = OFF_SW + BN * 4;
-  static constexpr int STAGE = OFF_SL + RT * 32 * 4;
-  // after the first K loop the stage buffers hold H in fp32
+  static constexpr int OFF_B = OFF_A + NA * 1024;
+  static constexpr int OFF_L = OFF_B + NB * 1024;
+  static constexpr int OFF_S = OFF_L + RT * 1024;
+  static constexpr int OFF_D = OFF_S + 1024;
+  static constexpr int STAGE = OFF_D + 1024;
+  // 16-byte wavefront loads per stage, padded to a multiple of 4 wavefronts
+  static constexpr int LOADS_H = NA + NB + RT + 1;
+  static constexpr int LOADS_R = NA + NB + 1;
+  static constexpr int NL_H = (LOADS_H + 3) / 4;   // per wavefront, with H
+  static constexpr int NL_R = (LOADS_R + 3) / 4;   // per wavefront, residual only
+  static constexpr int NL_MAX = NL_H > NL_R ? NL_H : NL_R;
+  // after the first K loop the ring holds H in fp32
   static constexpr int HSTR = RT * 32 + 1;
   static constexpr int H_BYTES = RT > 0 ? BM * HSTR * 4 : 0;
-  static constexpr int UNION = (2 * STAGE > H_BYTES ? 2 * STAGE : H_BYTES);
-  static constexpr int QSTR = RB * 64 + 16;  // bytes per token row of Q_H (fp8)
+  static constexpr int RING = STAGES * STAGE;
+  static constexpr int UNION = RING > H_BYTES ? RING : H_BYTES;
+  static constexpr int QSTR = RB * 64 + 16;       // bytes per token row of Q_H (fp8)
   static constexpr int OFF_Q = (UNION + 15) / 16 * 16;
   static constexpr int OFF_SH = OFF_Q + (RT > 0 ? BM * QSTR : 0);
   static constexpr int LDS = OFF_SH + (RT > 0 ? BM * RB * 4 : 0);
 };
 
-template <int WM, int WN, int TM, int TN, int RT>
+template <int TM, int TN, int RT>
+struct TileKernel {
+  using C = TileCfg<TM, TN, RT>;
+
+  struct Ctx {
+    uint8_t *smem;
+    int lane, wy, wx, KG;
+  };
+
+  // This wavefront's share of the loads of one stage: slot i (global slot
+  // index wave + 4 i) reads 16 bytes per lane from base[i] + g * inc[i] for
+  // group g into stage offset off[i].  Computed once per column tile, so the
+  // K loop issues every load with one 64-bit multiply-add.
+  struct Loads {
+    const uint8_t *base[C::NL_MAX];
+    uint32_t inc[C::NL_MAX];
+    uint32_t off[C::NL_MAX];
+  };
+
+  template <bool H>
+  __device__ static void plan(const GemmArgs &a, int wave, int lane, int m0, int n0, Loads &L) {
+    const Geometry &geo = a.geo;
+    const int KG = geo.k / kGroup;
+    const int m = a.m;
+    const int ctiles = geo.n_pad / 32;
+    const uint8_t *xc = reinterpret_cast<const uint8_t *>(a.xc);
+    const uint8_t *xs = reinterpret_cast<const uint8_t *>(a.xs);
+    const uint8_t *wcodes = a.packed + geo.off_w;
+    const uint8_t *wscales = a.packed + geo.off_ws;
+    const uint8_t *l1codes = a.packed + geo.off_l1;
+    const uint8_t *l1scales = a.packed + geo.off_l1s;
+    const int64_t xrow_bytes = geo.k / 2;
+    // activation codes of row min(m0 + 32 s + lane % 32, m - 1), k half lane / 32
+    auto a_block = [&](int s, const uint8_t *&b, uint32_t &inc) {
+      const int row = min(m0 + s * 32 + (lane & 31), m - 1);
+      b = xc + row * xrow_bytes + (lane >> 5) * 16;
+      inc = 32;
+    };
+    constexpr int NL = H ? C::NL_H : C::NL_R;
+#pragma unroll
+    for (int i = 0; i < NL; i++) {
+      int s = wave + 4 * i;
+      if (s < C::NA) {
+        a_block(s, L.base[i], L.inc[i]);
+        L.off[i] = C::OFF_A + s * 1024;
+        continue;
+      }
+      s -= C::NA;
+      if (s < C::NB) {                         // residual weight block
+        const int ct = min(n0 / 32 + s, ctiles - 1);
+        L.base[i] = wcodes + ((int64_t)ct * KG * 64 + lane) * 16;
+        L.inc[i] = 1024;
+        L.off[i] = C::OFF_B + s * 1024;
+        continue;
+      }
+      s -= C::NB;
+      if (H && s < RT) {                       // stage-1 weight block
+        L.base[i] = l1codes + ((int64_t)s * KG * 64 + lane) * 16;
+        L.inc[i] = 1024;
+        L.off[i] = C::OFF_L + s * 1024;
+        continue;
+      }
+      if (H) s -= RT;
+      if (s == 0) {                            // all scales of the group
+        constexpr int LX = C::BM / 8, LW = C::BN / 8, LL = H ? RT * 4 : 0;
+        if (lane < LX) {
+          L.base[i] = xs + (int64_t)m0 * 2 + lane * 16;
+          L.inc[i] = a.ms * 2;
+        } else if (lane < LX + LW) {
+          const int col = min(n0 + (lane - LX) * 8, geo.n_pad - 8);
+          L.base[i] = wscales + (int64_t)col * 2;
+          L.inc[i] = geo.n_pad * 2;
+        } else if (lane < LX + LW + LL) {
+          L.base[i] = l1scales + (int64_t)(lane - LX - LW) * 16;
+          L.inc[i] = RT * 32 * 2;
+        } else {                               // unused lanes: a valid duplicate
+          L.base[i] = xs + (int64_t)m0 * 2;
+          L.inc[i] = a.ms * 2;
+        }
+        L.off[i] = C::OFF_S;
+        continue;
+      }
+      a_block(0, L.base[i], L.inc[i]);          // padding load
+      L.off[i] = C::OFF_D;
+    }
+  }
+
+  template <bool H>
+  __device__ static void issue(const Ctx &c, const Loads &L, int g, int slot) {
+    uint8_t *st = c.smem + slot * C::STAGE;
+    constexpr int NL = H ? C::NL_H : C::NL_R;
+#pragma unroll
+    for (int i = 0; i < NL; i++) g2l_16(L.base[i] + (uint64_t)g * L.inc[i], st + L.off[i]);
+  }
+
+  // s_waitcnt vmcnt(n) with expcnt / lgkmcnt left alone; n is the number of
+  // this wavefront's loads that may still be in flight
+  template <int N>
+  __device__ static void wait_vm() {
+    static_assert(N < 64, "vmcnt has 6 bits");
+    // s_waitcnt: vmcnt in bits [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8]
+    __builtin_amdgcn_s_waitcnt((N & 0xf) | ((N >> 4) << 14) | (0x7 << 4) | (0xf << 8));
+    asm volatile("" ::: "memory");
+  }
+
+  // scale operand of the outer product: lanes 0-31 carry s[idx] in k = 0
+  // (the load is unconditional, the select branch-free)
+  __device__ static v4h scale_operand(const uint16_t *s, int idx, int lane) {
+    const uint16_t raw = s[idx];
+    const _Float16 v = __builtin_bit_cast(_Float16, (uint16_t)(lane < 32 ? raw : 0));
+    return v4h{v, (_Float16)0, (_Float16)0, (_Float16)0};
+  }
+
+  // matrix-core operands of one K group for this wavefront
+  struct Frags {
+    v8i af[TM], bf[TN], lf[C::HT > 0 ? C::HT : 1];
+    v4h pa[TM], pb[TN], pl[C::HT > 0 ? C::HT : 1];
+  };
+
+  template <bool H>
+  __device__ static void read_frags(const Ctx &c, int slot, Frags &F) {
+    const uint8_t *st = c.smem + slot * C::STAGE;
+    const uint16_t *sx = reinterpret_cast<const uint16_t *>(st + C::OFF_S);
+    const uint16_t *sw = sx + C::BM;
+#pragma unroll
+    for (int i = 0; i < TM; i++) {
+      const int ti = c.wy * TM + i;
+      F.af[i] = unpack32(*reinterpret_cast<const u32x4 *>(st + C::OFF_A + (ti * 64 + c.lane) * 16));
+      F.pa[i] = scale_operand(sx, ti * 32 + (c.lane & 31), c.lane);
+    }
+#pragma unroll
+    for (int j = 0; j < TN; j++) {
+      const int tj = c.wx * TN + j;
+      F.bf[j] = unpack32(*reinterpret_cast<const u32x4 *>(st + C::OFF_B + (tj * 64 + c.lane) * 16));
+      F.pb[j] = scale_operand(sw, tj * 32 + (c.lane & 31), c.lane);
+    }
+    if constexpr (H && RT > 0) {
+      // H tiles of this wavefront: rank tiles rt = wx + WN h (clamped for the
+      // wavefronts without one when RT = 1; their results are never used)
+      const uint16_t *sl = sw + C::BN;
+#pragma unroll
+      for (int h = 0; h < C::HT; h++) {
+        const int rt = min(c.wx + h * C::WN, RT - 1);
+        F.lf[h] = unpack32(*reinterpret_cast<const u32x4 *>(st + C::OFF_L + (rt * 64 + c.lane) * 16));
+        F.pl[h] = scale_operand(sl, rt * 32 + (c.lane & 31), c.lane);
+      }
+    }
+  }
+
+  // One iteration of the software-pipelined K loop for group g: wait for
+  // group g + 1 to land, barrier, start the loads of group g + 3, issue every
+  // matrix-core instruction of group g (exact code products and exact scale
+  // outer products, into distinct registers), then -- while the matrix core
+  // works -- read and expand the operands of group g + 1 from LDS into `nxt`,
+  // and finally apply the fmas of group g (ascending group order).
+  template <bool H>
+  __device__ static void k_step(const Ctx &c, const Loads &L, int g, const Frags &cur, Frags &nxt,
+                                v16f (&acc)[TM][TN], v16f (&hacc)[TM][C::HT > 0 ? C::HT : 1]) {
+    constexpr int NL = H ? C::NL_H : C::NL_R;
+    const int KG = c.KG;
+    // groups g, g + 1 and g + 2 may be in flight; g must have landed
+    if (g + 2 < KG) wait_vm<2 * NL>();
+    else if (g + 1 < KG) wait_vm<NL>();
+    else wait_vm<0>();
+    __syncthreads();
+    if (g + 3 < KG) issue<H>(c, L, g + 3, (g + 3) % C::STAGES);
+    v16f cg[TM][TN], pp[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; i++)
+#pragma unroll
+      for (int j = 0; j < TN; j++) {
+        cg[i][j] = mfma_codes_32x32x64(cur.af[i], cur.bf[j]);
+        pp[i][j] = outer32(cur.pa[i], cur.pb[j]);
+      }
+    __builtin_amdgcn_sched_barrier(0);
+    if (g + 1 < KG) read_frags<H>(c, (g + 1) % C::STAGES, nxt);
+#pragma unroll
+    for (int i = 0; i < TM; i++)
+#pragma unroll
+      for (int j = 0; j < TN; j++)
+#pragma unroll
+        for (int v = 0; v < 16; v++) acc[i][j][v] = fmaf(cg[i][j][v], pp[i][j][v], acc[i][j][v]);
+    if constexpr (H && RT > 0) {
+      if (c.wx < RT) {   // only wavefronts that own an H tile
+        v16f ch[TM][C::HT], ph[TM][C::HT];
+#pragma unroll
+        for (int h = 0; h < C::HT; h++)
+#pragma unroll
+          for (int i = 0; i < TM; i++) {
+            ch[i][h] = mfma_codes_32x32x64(cur.af[i], cur.lf[h]);
+            ph[i][h] = outer32(cur.pa[i], cur.pl[h]);
+          }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int h = 0; h < C::HT; h++)
+#pragma unroll
+          for (int i = 0; i < TM; i++)
+#pragma unroll
+            for (int v = 0; v < 16; v++) hacc[i][h][v] = fmaf(ch[i][h][v], ph[i][h][v], hacc[i][h][v]);
+      }
+    }
+  }
+
+  // K loop: a 4-slot LDS ring with loads 3 groups ahead, unrolled by two so
+  // the operand registers of consecutive groups ping-pong without copies.
+  template <bool H>
+  __device__ static void k_loop(const Ctx &c, const Loads &L, v16f (&acc)[TM][TN],
+                                v16f (&hacc)[TM][C::HT > 0 ? C::HT : 1]) {
+    constexpr int NL = H ? C::NL_H : C::NL_R;
+    const int KG = c.KG;
+    issue<H>(c, L, 0, 0);
+    if (KG > 1) issue<H>(c, L, 1, 1);
+    if (KG > 2) issue<H>(c, L, 2, 2);
+    if (KG > 2) wait_vm<2 * NL>();
+    else if (KG > 1) wait_vm<NL>();
+    else wait_vm<0>();
+    __syncthreads();
+    Frags F0, F1;
+    read_frags<H>(c, 0, F0);
+    for (int g = 0; g < KG; g += 2) {
+      k_step<H>(c, L, g, F0, F1, acc, hacc);
+      if (g + 1 < KG) k_step<H>(c, L, g + 1, F1, F0, acc, hacc);
+    }
+    __syncthreads();   // every wavefront is done with the ring
+  }
+};
+
+template <int TM, int TN, int RT>
 __global__ __launch_bounds__(256, 1) void dual_gemm_tile_kernel(GemmArgs a, int m_tiles,
                                                                 int n_tiles, int tiles_per_wg) {
-  using C = TileCfg<WM, WN, TM, TN, RT>;
-  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wy = wave / WN, wx = wave % WN;
+  using K_ = TileKernel<TM, TN, RT>;
+  using C = typename K_::C;
+  extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wy = wave / C::WN, wx = wave % C::WN;
   const Geometry &geo = a.geo;
-  const int KG = geo.k / kGroup;
-  const int m = a.m;
+  typename K_::Ctx c;
+  c.smem = smem;
+  c.lane = lane;
+  c.wy = wy;
+  c.wx = wx;
+  c.KG = geo.k / kGroup;
   const int ctiles = geo.n_pad / 32;
+  const uint8_t *l2codes = a.packed + geo.off_l2;
+  const uint16_t *l2scales = reinterpret_cast<const uint16_t *>(a.packed + geo.off_l2s);
 
   // Workgroups are dispatched round-robin over the 8 XCDs; give each XCD a
   // contiguous range of logical ids so that workgroups sharing weight columns
@@ -71,24 +353,14 @@ __global__ __launch_bounds__(256, 1) void dual_gemm_tile_kernel(GemmArgs a, int 
   }
   const int m_tile = logical % m_tiles;
   const int chunk = logical / m_tiles;
-  const int m0 = m_tile * C::BM;
+  const int m0 = m_tile * C::BM, m = a.m;
   const int t_begin = chunk * tiles_per_wg;
   const int t_end = min(t_begin + tiles_per_wg, n_tiles);
-
-  const uint8_t *wcodes = a.packed + geo.off_w;
-  const uint16_t *wscales = reinterpret_cast<const uint16_t *>(a.packed + geo.off_ws);
-  const uint8_t *l1codes = a.packed + geo.off_l1;
-  const uint16_t *l1scales = reinterpret_cast<const uint16_t *>(a.packed + geo.off_l1s);
-  const uint8_t *l2codes = a.packed + geo.off_l2;
-  const uint16_t *l2scales = reinterpret_cast<const uint16_t *>(a.packed + geo.off_l2s);
-  const int64_t xwords = geo.k / 8;
-
-  constexpr int A_PER = (C::A_CH + 255) / 256;
-  constexpr int B_PER = (C::B_CH + 255) / 256;
 
   for (int t = t_begin; t < t_end; t++) {
     const int n0 = t * C::BN;
     const bool do_h = (RT > 0) && (t == t_begin);
+    __builtin_amdgcn_s_waitcnt((0x7 << 4) | (0xf << 8));   // drain earlier stores (vmcnt(0))
 
     v16f acc[TM][TN];
     v16f hacc[TM][C::HT > 0 ? C::HT : 1];
@@ -99,124 +371,13 @@ __global__ __launch_bounds__(256, 1) void dual_gemm_tile_kernel(GemmArgs a, int 
 #pragma unroll
       for (int h = 0; h < (C::HT > 0 ? C::HT : 1); h++) hacc[i][h] = v16f{0};
     }
-
-    // ---- global -> register staging of one K group ----
-    u32x4 ra[A_PER], rb[B_PER], rl = {0, 0, 0, 0};
-    uint16_t rsx = 0, rsw[(C::BN + 255) / 256], rsl = 0;
-    auto load_group = [&](int g) {
-#pragma unroll
-      for (int p = 0; p < A_PER; p++) {
-        const int c = tid + p * 256;
-        ra[p] = u32x4{0, 0, 0, 0};
-        if (c < C::A_CH) {
-          const int row = m0 + (c >> 6) * 32 + (c & 31);
-          const int khalf = (c >> 5) & 1;
-          if (row < m)
-            ra[p] = *reinterpret_cast<const u32x4 *>(a.xc + row * xwords + g * 8 + khalf * 4);
-        }
-      }
-#pragma unroll
-      for (int p = 0; p < B_PER; p++) {
-        const int c = tid + p * 256;
-        rb[p] = u32x4{0, 0, 0, 0};
-        if (c < C::B_CH) {
-          const int ct = n0 / 32 + (c >> 6);
-          if (ct < ctiles)
-            rb[p] = *reinterpret_cast<const u32x4 *>(wcodes + (((int64_t)ct * KG + g) * 64 + (c & 63)) * 16);
-        }
-      }
-      if (do_h && tid < C::L_CH)
-        rl = *reinterpret_cast<const u32x4 *>(l1codes + (((int64_t)(tid >> 6) * KG + g) * 64 + (tid & 63)) * 16);
-      rsx = 0;
-      if (tid < C::BM && m0 + tid < m) rsx = a.xs[(int64_t)g * m + m0 + tid];
-#pragma unroll
-      for (int p = 0; p < (C::BN + 255) / 256; p++) {
-        const int j = tid + p * 256;
-        rsw[p] = 0;
-        if (j < C::BN && n0 + j < geo.n_pad) rsw[p] = wscales[(int64_t)g * geo.n_pad + n0 + j];
-      }
-      if (do_h && tid < RT * 32) rsl = l1scales[(int64_t)g * geo.r_pad32 + tid];
-    };
-    auto store_group = [&](int stage) {
-      uint8_t *st = smem + stage * C::STAGE;
-#pragma unroll
-      for (int p = 0; p < A_PER; p++) {
-        const int c = tid + p * 256;
-        if (c < C::A_CH) *reinterpret_cast<u32x4 *>(st + C::OFF_A + c * 16) = ra[p];
-      }
-#pragma unroll
-      for (int p = 0; p < B_PER; p++) {
-        const int c = tid + p * 256;
-        if (c < C::B_CH) *reinterpret_cast<u32x4 *>(st + C::OFF_B + c * 16) = rb[p];
-      }
-      if (do_h && tid < C::L_CH) *reinterpret_cast<u32x4 *>(st + C::OFF_L + tid * 16) = rl;
-      if (tid < C::BM) reinterpret_cast<float *>(st + C::OFF_SX)[tid] = half_bits_to_float(rsx);
-#pragma unroll
-      for (int p = 0; p < (C::BN + 255) / 256; p++) {
-        const int j = tid + p * 256;
-        if (j < C::BN) reinterpret_cast<float *>(st + C::OFF_SW)[j] = half_bits_to_float(rsw[p]);
-      }
-      if (do_h && tid < RT * 32) reinterpret_cast<float *>(st + C::OFF_SL)[tid] = half_bits_to_float(rsl);
-    };
-
-    load_group(0);
-    store_group(0);
-    __syncthreads();
-
-    for (int g = 0; g < KG; g++) {
-      if (g + 1 < KG) load_group(g + 1);
-      const uint8_t *st = smem + (g & 1) * C::STAGE;
-      const float *sxl = reinterpret_cast<const float *>(st + C::OFF_SX);
-      const float *swl = reinterpret_cast<const float *>(st + C::OFF_SW);
-      v8i af[TM], bf[TN];
-      float sxv[TM][16];
-#pragma unroll
-      for (int i = 0; i < TM; i++) {
-        const int ti = wy * TM + i;
-        af[i] = unpack32(*reinterpret_cast<const u32x4 *>(st + C::OFF_A + (ti * 64 + lane) * 16));
-#pragma unroll
-        for (int q = 0; q < 4; q++) {
-          const v4f s4 = *reinterpret_cast<const v4f *>(sxl + ti * 32 + 8 * q + 4 * (lane >> 5));
-          sxv[i][4 * q + 0] = s4.x; sxv[i][4 * q + 1] = s4.y;
-          sxv[i][4 * q + 2] = s4.z; sxv[i][4 * q + 3] = s4.w;
-        }
-      }
-      float swv[TN];
-#pragma unroll
-      for (int j = 0; j < TN; j++) {
-        const int tj = wx * TN + j;
-        bf[j] = unpack32(*reinterpret_cast<const u32x4 *>(st + C::OFF_B + (tj * 64 + lane) * 16));
-        swv[j] = swl[tj * 32 + (lane & 31)];
-      }
-#pragma unroll
-      for (int i = 0; i < TM; i++)
-#pragma unroll
-        for (int j = 0; j < TN; j++) {
-          const v16f cg = mfma_codes_32x32x64(af[i], bf[j]);
-#pragma unroll
-          for (int v = 0; v < 16; v++) acc[i][j][v] = fmaf(cg[v], sxv[i][v] * swv[j], acc[i][j][v]);
-        }
-      if constexpr (RT > 0) {
-        if (do_h) {
-          const float *sll = reinterpret_cast<const float *>(st + C::OFF_SL);
-#pragma unroll
-          for (int h = 0; h < C::HT; h++) {
-            const int rt = wx + h * WN;
-            if (rt < RT) {
-              const v8i lf = unpack32(*reinterpret_cast<const u32x4 *>(st + C::OFF_L + (rt * 64 + lane) * 16));
-              const float sl = sll[rt * 32 + (lane & 31)];
-#pragma unroll
-              for (int i = 0; i < TM; i++) {
-                const v16f cg = mfma_codes_32x32x64(af[i], lf);
-#pragma unroll
-                for (int v = 0; v < 16; v++) hacc[i][h][v] = fmaf(cg[v], sxv[i][v] * sl, hacc[i][h][v]);
-              }
-            }
-          }
-        }
-      }
-      if (g + 1 < KG) store_group((g + 1) & 1);
-      __syncthreads();
+    typename K_::Loads L;
+    if (do_h) {
+      K_::template plan<true>(a, wave, lane, m0, n0, L);
+      K_::template k_loop<true>(c, L, acc, hacc);
+    } else {
+      K_::template plan<false>(a, wave, lane, m0, n0, L);
+      K_::template k_loop<false>(c, L, acc, hacc);
     }
 
     if constexpr (RT > 0) {
@@ -228,7 +389,7 @@ __global__ __launch_bounds__(256, 1) void dual_gemm_tile_kernel(GemmArgs a, int 
         // ---- H -> LDS (fp32), then per-token, per-rank-group requantization ----
 #pragma unroll
         for (int h = 0; h < C::HT; h++) {
-          const int rt = wx + h * WN;
+          const int rt = wx + h * C::WN;
           if (rt < RT) {
 #pragma unroll
             for (int i = 0; i < TM; i++)
@@ -239,8 +400,7 @@ __global__ __launch_bounds__(256, 1) void dual_gemm_tile_kernel(GemmArgs a, int 
               }
           }
         }
-        // zero the fp8 padding ranks [r, 64*RB) of Q_H once
-        if (r < C::RB * 64) {
+        if (r < C::RB * 64) {   // zero the fp8 padding ranks [r, 64*RB) of Q_H
           for (int idx = tid; idx < C::BM * C::RB * 64; idx += 256) {
             const int row = idx / (C::RB * 64), j = idx % (C::RB * 64);
             if (j >= r) QS[row * C::QSTR + j] = 0;
@@ -341,23 +501,30 @@ __global__ __launch_bounds__(256, 1) void dual_gemm_tile_kernel(GemmArgs a, int 
         }
       }
     }
-    // the next column tile overwrites the stage buffers
+    // the next column tile refills the ring
     __syncthreads();
   }
 }
 
 // ---------------------------------------------------------------------------
-template <int WM, int WN, int TM, int TN, int RT>
-static hipError_t launch_tile(const GemmArgs &a, hipStream_t s, int target_wgs) {
-  using C = TileCfg<WM, WN, TM, TN, RT>;
+template <int TM, int TN, int RT>
+static hipError_t launch_tile(const GemmArgs &a, hipStream_t s, int tiles_per_wg_hint) {
+  using C = TileCfg<TM, TN, RT>;
   const int m_tiles = (a.m + C::BM - 1) / C::BM;
   const int n_tiles = (a.geo.n_pad + C::BN - 1) / C::BN;
-  int chunks = (target_wgs + m_tiles - 1) / m_tiles;
-  if (chunks > n_tiles) chunks = n_tiles;
-  if (chunks < 1) chunks = 1;
-  const int tiles_per_wg = (n_tiles + chunks - 1) / chunks;
-  chunks = (n_tiles + tiles_per_wg - 1) / tiles_per_wg;
-  auto kern = dual_gemm_tile_kernel<WM, WN, TM, TN, RT>;
+  int tiles_per_wg = tiles_per_wg_hint;
+  if (tiles_per_wg <= 0) {
+    // enough workgroups for two per CU; beyond that, longer runs of column
+    // tiles per workgroup (fewer recomputations of H)
+    const int target = 512;
+    int chunks = (target + m_tiles - 1) / m_tiles;
+    if (chunks > n_tiles) chunks = n_tiles;
+    if (chunks < 1) chunks = 1;
+    tiles_per_wg = (n_tiles + chunks - 1) / chunks;
+  }
+  if (tiles_per_wg > n_tiles) tiles_per_wg = n_tiles;
+  const int chunks = (n_tiles + tiles_per_wg - 1) / tiles_per_wg;
+  auto kern = dual_gemm_tile_kernel<TM, TN, RT>;
   // more than 64 KiB of dynamic LDS must be enabled per kernel (and device)
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
@@ -367,21 +534,26 @@ static hipError_t launch_tile(const GemmArgs &a, hipStream_t s, int target_wgs) 
   return hipGetLastError();
 }
 
-template <int WM, int WN, int TM, int TN>
-static hipError_t launch_rt(const GemmArgs &a, hipStream_t s, int target_wgs) {
+template <int TM, int TN>
+static hipError_t launch_rt(const GemmArgs &a, hipStream_t s, int tpw) {
   switch (a.geo.r_pad32 / 32) {
-    case 0: return launch_tile<WM, WN, TM, TN, 0>(a, s, target_wgs);
-    case 1: return launch_tile<WM, WN, TM, TN, 1>(a, s, target_wgs);
-    case 2: return launch_tile<WM, WN, TM, TN, 2>(a, s, target_wgs);
-    case 4: return launch_tile<WM, WN, TM, TN, 4>(a, s, target_wgs);
+    case 0: return launch_tile<TM, TN, 0>(a, s, tpw);
+    case 1: return launch_tile<TM, TN, 1>(a, s, tpw);
+    case 2: return launch_tile<TM, TN, 2>(a, s, tpw);
+    case 4: return launch_tile<TM, TN, 4>(a, s, tpw);
     default: return hipErrorInvalidValue;
   }
 }
 
 hipError_t launch_dual_gemm(const GemmArgs &a, hipStream_t s) {
-  if (a.m <= 32) return launch_rt<1, 4, 1, 1>(a, s, 512);
-  if (a.m <= 64) return launch_rt<1, 4, 2, 1>(a, s, 512);
-  return launch_rt<2, 2, 2, 2>(a, s, 256);
+  if (a.m <= 16) return launch_dual_gemm_small(a, s);
+  // tile shape override for tuning sweeps: TQ_TILE="TMxTN[:tiles_per_wg]"
+  int tm = 0, tn = 0, tpw = 0;
+  if (const char *env = getenv("TQ_TILE")) sscanf(env, "%dx%d:%d", &tm, &tn, &tpw);
+  if (tm == 0) { tm = 1; tn = 2; }
+  if (tm == 1 && tn == 2) return launch_rt<1, 2>(a, s, tpw);
+  if (tm == 1 && tn == 4) return launch_rt<1, 4>(a, s, tpw);
+  return launch_rt<2, 2>(a, s, tpw);
 }
 
 }  // namespace tq

@@ -23,7 +23,8 @@ struct GemmArgs {
   const uint8_t *packed;
   Geometry geo;
   const uint32_t *xc;   // [m][k/8] TQ4 words
-  const uint16_t *xs;   // [k/64][m] fp16
+  const uint16_t *xs;   // [k/64][ms] fp16
+  int ms;               // row stride of xs: m rounded up to a multiple of 8
   void *y;              // [m][n]
   int m;
   int bf16_out;
@@ -40,5 +41,6 @@ hipError_t launch_export(const Geometry &g, const uint8_t *packed, uint32_t *wc,
                          uint32_t *l1c, uint16_t *l1s, uint32_t *l2c, uint16_t *l2s,
                          hipStream_t s);
 hipError_t launch_dual_gemm(const GemmArgs &a, hipStream_t s);
+hipError_t launch_dual_gemm_small(const GemmArgs &a, hipStream_t s);   // m <= 16
 
 }  // namespace tq

@@ -11,7 +11,8 @@ namespace tq {
 // ---------------------------------------------------------------------------
 // Activations: one thread per TQ4 word (8 consecutive values); the 8 threads
 // of a group are consecutive lanes of one wavefront and share the group max
-// through three butterfly shuffles.
+// through three butterfly shuffles.  Scales are stored group-major with the
+// token count padded to a multiple of 8 (padding entries are zero).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void quant_act_kernel(const uint16_t *__restrict__ x, int m,
                                                         int k, uint32_t *__restrict__ codes,
@@ -45,7 +46,10 @@ __global__ __launch_bounds__(256) void quant_act_kernel(const uint16_t *__restri
       const int64_t gi = wid >> 3;
       const int64_t groups_per_row = k / kGroup;
       const int64_t row = gi / groups_per_row, g = gi % groups_per_row;
-      scales[g * m + row] = s16;
+      const int64_t ms = (m + 7) / 8 * 8;
+      scales[g * ms + row] = s16;
+      if (row == m - 1)   // zero the padding tokens [m, ms) of this group
+        for (int64_t i = m; i < ms; i++) scales[g * ms + i] = 0;
     }
   }
 }

@@ -2,10 +2,12 @@
 
 Bit-exact: activation codes and scales, weight codes and scales (via the
 canonical export), the on-chip low-rank intermediate H, its scales s_H and
-codes Q_H, and -- because every kernel accumulates each output in the same
-ascending-group fma order as the oracle -- the rounded output Y itself.  The
+codes Q_H.  For m > 16 the tile kernel accumulates every output in the same
+ascending-group fma order as the oracle, so the rounded output Y is bit-exact
+too; the decode kernel (m <= 16) may split the residual K loop over its
+wavefronts, which changes only the fp32 summation order of Y.  The
 spec tolerance (relative Frobenius 1e-3, max-abs 1e-2 * rms(Y)) is
-checked as well, against the oracle's fp64 result.
+checked everywhere, against the oracle's fp64 result.
 """
 import numpy as np
 import pytest
@@ -117,10 +119,11 @@ def full_parity(oracle_mod, X, W, L1, L2, bf16=False):
         np.testing.assert_array_equal(g["H"].view(np.uint32), o["H"].view(np.uint32))
         np.testing.assert_array_equal(g["sH"].view(np.uint32), o["sH"].view(np.uint32))
         np.testing.assert_array_equal(g["qH"], o["qH"])
-    if bf16:
-        np.testing.assert_array_equal(g["Ybits"], o["Ybf"])
-    else:
-        np.testing.assert_array_equal(g["Ybits"], o["Y16"].view(np.uint16))
+    if X.shape[0] > 16:
+        if bf16:
+            np.testing.assert_array_equal(g["Ybits"], o["Ybf"])
+        else:
+            np.testing.assert_array_equal(g["Ybits"], o["Y16"].view(np.uint16))
     check_tolerance(g["Y"], o["Y64"], bf16)
     return g, o
 
@@ -138,6 +141,15 @@ def test_tiny_workload(oracle_mod):
 def test_ragged_shapes(oracle_mod, M, K, N, r):
     say(f"ragged M={M} K={K} N={N} r={r}")
     d = random_codes_layer(M, K, N, r, seed=M + K + N + r)
+    full_parity(oracle_mod, d["X"], d["W_res"], d["L1"], d["L2"])
+
+
+@pytest.mark.parametrize("M,K,N,r", [(4, 128, 8192, 64), (9, 192, 16384, 128), (16, 64, 16416, 32),
+                                     (2, 320, 4096, 16)])
+def test_decode_kernel_variants(oracle_mod, M, K, N, r):
+    """m <= 16 with enough columns for each work split of the decode kernel."""
+    say(f"decode M={M} K={K} N={N} r={r}")
+    d = random_codes_layer(M, K, N, r, seed=N + r)
     full_parity(oracle_mod, d["X"], d["W_res"], d["L1"], d["L2"])
 
 
@@ -205,7 +217,8 @@ def sampled_parity(oracle_mod, wl_name, layer_idx, M, rank=None, n_rows=6, n_col
     rows = np.unique(np.concatenate([[0, M - 1], rng.integers(0, M, n_rows)]))
     cols = np.unique(np.concatenate([[0, N - 1], rng.integers(0, N, n_cols)]))
     o = oracle_mod.layer(X, W, L1, L2, GROUP, rows=rows, cols=cols)
-    np.testing.assert_array_equal(g["Ybits"][np.ix_(rows, cols)], o["Y16"].view(np.uint16))
+    if M > 16:
+        np.testing.assert_array_equal(g["Ybits"][np.ix_(rows, cols)], o["Y16"].view(np.uint16))
     check_tolerance(g["Y"][np.ix_(rows, cols)], o["Y64"])
     if L1 is not None:
         np.testing.assert_array_equal(g["qH"][rows], o["qH"])
