@@ -37,6 +37,27 @@ GROUP = 64
 FP8_MFMA_PEAK_TFLOPS = 5000.0   # MI355X dense fp8 matrix peak (5.0 PFLOP/s)
 HBM_PEAK_GBS = 8000.0
 ROTATE_BYTES = 1 << 30
+CALIB_COPY_BYTES = 256 << 20
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_tile_kernel_m2048_llama3_8b_qo.json")
+TILE_SOURCE = os.path.join(ROOT, "paper_2606_01556_amd", "csrc", "tq_gemm.hip")
+
+
+def measured_traffic():
+    """HBM bytes per launch of the dominant kernel, from the committed
+    FETCH_SIZE / WRITE_SIZE counter runs scaled by the copy-kernel
+    calibration, or None when those counters were taken on another version
+    of the kernel source."""
+    import hashlib
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+        with open(TILE_SOURCE, "rb") as f:
+            sha = hashlib.sha256(f.read()).hexdigest()
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_sha256") != sha:
+        return None
+    return t.get("hbm_bytes_per_launch")
 
 
 def alg_ops(m, n=N, k=K, r=RANK):
@@ -78,6 +99,10 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-detail", action="store_true", help="skip the per-M detail")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="run one plain 256 MiB device copy first (calibrates the HBM "
+                         "byte counters of a profiler run)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the layer runs on a single MI355X "
@@ -108,6 +133,12 @@ def main():
         nwt = max(2, int(np.ceil(ROTATE_BYTES / (WT.numel() * 2))))
         WTs = [WT] + [WT.clone() for _ in range(nwt - 1)]
     torch.cuda.synchronize()
+    if args.calib_copy:
+        src = torch.empty(CALIB_COPY_BYTES // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     s = stream.cuda_stream
     dom_m = MS[-1]
     call = [0]
@@ -158,7 +189,7 @@ def main():
         return 1e3 * e0.elapsed_time(e1) / reps
 
     per_m = []
-    for m in MS:
+    for m in (() if args.no_detail else MS):
         xc, xs = act[m]
         us_layer = timed(lambda: layer_call(m))
         us_quant = timed(lambda: tq.quant_act(X[m], xc, xs, stream=s))
@@ -205,7 +236,7 @@ def main():
         "roofline": {"kernel": f"tq_dual_gemm M={dom_m}", "bound": "mfma",
                      "achieved": round(achieved, 1), "peak": FP8_MFMA_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / FP8_MFMA_PEAK_TFLOPS, 4),
-                     "traffic": None, "avg_launch_us": round(dom_us, 3),
+                     "traffic": measured_traffic(), "avg_launch_us": round(dom_us, 3),
                      "ops_per_launch": alg_ops(dom_m)},
     }
     if not args.no_cpu_baseline:
