@@ -547,6 +547,10 @@ static hipError_t launch_rt(const GemmArgs &a, hipStream_t s, int tpw) {
 
 hipError_t launch_dual_gemm(const GemmArgs &a, hipStream_t s) {
   if (a.m <= 16) return launch_dual_gemm_small(a, s);
+  // kernel family override for tuning sweeps: TQ_PATH=tile|wide
+  const char *path = getenv("TQ_PATH");
+  const bool wide = path ? path[0] == 'w' : a.m >= 1024;
+  if (wide) return launch_dual_gemm_wide(a, s);
   // tile shape override for tuning sweeps: TQ_TILE="TMxTN[:tiles_per_wg]"
   int tm = 0, tn = 0, tpw = 0;
   if (const char *env = getenv("TQ_TILE")) sscanf(env, "%dx%d:%d", &tm, &tn, &tpw);

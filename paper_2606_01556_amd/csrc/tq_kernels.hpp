@@ -42,5 +42,6 @@ hipError_t launch_export(const Geometry &g, const uint8_t *packed, uint32_t *wc,
                          hipStream_t s);
 hipError_t launch_dual_gemm(const GemmArgs &a, hipStream_t s);
 hipError_t launch_dual_gemm_small(const GemmArgs &a, hipStream_t s);   // m <= 16
+hipError_t launch_dual_gemm_wide(const GemmArgs &a, hipStream_t s);    // prefill sizes
 
 }  // namespace tq
