@@ -1,25 +1,30 @@
 // Fused dual-component layer for decode-sized token counts (m <= 16).
 //
-// Same computation as the tile kernel (paper Sec. 4.3), shaped for the
-// memory-bound regime: a workgroup owns NC 16-column output tiles and all
-// m <= 16 tokens; the 16x16x128 fp8 matrix-core instruction covers two K
-// groups per operand load (operand lanes 0-31 hold group g, lanes 32-63 group
-// g+1), and two instructions with complementary halves of the activation
-// operand zeroed give the two groups' exact integer sums separately.
+// Same computation as the tile kernels (paper Sec. 4.3), shaped for the
+// memory-bound regime.  A workgroup owns NC 16-column output tiles and all
+// m <= 16 tokens; its eight wavefronts split the work by kind:
+//  * wavefronts 0-3 run stage 1: the 16-rank column tiles of H, spread over
+//    them, each accumulated over the whole K loop in ascending group order, so
+//    H (and therefore Q_H) is bit-identical to the oracle's;
+//  * wavefronts 4-7 run the residual: in every chunk of K each takes its own
+//    group pairs for the NC column tiles; the partial sums are added in LDS in
+//    a fixed order (only Y's fp32 summation order differs from the oracle's).
+// The 16x16x128 fp8 matrix-core instruction covers two K groups per operand
+// load (operand lanes 0-31 hold group g, lanes 32-63 group g + 1); two
+// instructions, each reading zeros in the other half of the activation
+// operand, give the two groups' exact integer sums separately.
 //
-//  * Stage 1 (H, all r ranks): the 16-rank column tiles of H are spread over
-//    the four wavefronts; each wavefront runs the whole K loop for its tiles
-//    in ascending group order, so H (and therefore Q_H) is bit-identical to
-//    the tile kernel's and the oracle's.
-//  * Residual: with SPLITK the K loop of the NC column tiles is split over
-//    the four wavefronts (group pair p goes to wavefront p mod 4) and the
-//    partial sums are added in LDS in a fixed order; without SPLITK each
-//    wavefront owns one of NC = 4 column tiles and accumulates it in order.
-//  * After the K loop: H is re-quantized in LDS, stage 2 (Q_H Q(L2)) runs
-//    per column tile, and one epilogue stores Y.
-// Every operand fragment and scale is loaded straight from global memory
-// into a per-wavefront register ring four group pairs deep; nothing goes
-// through LDS in the K loop and the K loop has no barrier.
+// Data movement.  K runs in chunks of CHG groups.  Everything the eight
+// wavefronts share -- the activation codes of the chunk (expanded once to fp8
+// matrix-core bytes) and the activation, L1 and weight scales (converted once
+// to fp32) -- is loaded by the whole workgroup one chunk ahead into a
+// two-slot LDS buffer, with one workgroup barrier per chunk.  Each wavefront
+// streams only its own weight (or L1) code fragments, one coalesced 1 KiB
+// block pair per group pair, through a register ring DRING pairs deep.  All
+// loads are unconditional (indices clamped; pairs past the end use a zero
+// scale factor), so the compiler counts the loads in flight exactly.
+#include <stdlib.h>
+
 #include "tq_device.hpp"
 #include "tq_kernels.hpp"
 
@@ -27,43 +32,72 @@ namespace tq {
 
 namespace {
 
+constexpr int DWAVE = 8;              // wavefronts per workgroup (0-3 stage 1, 4-7 residual)
+constexpr int CHP = 8;                // group pairs per chunk
+constexpr int CHG = 2 * CHP;          // K-groups per chunk
+constexpr int XROW = CHG * 64 + 16;   // LDS bytes per token row of expanded codes (padded)
+constexpr int DRING = 8;              // group pairs of code fragments in flight per wavefront
+
+template <int NC, int RT16>
+struct DCfg {
+  static constexpr int RP = RT16 * 16;                // ranks covered by the 16-rank tiles
+  static constexpr int X_OFF = 0;                     // [16 rows][XROW] fp8 codes
+  static constexpr int XS_OFF = 16 * XROW;            // [CHG][16 rows] fp32 activation scales
+  static constexpr int LS_OFF = XS_OFF + CHG * 16 * 4;       // [CHG][RP] fp32 L1 scales
+  static constexpr int WS_OFF = LS_OFF + CHG * RP * 4;       // [CHG][16 NC] fp32 weight scales
+  static constexpr int BUF = WS_OFF + CHG * 16 * NC * 4;
+  static constexpr int ZERO_OFF = 2 * BUF;            // 32 bytes of zero codes
+  static constexpr int LDS = ZERO_OFF + 32;
+  // 16-byte scale pieces (8 fp16) of one chunk: activation, L1, weight
+  static constexpr int PX = CHG * 2;
+  static constexpr int PL = CHG * RP / 8;
+  static constexpr int PW = CHG * 2 * NC;
+  static constexpr int NPIECE = PX + PL + PW;
+  static constexpr int HT = (RT16 + 3) / 4;           // H tiles per stage-1 wavefront
+  static constexpr int HT1 = HT > 0 ? HT : 1;
+  static constexpr int RB = (RT16 + 3) / 4;           // 64-rank blocks (= rank groups)
+  static constexpr int HSTR = RP + 1;
+  static constexpr int QSTR = (RB > 0 ? RB : 1) * 64 + 16;
+  static_assert(NPIECE <= 64 * DWAVE, "one scale piece per thread and chunk");
+  static_assert(16 * (RP > 0 ? HSTR : 1) * 4 <= BUF, "H staging fits in a chunk buffer");
+};
+
 // operand fragment (16 bytes) of a 16-column slice of a packed 32-column
-// block pair: lane l = (q, c), q = l / 16 picks group g + q / 2 and the
-// 32-code half q % 2, c = l % 16 the column inside the slice.
-__device__ __forceinline__ u32x4 load_slice(const uint8_t *blocks, int64_t kblocks, int col16,
-                                            int g, int kgroups, int lane) {
+// block pair: lane l = (q, c), q = l / 16 picks the 32-code half q % 2 of
+// group gg (the caller's per-lane, clamped group), c = l % 16 the column
+__device__ __forceinline__ u32x4 slice16(const uint8_t *blocks, int64_t kblocks, int col16, int gg,
+                                         int lane) {
   const int q = lane >> 4, c = lane & 15;
-  const int gg = g + (q >> 1);
-  if (gg >= kgroups) return u32x4{0, 0, 0, 0};
   const int64_t blk = (int64_t)(col16 >> 1) * kblocks + gg;
   const int L = (q & 1) * 32 + (col16 & 1) * 16 + c;
   return *reinterpret_cast<const u32x4 *>(blocks + (blk * 64 + L) * 16);
 }
 
-__device__ __forceinline__ v8i zero_v8i() { return v8i{0, 0, 0, 0, 0, 0, 0, 0}; }
+__device__ __forceinline__ v8i lds_v8i(const uint8_t *p) {
+  const u32x4 lo = *reinterpret_cast<const u32x4 *>(p);
+  const u32x4 hi = *reinterpret_cast<const u32x4 *>(p + 16);
+  return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+}
 
 }  // namespace
 
-template <int NC, int RT16, bool SPLITK>
-__global__ __launch_bounds__(256) void dual_gemm_small_kernel(GemmArgs a) {
-  constexpr int HT = (RT16 + 3) / 4;          // H tiles (16 ranks) per wavefront
-  constexpr int RB = (RT16 + 3) / 4;          // 64-rank blocks (= rank groups)
-  constexpr int RP = RT16 * 16;               // padded rank
-  constexpr int HSTR = RP + 1;
-  constexpr int QSTR = (RB > 0 ? RB : 1) * 64 + 16;
-  static_assert(SPLITK || NC == 4, "without split-K each wavefront owns one column tile");
-  constexpr int RT_W = SPLITK ? NC : 1;       // residual tiles per wavefront
+template <int NC, int RT16>
+__global__ __launch_bounds__(64 * DWAVE, 1) void dual_gemm_small_kernel(GemmArgs a) {
+  using C = DCfg<NC, RT16>;
+  constexpr int RP = C::RP, RB = C::RB, HT = C::HT, HT1 = C::HT1, HSTR = C::HSTR, QSTR = C::QSTR;
 
-  __shared__ float RES[SPLITK ? 4 : 1][NC][4][64];
-  __shared__ float HS[16 * (RP > 0 ? HSTR : 1)];
+  __shared__ __attribute__((aligned(16))) uint8_t SM[C::LDS];
+  __shared__ float RES[4][NC][4][64];
   __shared__ __attribute__((aligned(16))) uint8_t QS[16 * QSTR];
   __shared__ float SHS[16 * (RB > 0 ? RB : 1)];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int q = lane >> 4, c16 = lane & 15;
   const Geometry &geo = a.geo;
   const int KG = geo.k / kGroup, NP = (KG + 1) / 2;
-  const int m = a.m;
+  const int NCH = (KG + CHG - 1) / CHG;
+  const int m = a.m, ms = a.ms;
   const int col0 = blockIdx.x * NC;             // first 16-column tile of this workgroup
   const int ctiles16 = geo.n_pad / 16;
   const uint8_t *wcodes = a.packed + geo.off_w;
@@ -72,151 +106,217 @@ __global__ __launch_bounds__(256) void dual_gemm_small_kernel(GemmArgs a) {
   const uint16_t *l1scales = reinterpret_cast<const uint16_t *>(a.packed + geo.off_l1s);
   const uint8_t *l2codes = a.packed + geo.off_l2;
   const uint16_t *l2scales = reinterpret_cast<const uint16_t *>(a.packed + geo.off_l2s);
-  const int64_t xwords = geo.k / 8;
-  const int xrow = c16;                          // activation row held by this lane
+  const uint8_t *xc = reinterpret_cast<const uint8_t *>(a.xc);
+  const int64_t xrow_bytes = geo.k / 2;
   const int orow0 = 4 * q;                       // output rows 4q..4q+3 held by this lane
 
-  // residual tiles handled by this wavefront
-  auto res_tile = [&](int j) { return SPLITK ? col0 + j : col0 + w; };
-
-  v4f acc[RT_W];
-  v4f hacc[HT > 0 ? HT : 1];
-#pragma unroll
-  for (int j = 0; j < RT_W; j++) acc[j] = v4f{0, 0, 0, 0};
-#pragma unroll
-  for (int h = 0; h < (HT > 0 ? HT : 1); h++) hacc[h] = v4f{0, 0, 0, 0};
-
-  // one group pair of operand slices and scales; a ring of D pairs per
-  // wavefront keeps D pairs of loads in flight (no LDS, no barriers)
-  struct Frag {
-    u32x4 x, l[HT > 0 ? HT : 1], wv[RT_W];
-    uint16_t sx1[4], sx2[4], sl1[HT > 0 ? HT : 1][2], sw[RT_W][2];
-  };
-  auto load_pair = [&](int p, Frag &f) {
-    const int g = 2 * p;
-    const int gg = g + (q >> 1);
-    const bool two = g + 1 < KG;
-    f.x = u32x4{0, 0, 0, 0};
-    if (xrow < m && gg < KG)
-      f.x = *reinterpret_cast<const u32x4 *>(a.xc + xrow * xwords + gg * 8 + (q & 1) * 4);
-#pragma unroll
-    for (int v = 0; v < 4; v++) {
-      const int row = orow0 + v;
-      f.sx1[v] = row < m ? a.xs[(int64_t)g * a.ms + row] : (uint16_t)0;
-      f.sx2[v] = (row < m && two) ? a.xs[(int64_t)(g + 1) * a.ms + row] : (uint16_t)0;
-    }
-#pragma unroll
-    for (int h = 0; h < HT; h++) {
-      const int t16 = w + 4 * h;
-      f.l[h] = u32x4{0, 0, 0, 0};
-      f.sl1[h][0] = f.sl1[h][1] = 0;
-      if (t16 < RT16) {
-        f.l[h] = load_slice(l1codes, KG, t16, g, KG, lane);
-        const int rk = t16 * 16 + c16;
-        f.sl1[h][0] = l1scales[(int64_t)g * geo.r_pad32 + rk];
-        if (two) f.sl1[h][1] = l1scales[(int64_t)(g + 1) * geo.r_pad32 + rk];
-      }
-    }
-    const bool mine = SPLITK ? ((p & 3) == w) : true;
-#pragma unroll
-    for (int j = 0; j < RT_W; j++) {
-      const int ct = res_tile(j);
-      f.wv[j] = u32x4{0, 0, 0, 0};
-      f.sw[j][0] = f.sw[j][1] = 0;
-      if (mine && ct < ctiles16) {
-        f.wv[j] = load_slice(wcodes, KG, ct, g, KG, lane);
-        const int col = ct * 16 + c16;
-        f.sw[j][0] = wscales[(int64_t)g * geo.n_pad + col];
-        if (two) f.sw[j][1] = wscales[(int64_t)(g + 1) * geo.n_pad + col];
-      }
-    }
-  };
-
-  auto compute_pair = [&](int p, const Frag &f) {
-    const int g = 2 * p;
-    const bool two = g + 1 < KG;
-    const v8i xa = unpack32(f.x);
-    const v8i x1 = q < 2 ? xa : zero_v8i();     // group g only
-    const v8i x2 = q < 2 ? zero_v8i() : xa;     // group g + 1 only
-    float sx1[4], sx2[4];
-#pragma unroll
-    for (int v = 0; v < 4; v++) {
-      sx1[v] = half_bits_to_float(f.sx1[v]);
-      sx2[v] = half_bits_to_float(f.sx2[v]);
-    }
-    // ---- stage 1: H tiles of this wavefront, ascending groups ----
-#pragma unroll
-    for (int h = 0; h < HT; h++) {
-      const int t16 = w + 4 * h;
-      if (t16 < RT16) {
-        const v8i lb = unpack32(f.l[h]);
-        const float s1 = half_bits_to_float(f.sl1[h][0]);
-        const v4f c1 = mfma_codes_16x16x128(x1, lb);
-#pragma unroll
-        for (int v = 0; v < 4; v++) hacc[h][v] = fmaf(c1[v], sx1[v] * s1, hacc[h][v]);
-        if (two) {
-          const float s2 = half_bits_to_float(f.sl1[h][1]);
-          const v4f c2 = mfma_codes_16x16x128(x2, lb);
-#pragma unroll
-          for (int v = 0; v < 4; v++) hacc[h][v] = fmaf(c2[v], sx2[v] * s2, hacc[h][v]);
-        }
-      }
-    }
-    // ---- residual ----
-    const bool mine = SPLITK ? ((p & 3) == w) : true;
-    if (mine) {
-#pragma unroll
-      for (int j = 0; j < RT_W; j++) {
-        const int ct = res_tile(j);
-        if (ct < ctiles16) {
-          const v8i wb = unpack32(f.wv[j]);
-          const float s1 = half_bits_to_float(f.sw[j][0]);
-          const v4f c1 = mfma_codes_16x16x128(x1, wb);
-#pragma unroll
-          for (int v = 0; v < 4; v++) acc[j][v] = fmaf(c1[v], sx1[v] * s1, acc[j][v]);
-          if (two) {
-            const float s2 = half_bits_to_float(f.sw[j][1]);
-            const v4f c2 = mfma_codes_16x16x128(x2, wb);
-#pragma unroll
-            for (int v = 0; v < 4; v++) acc[j][v] = fmaf(c2[v], sx2[v] * s2, acc[j][v]);
-          }
-        }
-      }
-    }
-  };
-
-  constexpr int D = 4;
-  Frag ring[D];
-#pragma unroll
-  for (int i = 0; i < D; i++)
-    if (i < NP) load_pair(i, ring[i]);
-  for (int p0 = 0; p0 < NP; p0 += D) {
-#pragma unroll
-    for (int i = 0; i < D; i++) {
-      const int p = p0 + i;
-      if (p < NP) {
-        compute_pair(p, ring[i]);
-        if (p + D < NP) load_pair(p + D, ring[i]);
-      }
+  // ---- this thread's share of a chunk load ----
+  // activation codes: row t / 32, 16-byte piece t % 32 (group t % 32 / 2, half t % 2)
+  const int xl_row = tid >> 5, xl_gi = (tid & 31) >> 1, xl_half = tid & 1;
+  const uint8_t *xl_src = xc + (int64_t)min(xl_row, m - 1) * xrow_bytes + xl_half * 16;
+  const int xl_dst = C::X_OFF + xl_row * XROW + xl_gi * 64 + xl_half * 32;
+  // one scale piece: 8 fp16 from src + group * stride, to dst as 8 fp32
+  const uint16_t *sp_src;
+  int sp_gi, sp_stride, sp_dst;
+  {
+    const int sp = min(tid, C::NPIECE - 1);
+    if (sp < C::PX) {
+      sp_gi = sp >> 1;
+      sp_src = a.xs + min(8 * (sp & 1), ms - 8);
+      sp_stride = ms;
+      sp_dst = C::XS_OFF + (sp_gi * 16 + 8 * (sp & 1)) * 4;
+    } else if (sp < C::PX + C::PL) {
+      const int s2 = sp - C::PX;
+      sp_gi = s2 / (RP / 8);
+      const int r8 = s2 % (RP / 8);
+      sp_src = l1scales + 8 * r8;
+      sp_stride = geo.r_pad32;
+      sp_dst = C::LS_OFF + (sp_gi * RP + 8 * r8) * 4;
+    } else {
+      const int s3 = sp - C::PX - C::PL;
+      sp_gi = s3 / (2 * NC);
+      const int c8 = s3 % (2 * NC);
+      sp_src = wscales + min(col0 * 16 + 8 * c8, geo.n_pad - 8);
+      sp_stride = geo.n_pad;
+      sp_dst = C::WS_OFF + (sp_gi * 16 * NC + 8 * c8) * 4;
     }
   }
-
-  // ---- partial sums and H to LDS ----
+  struct Chunk {
+    u32x4 x, s;
+  };
+  auto chunk_load = [&](int c, Chunk &k) {
+    c = min(c, NCH - 1);
+    const int g0 = c * CHG;
+    k.x = *reinterpret_cast<const u32x4 *>(xl_src + min(g0 + xl_gi, KG - 1) * 32);
+    k.s = *reinterpret_cast<const u32x4 *>(sp_src + (int64_t)min(g0 + sp_gi, KG - 1) * sp_stride);
+  };
+  auto chunk_store = [&](int buf, const Chunk &k) {
+    uint8_t *B = SM + buf * C::BUF;
+    const v8i u = unpack32(k.x);
+    *reinterpret_cast<u32x4 *>(B + xl_dst) = u32x4{(uint32_t)u[0], (uint32_t)u[1], (uint32_t)u[2], (uint32_t)u[3]};
+    *reinterpret_cast<u32x4 *>(B + xl_dst + 16) = u32x4{(uint32_t)u[4], (uint32_t)u[5], (uint32_t)u[6], (uint32_t)u[7]};
+    const uint32_t h[4] = {k.s.x, k.s.y, k.s.z, k.s.w};
+    float f[8];
 #pragma unroll
-  for (int j = 0; j < RT_W; j++)
-#pragma unroll
-    for (int v = 0; v < 4; v++) RES[SPLITK ? w : 0][SPLITK ? j : w][v][lane] = acc[j][v];
-  if constexpr (RT16 > 0) {
-#pragma unroll
-    for (int h = 0; h < HT; h++) {
-      const int t16 = w + 4 * h;
-      if (t16 < RT16)
-#pragma unroll
-        for (int v = 0; v < 4; v++) HS[(orow0 + v) * HSTR + t16 * 16 + c16] = hacc[h][v];
+    for (int i = 0; i < 4; i++) {
+      f[2 * i] = half_bits_to_float((uint16_t)h[i]);
+      f[2 * i + 1] = half_bits_to_float((uint16_t)(h[i] >> 16));
     }
+    *reinterpret_cast<v4f *>(B + sp_dst) = v4f{f[0], f[1], f[2], f[3]};
+    *reinterpret_cast<v4f *>(B + sp_dst + 16) = v4f{f[4], f[5], f[6], f[7]};
+  };
+
+  // ---- activation operands of a group pair from the chunk buffer ----
+  // lane (q, c16) holds token row c16, group 2 pl + q / 2, code half q % 2; the
+  // other single-group operand reads zeros
+  const uint32_t x_lane = C::X_OFF + c16 * XROW + (q >> 1) * 64 + (q & 1) * 32;
+  auto x_ops = [&](int buf, int pl, v8i &x1, v8i &x2) {
+    const uint32_t data = buf * C::BUF + x_lane + pl * 128;
+    x1 = lds_v8i(SM + (q < 2 ? data : C::ZERO_OFF));
+    x2 = lds_v8i(SM + (q < 2 ? C::ZERO_OFF : data));
+  };
+  auto x_scales = [&](int buf, int pl, v4f &s1, v4f &s2) {
+    const uint8_t *B = SM + buf * C::BUF + C::XS_OFF;
+    s1 = *reinterpret_cast<const v4f *>(B + ((2 * pl) * 16 + orow0) * 4);
+    s2 = *reinterpret_cast<const v4f *>(B + ((2 * pl + 1) * 16 + orow0) * 4);
+  };
+
+  if (tid < 8) reinterpret_cast<uint32_t *>(SM + C::ZERO_OFF)[tid] = 0;
+  {
+    Chunk k0;
+    chunk_load(0, k0);
+    chunk_store(0, k0);
+  }
+  __syncthreads();
+
+  if (w < 4) {
+    // ---------------- stage 1: H tiles w + 4 h, all K, ascending groups ----------------
+    v4f hacc[HT1];
+#pragma unroll
+    for (int h = 0; h < HT1; h++) hacc[h] = v4f{0, 0, 0, 0};
+    // wavefronts past the last H tile run the same loop on a duplicate tile
+    // (no branch in the K loop) and never store it
+    const bool active = RT16 > 0 && w < RT16;   // wave-uniform
+    u32x4 ring[DRING][HT1];
+    auto load = [&](int p, u32x4 (&l)[HT1]) {
+      if constexpr (RT16 > 0) {
+        p = min(p, NP - 1);
+        const int gl = min(2 * p + (q >> 1), KG - 1);
+#pragma unroll
+        for (int h = 0; h < HT1; h++) l[h] = slice16(l1codes, KG, min(w + 4 * h, RT16 - 1), gl, lane);
+      }
+    };
+#pragma unroll
+    for (int i = 0; i < DRING; i++) load(i, ring[i]);
+    for (int c = 0; c < NCH; c++) {
+      const int buf = c & 1;
+      Chunk nk;
+      chunk_load(c + 1, nk);
+      if constexpr (RT16 > 0) {
+        const uint8_t *LS = SM + buf * C::BUF + C::LS_OFF;
+#pragma unroll
+        for (int pl = 0; pl < CHP; pl++) {
+          const int p = c * CHP + pl;
+          const float v1 = p < NP ? 1.0f : 0.0f;
+          const float v2 = 2 * p + 1 < KG ? 1.0f : 0.0f;
+          v8i x1, x2;
+          x_ops(buf, pl, x1, x2);
+          v4f sa1, sa2;
+          x_scales(buf, pl, sa1, sa2);
+#pragma unroll
+          for (int h = 0; h < HT1; h++) {
+            const int rk = min(w + 4 * h, RT16 - 1) * 16 + c16;
+            const float s1 = reinterpret_cast<const float *>(LS)[(2 * pl) * RP + rk] * v1;
+            const float s2 = reinterpret_cast<const float *>(LS)[(2 * pl + 1) * RP + rk] * v2;
+            const v8i lb = unpack32(ring[pl][h]);
+            const v4f c1 = mfma_codes_16x16x128(x1, lb);
+            const v4f c2 = mfma_codes_16x16x128(x2, lb);
+#pragma unroll
+            for (int v = 0; v < 4; v++) hacc[h][v] = fmaf(c1[v], sa1[v] * s1, hacc[h][v]);
+#pragma unroll
+            for (int v = 0; v < 4; v++) hacc[h][v] = fmaf(c2[v], sa2[v] * s2, hacc[h][v]);
+          }
+          load(p + DRING, ring[pl]);
+        }
+      }
+      chunk_store(buf ^ 1, nk);
+      __syncthreads();
+    }
+    if (active) {
+#pragma unroll
+      for (int h = 0; h < HT; h++) {
+        const int t16 = w + 4 * h;
+        if (t16 < RT16)
+#pragma unroll
+          for (int v = 0; v < 4; v++)
+            reinterpret_cast<float *>(SM)[(orow0 + v) * HSTR + t16 * 16 + c16] = hacc[h][v];
+      }
+    }
+  } else {
+    // ---------------- residual: group pairs rw, rw + 4 of every chunk ----------------
+    const int rw = w - 4;
+    v4f acc[NC];
+#pragma unroll
+    for (int j = 0; j < NC; j++) acc[j] = v4f{0, 0, 0, 0};
+    // this wavefront's pairs of chunk c: c * CHP + rw + 4 i, i = 0, 1
+    constexpr int RPC = CHP / 4;
+    constexpr int RR = 2 * RPC;                    // ring: two chunks ahead
+    u32x4 ring[RR][NC];
+    auto load = [&](int c, int i, u32x4 (&wv)[NC]) {
+      const int p = min(c * CHP + rw + 4 * i, NP - 1);
+      const int gl = min(2 * p + (q >> 1), KG - 1);
+#pragma unroll
+      for (int j = 0; j < NC; j++) wv[j] = slice16(wcodes, KG, min(col0 + j, ctiles16 - 1), gl, lane);
+    };
+#pragma unroll
+    for (int i = 0; i < RR; i++) load(i / RPC, i % RPC, ring[i]);
+    for (int c = 0; c < NCH; c += 2) {
+#pragma unroll
+      for (int cc = 0; cc < 2; cc++) {
+        const int ch = c + cc;
+        if (cc == 1 && ch >= NCH) break;
+        const int buf = ch & 1;
+        Chunk nk;
+        chunk_load(ch + 1, nk);
+        const uint8_t *WS = SM + buf * C::BUF + C::WS_OFF;
+#pragma unroll
+        for (int i = 0; i < RPC; i++) {
+          const int pl = rw + 4 * i;
+          const int p = ch * CHP + pl;
+          const float v1 = p < NP ? 1.0f : 0.0f;
+          const float v2 = 2 * p + 1 < KG ? 1.0f : 0.0f;
+          v8i x1, x2;
+          x_ops(buf, pl, x1, x2);
+          v4f sa1, sa2;
+          x_scales(buf, pl, sa1, sa2);
+#pragma unroll
+          for (int j = 0; j < NC; j++) {
+            const float s1 = reinterpret_cast<const float *>(WS)[(2 * pl) * 16 * NC + j * 16 + c16] * v1;
+            const float s2 = reinterpret_cast<const float *>(WS)[(2 * pl + 1) * 16 * NC + j * 16 + c16] * v2;
+            const v8i wb = unpack32(ring[cc * RPC + i][j]);
+            const v4f c1 = mfma_codes_16x16x128(x1, wb);
+            const v4f c2 = mfma_codes_16x16x128(x2, wb);
+#pragma unroll
+            for (int v = 0; v < 4; v++) acc[j][v] = fmaf(c1[v], sa1[v] * s1, acc[j][v]);
+#pragma unroll
+            for (int v = 0; v < 4; v++) acc[j][v] = fmaf(c2[v], sa2[v] * s2, acc[j][v]);
+          }
+          load(ch + 2, i, ring[cc * RPC + i]);
+        }
+        chunk_store(buf ^ 1, nk);
+        __syncthreads();
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < NC; j++)
+#pragma unroll
+      for (int v = 0; v < 4; v++) RES[rw][j][v][lane] = acc[j][v];
+  }
+
+  if constexpr (RT16 > 0) {
     const int r = geo.r;
     if (r < RB * 64)
-      for (int idx = tid; idx < 16 * RB * 64; idx += 256) {
+      for (int idx = tid; idx < 16 * RB * 64; idx += 64 * DWAVE) {
         const int row = idx / (RB * 64), j = idx % (RB * 64);
         if (j >= r) QS[row * QSTR + j] = 0;
       }
@@ -225,6 +325,7 @@ __global__ __launch_bounds__(256) void dual_gemm_small_kernel(GemmArgs a) {
 
   // ---- requantize H per token and rank group (s_H stays fp32) ----
   if constexpr (RT16 > 0) {
+    const float *HS = reinterpret_cast<const float *>(SM);
     const int r = geo.r, gr = geo.gr, rg = r / gr;
     const int subs = gr / 8;
     const int work = 16 * rg * subs;        // <= 256
@@ -271,26 +372,19 @@ __global__ __launch_bounds__(256) void dual_gemm_small_kernel(GemmArgs a) {
   }
 
   // ---- stage 2 and the single epilogue: wavefront j < NC stores tile j ----
-  for (int j = w; j < NC; j += 4) {
+  for (int j = w; j < NC; j += DWAVE) {
     const int ct = col0 + j;
     if (ct >= ctiles16) continue;
     v4f ylr = v4f{0, 0, 0, 0};
     if constexpr (RT16 > 0) {
       // rank blocks in pairs: lanes q < 2 carry block rb, lanes q >= 2 block rb + 1
       for (int rb = 0; rb < RB; rb += 2) {
-        const int rbq = rb + (q >> 1);
-        v8i qa = zero_v8i();
-        u32x4 lraw = u32x4{0, 0, 0, 0};
-        if (rbq < RB) {
-          const uint8_t *qrow = QS + c16 * QSTR + rbq * 64 + (q & 1) * 32;
-          const u32x4 q0 = *reinterpret_cast<const u32x4 *>(qrow);
-          const u32x4 q1 = *reinterpret_cast<const u32x4 *>(qrow + 16);
-          qa = v8i{(int)q0.x, (int)q0.y, (int)q0.z, (int)q0.w, (int)q1.x, (int)q1.y, (int)q1.z, (int)q1.w};
-          lraw = load_slice(l2codes, RB, ct, rb, RB, lane);
-        }
-        const v8i lb = unpack32(lraw);
-        const v8i qa1 = q < 2 ? qa : zero_v8i();
-        const v8i qa2 = q < 2 ? zero_v8i() : qa;
+        const int rbq = min(rb + (q >> 1), RB - 1);
+        const v8i qa = lds_v8i(QS + c16 * QSTR + rbq * 64 + (q & 1) * 32);
+        const v8i lb = unpack32(slice16(l2codes, RB, ct, rbq, lane));
+        const v8i zero = {0, 0, 0, 0, 0, 0, 0, 0};
+        const v8i qa1 = q < 2 ? qa : zero;
+        const v8i qa2 = q < 2 ? zero : qa;
         const int col = ct * 16 + c16;
         {
           const float sl2 = half_bits_to_float(l2scales[(int64_t)rb * geo.n_pad + col]);
@@ -312,11 +406,7 @@ __global__ __launch_bounds__(256) void dual_gemm_small_kernel(GemmArgs a) {
       for (int v = 0; v < 4; v++) {
         const int row = orow0 + v;
         if (row < m) {
-          float yres;
-          if (SPLITK)
-            yres = ((RES[0][j][v][lane] + RES[1][j][v][lane]) + RES[2][j][v][lane]) + RES[3][j][v][lane];
-          else
-            yres = RES[0][j][v][lane];
+          const float yres = ((RES[0][j][v][lane] + RES[1][j][v][lane]) + RES[2][j][v][lane]) + RES[3][j][v][lane];
           const float yv = yres + ylr[v];
           const uint16_t bits = a.bf16_out ? float_to_bf16_bits(yv) : float_to_half_bits(yv);
           reinterpret_cast<uint16_t *>(a.y)[(int64_t)row * geo.n + col] = bits;
@@ -326,28 +416,29 @@ __global__ __launch_bounds__(256) void dual_gemm_small_kernel(GemmArgs a) {
   }
 }
 
-template <int NC, bool SPLITK>
+template <int NC>
 static hipError_t launch_small_nc(const GemmArgs &a, hipStream_t s) {
   const int tiles16 = a.geo.n_pad / 16;
   const dim3 grid((tiles16 + NC - 1) / NC);
+  const dim3 block(64 * DWAVE);
   switch ((a.geo.r + 15) / 16) {
-    case 0: hipLaunchKernelGGL((dual_gemm_small_kernel<NC, 0, SPLITK>), grid, dim3(256), 0, s, a); break;
-    case 1: hipLaunchKernelGGL((dual_gemm_small_kernel<NC, 1, SPLITK>), grid, dim3(256), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((dual_gemm_small_kernel<NC, 2, SPLITK>), grid, dim3(256), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((dual_gemm_small_kernel<NC, 4, SPLITK>), grid, dim3(256), 0, s, a); break;
-    case 8: hipLaunchKernelGGL((dual_gemm_small_kernel<NC, 8, SPLITK>), grid, dim3(256), 0, s, a); break;
+    case 0: hipLaunchKernelGGL((dual_gemm_small_kernel<NC, 0>), grid, block, 0, s, a); break;
+    case 1: hipLaunchKernelGGL((dual_gemm_small_kernel<NC, 1>), grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL((dual_gemm_small_kernel<NC, 2>), grid, block, 0, s, a); break;
+    case 4: hipLaunchKernelGGL((dual_gemm_small_kernel<NC, 4>), grid, block, 0, s, a); break;
+    case 8: hipLaunchKernelGGL((dual_gemm_small_kernel<NC, 8>), grid, block, 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
 hipError_t launch_dual_gemm_small(const GemmArgs &a, hipStream_t s) {
-  // aim at >= 256 workgroups (one per CU); own whole column tiles (exact
-  // accumulation order) only when that still fills the GPU
+  // one 16-column tile per workgroup while that gives at least two
+  // workgroups per CU; wider layers take two tiles per workgroup
   const int tiles16 = a.geo.n_pad / 16;
-  if (tiles16 >= 4 * 256) return launch_small_nc<4, false>(a, s);
-  if (tiles16 >= 2 * 256) return launch_small_nc<2, true>(a, s);
-  return launch_small_nc<1, true>(a, s);
+  int nc = tiles16 >= 2 * 512 ? 2 : 1;
+  if (const char *env = getenv("TQ_SMALL_NC")) nc = atoi(env) == 2 ? 2 : 1;
+  return nc == 2 ? launch_small_nc<2>(a, s) : launch_small_nc<1>(a, s);
 }
 
 }  // namespace tq
