@@ -549,6 +549,7 @@ hipError_t launch_dual_gemm(const GemmArgs &a, hipStream_t s) {
   if (a.m <= 16) return launch_dual_gemm_small(a, s);
   // kernel family override for tuning sweeps: TQ_PATH=tile|wide
   const char *path = getenv("TQ_PATH");
+  if (path && path[0] == 's') return launch_dual_gemm_stream(a, s);
   const bool wide = path ? path[0] == 'w' : a.m >= 1024;
   if (wide) return launch_dual_gemm_wide(a, s);
   // tile shape override for tuning sweeps: TQ_TILE="TMxTN[:tiles_per_wg]"

@@ -3,26 +3,30 @@
 // chip, its on-the-fly re-quantization, stage 2 Q_H Q(L2) and one epilogue,
 // in one kernel.
 //
-// Work decomposition.  A workgroup of 8 wavefronts (two per SIMD) owns 64
-// tokens and a run of 512-column passes; each wavefront computes all 64
+// Work decomposition.  A workgroup of 4 wavefronts (one per SIMD) owns 64
+// tokens and a run of 256-column passes; each wavefront computes all 64
 // tokens x 64 columns of a pass (four 32x32 tiles).  The activation operand of
-// a K-group is therefore shared by all eight wavefronts: it is expanded from
+// a K-group is therefore shared by the four wavefronts: it is expanded from
 // 4-bit codes to fp8 once per workgroup, into LDS, while every wavefront
 // expands its own weight columns in registers.  During the first pass the
-// workgroup also accumulates H for its 64 tokens (2 r / 32 tiles of 32x32, one
-// per wavefront), then re-quantizes H into LDS; later passes reuse Q_H and
-// s_H, so H is formed once per workgroup.  Two wavefronts per SIMD let the
-// matrix core of one overlap the fp32 rescaling fmas of the other.
+// workgroup also accumulates H for its 64 tokens (2 r / 32 tiles of 32x32,
+// spread over the wavefronts), then re-quantizes H into LDS; later passes
+// reuse Q_H and s_H, so H is formed once per workgroup.
 //
 // K pipeline (one K-group of 64 per step, one workgroup barrier per step):
 //   * every global byte arrives by direct global->LDS loads
-//     (global_load_lds_dwordx4: scalar base + per-lane offset), three groups
+//     (global_load_lds_dwordx4: scalar base + per-lane offset), four groups
 //     ahead, into a 4-slot ring; every step of every wavefront issues the same
 //     number of loads (the last groups repeat the final group), so waiting
 //     for a group is one constant s_waitcnt, and the barrier then publishes
 //     the group to the workgroup;
-//   * one group ahead, the workgroup expands the shared activation and L1
-//     codes into fp8 matrix-core operands (2-slot LDS buffer).
+//   * two groups ahead, the workgroup expands the shared activation and L1
+//     codes into fp8 matrix-core operands (4-slot LDS buffer);
+//   * one group ahead, each wavefront reads its next operands into a second
+//     register set while the current group's products run;
+//   * within a step the matrix-core products of all tiles are issued before
+//     the fp32 rescaling fmas, so the matrix core and the vector ALU overlap
+//     inside each wavefront (one wavefront per SIMD, 512 registers).
 //
 // Arithmetic per 32x32 tile and group (Eq. 2): the exact integer group sum of
 // code products comes from v_mfma_scale_f32_32x32x64_f8f6f4 (codes as fp8
@@ -44,17 +48,19 @@ typedef _Float16 v4h __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int WBM = 64;     // tokens per workgroup (two 32-row tiles)
-constexpr int NWAVE = 8;    // wavefronts per workgroup
-constexpr int WPASS = 512;  // output columns per pass (8 wavefronts x 64)
-constexpr int WST = 4;      // raw ring slots
-constexpr int WDIST = 3;    // load distance in K-groups
+constexpr int NWAVE = 4;    // wavefronts per workgroup
+constexpr int WPASS = 256;  // output columns per pass (4 wavefronts x 64)
+constexpr int WST = 4;      // raw ring slots (= load distance in K-groups)
+constexpr int WUN = 4;      // expanded-operand slots
 
 template <int RT>
 struct WCfg {
-  static constexpr int HTILES = 2 * RT;   // 32x32 H tiles of a workgroup: wavefront h owns tile h
+  static constexpr int HTILES = 2 * RT;                  // 32x32 H tiles of a workgroup
+  static constexpr int HT = (HTILES + NWAVE - 1) / NWAVE;  // per wavefront: tiles w + 4 hh
+  static constexpr int HT1 = HT > 0 ? HT : 1;
   // shared loads of a group: activation blocks (2), L1 blocks (RT, first
   // pass), activation scales, weight scales, L1 scales (first pass); item q
-  // is loaded by wavefront q % 8 as its load 2 + q / 8 (loads 0 and 1 are its
+  // is loaded by wavefront q % 4 as its load 2 + q / 4 (loads 0 and 1 are its
   // own weight blocks); the other wavefronts pad with a dummy load
   static constexpr int NSH_H = 2 + RT + 3;
   static constexpr int NSH_R = 4;
@@ -64,17 +70,17 @@ struct WCfg {
   // raw slot: codes in matrix-core lane order, 1 KiB per 32-row/column block
   static constexpr int R_A = 0;                  // 2 activation blocks
   static constexpr int R_L = 2048;               // RT L1 blocks
-  static constexpr int R_B = R_L + RT * 1024;    // 16 weight blocks (2 per wavefront)
-  static constexpr int R_SA = R_B + 16384;       // 64 activation scales (first 128 B)
+  static constexpr int R_B = R_L + RT * 1024;    // 8 weight blocks (2 per wavefront)
+  static constexpr int R_SA = R_B + 8192;        // 64 activation scales (first 128 B)
   static constexpr int R_SL = R_SA + 1024;       // 32 RT L1 scales
-  static constexpr int R_SW = R_SL + 1024;       // 512 weight scales
+  static constexpr int R_SW = R_SL + 1024;       // 256 weight scales (first 512 B)
   static constexpr int R_D = R_SW + 1024;        // dummy-load target
   static constexpr int SLOT = R_D + 1024;
   // expanded slot: fp8 operands [block][half][lane][16 B]
   static constexpr int U_L = 4096;
   static constexpr int USLOT = U_L + RT * 2048;
   static constexpr int OFF_UNP = WST * SLOT;
-  static constexpr int LOOP_LDS = OFF_UNP + 2 * USLOT;
+  static constexpr int LOOP_LDS = OFF_UNP + WUN * USLOT;
   // after the first pass: H in fp32 (aliases the ring), then Q_H and s_H,
   // which later passes read, outside the ring
   static constexpr int HSTR = RT * 32 + 1;
@@ -83,7 +89,7 @@ struct WCfg {
   static constexpr int OFF_Q = LOOP_LDS;
   static constexpr int OFF_SH = OFF_Q + (RT > 0 ? WBM * QSTR : 0);
   static constexpr int LDS = OFF_SH + (RT > 0 ? WBM * RB * 4 : 0);
-  static_assert(HTILES <= NWAVE, "one H tile per wavefront");
+  static_assert(HT <= 2, "at most two H tiles per wavefront");
   static_assert(WBM * HSTR * 4 <= LOOP_LDS, "H staging fits in the ring");
   static_assert(LDS <= 160 * 1024, "fits the 160 KiB LDS of a CU");
 };
@@ -223,24 +229,29 @@ struct WKernel {
   template <bool H>
   __device__ __forceinline__ static void expand(const Ctx &c, int slot, int uslot) {
     constexpr int NCH = 64 * (2 + (H ? RT : 0));
-    static_assert(NCH <= 64 * NWAVE, "one chunk per thread");
-    const int ch = c.tid;
-    if (NCH == 64 * NWAVE || ch < NCH) {
-      const uint8_t *raw = c.smem + slot * C::SLOT + C::R_A;
-      uint8_t *d = c.smem + C::OFF_UNP + uslot * C::USLOT + (ch >> 6) * 2048 + (ch & 63) * 16;
-      const v8i u = unpack32(*reinterpret_cast<const u32x4 *>(raw + ch * 16));
-      *reinterpret_cast<u32x4 *>(d) = u32x4{(uint32_t)u[0], (uint32_t)u[1], (uint32_t)u[2], (uint32_t)u[3]};
-      *reinterpret_cast<u32x4 *>(d + 1024) =
-          u32x4{(uint32_t)u[4], (uint32_t)u[5], (uint32_t)u[6], (uint32_t)u[7]};
+    const uint8_t *raw = c.smem + slot * C::SLOT + C::R_A;
+    uint8_t *dst = c.smem + C::OFF_UNP + uslot * C::USLOT;
+#pragma unroll
+    for (int ch0 = 0; ch0 < NCH; ch0 += 64 * NWAVE) {
+      const int ch = ch0 + c.tid;
+      if (NCH % (64 * NWAVE) == 0 || ch < NCH) {
+        const v8i u = unpack32(*reinterpret_cast<const u32x4 *>(raw + ch * 16));
+        uint8_t *d = dst + (ch >> 6) * 2048 + (ch & 63) * 16;
+        *reinterpret_cast<u32x4 *>(d) = u32x4{(uint32_t)u[0], (uint32_t)u[1], (uint32_t)u[2], (uint32_t)u[3]};
+        *reinterpret_cast<u32x4 *>(d + 1024) =
+            u32x4{(uint32_t)u[4], (uint32_t)u[5], (uint32_t)u[6], (uint32_t)u[7]};
+      }
     }
   }
 
   // one group's operands for this wavefront
   struct Frags {
-    v8i a[2];        // activation rows 0-31, 32-63 (fp8)
-    u32x4 braw[2];   // this wavefront's two weight column tiles (codes)
-    v8i ah, l;       // H tile: activation rows and L1 ranks (fp8)
-    uint32_t sa[2], sb[2], sah, sl;   // scale operands (fp16 in the low half)
+    v8i a[2];              // activation rows 0-31, 32-63 (fp8)
+    u32x4 braw[2];         // this wavefront's two weight column tiles (codes)
+    v8i b[2];              // ... expanded
+    v8i ah;                // activation rows of this wavefront's H tiles (fp8)
+    v8i l[C::HT1];         // L1 ranks of its H tiles (fp8)
+    uint32_t sa[2], sb[2], sah, sl[C::HT1];   // scale operands (fp16 in the low half)
   };
 
   template <bool H>
@@ -260,60 +271,91 @@ struct WKernel {
       F.sb[j] = *reinterpret_cast<const uint16_t *>(R + C::R_SW + (64 * c.wave + 32 * j + l32) * 2);
     }
     if constexpr (H && RT > 0) {
-      // H tile of this wavefront: row tile h % 2, rank tile h / 2 (clamped for
-      // the wavefronts without one; their results are never used)
-      const int h = min(c.wave, C::HTILES - 1);
-      const int i = h & 1, rt = h >> 1;
+      // H tiles w + 4 hh: row tile w % 2 (the same for both), rank tile
+      // (w + 4 hh) / 2, clamped for the wavefronts without one (never stored)
+      const int i = c.wave & 1;
       F.ah = join(*reinterpret_cast<const u32x4 *>(U + i * 2048 + lane * 16),
                   *reinterpret_cast<const u32x4 *>(U + i * 2048 + 1024 + lane * 16));
       F.sah = *reinterpret_cast<const uint16_t *>(R + C::R_SA + (32 * i + l32) * 2);
-      F.l = join(*reinterpret_cast<const u32x4 *>(U + C::U_L + rt * 2048 + lane * 16),
-                 *reinterpret_cast<const u32x4 *>(U + C::U_L + rt * 2048 + 1024 + lane * 16));
-      F.sl = *reinterpret_cast<const uint16_t *>(R + C::R_SL + (32 * rt + l32) * 2);
+#pragma unroll
+      for (int hh = 0; hh < C::HT; hh++) {
+        const int rt = min(c.wave + NWAVE * hh, C::HTILES - 1) >> 1;
+        F.l[hh] = join(*reinterpret_cast<const u32x4 *>(U + C::U_L + rt * 2048 + lane * 16),
+                       *reinterpret_cast<const u32x4 *>(U + C::U_L + rt * 2048 + 1024 + lane * 16));
+        F.sl[hh] = *reinterpret_cast<const uint16_t *>(R + C::R_SL + (32 * rt + l32) * 2);
+      }
     }
   }
 
-  // One K-group g (ph = g % 4): wait for group g + 1, barrier, start the loads
-  // of group g + 3, expand group g + 1, then compute group g.
+  __device__ __forceinline__ static void expand_b(Frags &F) {
+    F.b[0] = unpack32(F.braw[0]);
+    F.b[1] = unpack32(F.braw[1]);
+  }
+
+  // One K-group g (ph = g % 4): wait for group g + 2, barrier, start the loads
+  // of group g + 4; issue the products of group g (operands in F), expand
+  // group g + 2 and read group g + 1's operands into N while they run, then
+  // apply the fmas of group g.
   template <bool H, int ph>
-  __device__ __forceinline__ static void step(const Ctx &c, const Plan &P, int g,
-                                              v16f (&acc)[2][2], v16f &hacc, bool hmine) {
+  __device__ __forceinline__ static void step(const Ctx &c, const Plan &P, int g, const Frags &F,
+                                              Frags &N, v16f (&acc)[2][2], v16f (&hacc)[C::HT1],
+                                              bool hmine) {
     constexpr int NL = H ? C::NL_H : C::NL_R;
     const int KG = c.KG;
-    wait_vm<NL>();                           // only group g + 2's loads may be in flight
+    wait_vm<NL>();                           // only group g + 3's loads may be in flight
     __builtin_amdgcn_s_waitcnt(0xc07f);      // lgkmcnt(0): this wavefront's LDS reads are done
     __syncthreads();
-    issue<H>(c, P, min(g + WDIST, KG - 1), (ph + WDIST) & 3);
-    expand<H>(c, (ph + 1) & 3, (ph + 1) & 1);
-    Frags F;
-    read_frags<H>(c, ph, ph & 1, F);
-    const v8i b0 = unpack32(F.braw[0]);
-    const v8i b1 = unpack32(F.braw[1]);
-    fma16(acc[0][0], codes_half(F.a[0], b0), outer2(F.sa[0], F.sb[0]));
-    fma16(acc[0][1], codes_half(F.a[0], b1), outer2(F.sa[0], F.sb[1]));
-    fma16(acc[1][0], codes_half(F.a[1], b0), outer2(F.sa[1], F.sb[0]));
-    fma16(acc[1][1], codes_half(F.a[1], b1), outer2(F.sa[1], F.sb[1]));
+    issue<H>(c, P, min(g + WST, KG - 1), ph);
+    const v16f c00 = codes_half(F.a[0], F.b[0]), p00 = outer2(F.sa[0], F.sb[0]);
+    const v16f c01 = codes_half(F.a[0], F.b[1]), p01 = outer2(F.sa[0], F.sb[1]);
+    const v16f c10 = codes_half(F.a[1], F.b[0]), p10 = outer2(F.sa[1], F.sb[0]);
+    const v16f c11 = codes_half(F.a[1], F.b[1]), p11 = outer2(F.sa[1], F.sb[1]);
+    expand<H>(c, (ph + 2) & 3, (ph + 2) & 3);
+    read_frags<H>(c, (ph + 1) & 3, (ph + 1) & 3, N);
+    fma16(acc[0][0], c00, p00);
+    fma16(acc[0][1], c01, p01);
     if constexpr (H && RT > 0) {
-      if (hmine) fma16(hacc, codes_half(F.ah, F.l), outer2(F.sah, F.sl));
+      if (hmine) {
+        const v16f ch0 = codes_half(F.ah, F.l[0]), ph0 = outer2(F.sah, F.sl[0]);
+        fma16(acc[1][0], c10, p10);
+        fma16(acc[1][1], c11, p11);
+        if constexpr (C::HT > 1) {
+          const v16f ch1 = codes_half(F.ah, F.l[1]), ph1 = outer2(F.sah, F.sl[1]);
+          fma16(hacc[0], ch0, ph0);
+          expand_b(N);
+          fma16(hacc[1], ch1, ph1);
+        } else {
+          expand_b(N);
+          fma16(hacc[0], ch0, ph0);
+        }
+        return;
+      }
     }
+    fma16(acc[1][0], c10, p10);
+    expand_b(N);
+    fma16(acc[1][1], c11, p11);
   }
 
   template <bool H>
   __device__ __forceinline__ static void k_loop(const Ctx &c, const Plan &P, v16f (&acc)[2][2],
-                                                v16f &hacc, bool hmine) {
+                                                v16f (&hacc)[C::HT1], bool hmine) {
     constexpr int NL = H ? C::NL_H : C::NL_R;
     const int KG = c.KG;
-    issue<H>(c, P, 0, 0);
-    issue<H>(c, P, min(1, KG - 1), 1);
-    issue<H>(c, P, min(2, KG - 1), 2);
-    wait_vm<2 * NL>();
+#pragma unroll
+    for (int j = 0; j < WST; j++) issue<H>(c, P, min(j, KG - 1), j);
+    wait_vm<2 * NL>();                       // groups 0 and 1 have landed
     __syncthreads();
     expand<H>(c, 0, 0);
+    expand<H>(c, 1, 1);
+    __syncthreads();
+    Frags F0, F1;
+    read_frags<H>(c, 0, 0, F0);
+    expand_b(F0);
     for (int g = 0; g < KG; g += 4) {
-      step<H, 0>(c, P, g, acc, hacc, hmine);
-      if (g + 1 < KG) step<H, 1>(c, P, g + 1, acc, hacc, hmine);
-      if (g + 2 < KG) step<H, 2>(c, P, g + 2, acc, hacc, hmine);
-      if (g + 3 < KG) step<H, 3>(c, P, g + 3, acc, hacc, hmine);
+      step<H, 0>(c, P, g, F0, F1, acc, hacc, hmine);
+      if (g + 1 < KG) step<H, 1>(c, P, g + 1, F1, F0, acc, hacc, hmine);
+      if (g + 2 < KG) step<H, 2>(c, P, g + 2, F0, F1, acc, hacc, hmine);
+      if (g + 3 < KG) step<H, 3>(c, P, g + 3, F1, F0, acc, hacc, hmine);
     }
     wait_vm<0>();
     __syncthreads();   // every wavefront is done with the ring
@@ -321,9 +363,9 @@ struct WKernel {
 };
 
 template <int RT>
-__global__ __launch_bounds__(512, 1) void dual_gemm_wide_kernel(GemmArgs a, int m_tiles,
-                                                                int n_chunks, int passes_per_wg,
-                                                                int band) {
+__global__ __launch_bounds__(64 * NWAVE, 1) void dual_gemm_wide_kernel(GemmArgs a, int m_tiles,
+                                                                       int n_chunks,
+                                                                       int passes_per_wg, int band) {
   using K_ = WKernel<RT>;
   using C = typename K_::C;
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
@@ -369,11 +411,13 @@ __global__ __launch_bounds__(512, 1) void dual_gemm_wide_kernel(GemmArgs a, int 
     __builtin_amdgcn_s_waitcnt((0x7 << 4) | (0xf << 8));   // earlier stores drained (vmcnt(0))
 
     v16f acc[2][2];
-    v16f hacc = v16f{0};
+    v16f hacc[C::HT1];
 #pragma unroll
     for (int i = 0; i < 2; i++)
 #pragma unroll
       for (int j = 0; j < 2; j++) acc[i][j] = v16f{0};
+#pragma unroll
+    for (int h = 0; h < C::HT1; h++) hacc[h] = v16f{0};
     typename K_::Plan P;
     if (do_h) {
       K_::template plan<true>(a, c, m0, n0, P);
@@ -391,11 +435,18 @@ __global__ __launch_bounds__(512, 1) void dual_gemm_wide_kernel(GemmArgs a, int 
       if (do_h) {
         // ---- H -> LDS (fp32), then per-token, per-rank-group requantization ----
         if (hmine) {
-          const int i = wave & 1, rt = wave >> 1;
+          const int i = wave & 1;
 #pragma unroll
-          for (int v = 0; v < 16; v++) {
-            const int row = 32 * i + row_of_32x32(lane, v);
-            HS[row * C::HSTR + rt * 32 + (lane & 31)] = hacc[v];
+          for (int hh = 0; hh < C::HT; hh++) {
+            const int h = wave + NWAVE * hh;
+            if (h < C::HTILES) {
+              const int rt = h >> 1;
+#pragma unroll
+              for (int v = 0; v < 16; v++) {
+                const int row = 32 * i + row_of_32x32(lane, v);
+                HS[row * C::HSTR + rt * 32 + (lane & 31)] = hacc[hh][v];
+              }
+            }
           }
         }
         if (r < C::RB * 64) {   // zero the fp8 padding ranks [r, 64 RB) of Q_H

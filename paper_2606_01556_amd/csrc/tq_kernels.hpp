@@ -43,5 +43,6 @@ hipError_t launch_export(const Geometry &g, const uint8_t *packed, uint32_t *wc,
 hipError_t launch_dual_gemm(const GemmArgs &a, hipStream_t s);
 hipError_t launch_dual_gemm_small(const GemmArgs &a, hipStream_t s);   // m <= 16
 hipError_t launch_dual_gemm_wide(const GemmArgs &a, hipStream_t s);    // prefill sizes
+hipError_t launch_dual_gemm_stream(const GemmArgs &a, hipStream_t s);  // prefill sizes
 
 }  // namespace tq
