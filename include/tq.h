@@ -101,11 +101,18 @@ tq_status tq_pack_weights(const tq_weight_desc *d, const void *w_res, const void
 /* Per-token, per-group activation quantizer (Sec. 2 Eq. 1; Sec. 4.3: the
  * activation is quantized once and shared by both branches).
  *   x         [m,k] fp16 row-major, m >= 0, k % group == 0, group == 64
- *   x_codes   [m, k/8] TQ4 code words (m*k/2 bytes), row-major
- *   x_scales  [k/group, m8] fp16 with m8 = m rounded up to a multiple of 8:
- *             the scale of token i, group g is x_scales[g*m8 + i]
- *             (group-major, so one group's scales of a token tile are
- *             contiguous and 16-byte aligned); entries i in [m, m8) are 0
+ *   x_codes   m32 * k / 2 bytes, m32 = m rounded up to a multiple of 32:
+ *             tile-major TQ4 codes.  The tokens are cut into tiles of 32 and
+ *             K into groups of 64; tile t, group g is one 1 KiB block at byte
+ *             (t * (k / 64) + g) * 1024, whose 16-byte lane slot 32 h + i
+ *             (h = 0, 1; i = 0 .. 31) holds the four TQ4 words of codes
+ *             32 h .. 32 h + 31 of the group for token 32 t + i (the order in
+ *             which the matrix cores take one operand of a 32 x 32 x 64
+ *             product, so each block is one coalesced load).  Tokens
+ *             [m, m32) get zero codes.
+ *   x_scales  [k/group, m32] fp16: the scale of token i, group g is
+ *             x_scales[g*m32 + i] (group-major, so one group's scales of a
+ *             token tile are contiguous); entries i in [m, m32) are 0
  * m == 0 is a no-op.  Errors: TQ_ERR_NULL, TQ_ERR_SHAPE, TQ_ERR_GROUP,
  * TQ_ERR_ALIGN, TQ_ERR_HIP. */
 tq_status tq_quant_act(const void *x, int m, int k, int group, void *x_codes,

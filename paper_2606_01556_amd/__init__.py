@@ -133,16 +133,19 @@ def empty_packed(desc: WeightDesc, device="cuda"):
     return torch.empty(int(desc.packed_bytes), dtype=torch.uint8, device=device)
 
 
-def scale_stride(m: int) -> int:
-    """Row stride of x_scales: the token count rounded up to a multiple of 8."""
-    return (m + 7) // 8 * 8
+def padded_tokens(m: int) -> int:
+    """m32: the token count rounded up to the 32-token activation tile (at least 32)."""
+    return max((m + 31) // 32 * 32, 32)
 
 
 def empty_act(m: int, k: int, device="cuda"):
-    """(x_codes [m, k/8] int32 TQ4 words, x_scales [k/64, m8] fp16, m8 = scale_stride(m))."""
+    """(x_codes, x_scales) buffers for tq_quant_act / tq_dual_gemm:
+    x_codes [m32/32, k/64, 256] int32 (one 1 KiB tile-major block per 32
+    tokens and K-group), x_scales [k/64, m32] fp16, m32 = padded_tokens(m)."""
     import torch
-    return (torch.empty((m, k // 8), dtype=torch.int32, device=device),
-            torch.empty((k // GROUP, max(scale_stride(m), 8)), dtype=torch.float16, device=device))
+    m32 = padded_tokens(m)
+    return (torch.empty((m32 // 32, k // GROUP, 256), dtype=torch.int32, device=device),
+            torch.empty((k // GROUP, m32), dtype=torch.float16, device=device))
 
 
 class Layer:
@@ -196,3 +199,13 @@ def tq4_encode(codes) -> np.ndarray:
         w |= mag[..., 4 + i] << (8 * i + 4)
         w |= neg[..., 4 + i] << (8 * ((i + 1) % 4) + 3)
     return w
+
+
+def act_codes_rows(x_codes, m: int) -> np.ndarray:
+    """Tile-major activation codes (host copy of x_codes) -> int8 codes [m, k]
+    (host side, for inspection and tests)."""
+    w = np.ascontiguousarray(x_codes).view(np.uint32)
+    tiles, kg = w.shape[0], w.shape[1]
+    w = w.reshape(tiles, kg, 2, 32, 4)            # tile, group, half, token, word
+    w = w.transpose(0, 3, 1, 2, 4)                 # tile, token, group, half, word
+    return tq4_decode(w.reshape(tiles * 32, kg * 8))[:m]

@@ -112,7 +112,7 @@ static tq_status dual_gemm_impl(const tq_weight_desc *d, const void *packed, con
   a.xs = static_cast<const uint16_t *>(x_scales);
   a.y = y;
   a.m = m;
-  a.ms = (m + 7) / 8 * 8;
+  a.ms = (m + 31) / 32 * 32;
   a.bf16_out = y_dtype == TQ_BF16;
   a.dbg_h = static_cast<float *>(h);
   a.dbg_sh = static_cast<float *>(sh);

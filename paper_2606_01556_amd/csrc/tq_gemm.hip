@@ -126,12 +126,11 @@ struct TileKernel {
     const uint8_t *wscales = a.packed + geo.off_ws;
     const uint8_t *l1codes = a.packed + geo.off_l1;
     const uint8_t *l1scales = a.packed + geo.off_l1s;
-    const int64_t xrow_bytes = geo.k / 2;
-    // activation codes of row min(m0 + 32 s + lane % 32, m - 1), k half lane / 32
+    // activation tile of rows m0 + 32 s .. + 32 (clamped to the last tile)
     auto a_block = [&](int s, const uint8_t *&b, uint32_t &inc) {
-      const int row = min(m0 + s * 32 + (lane & 31), m - 1);
-      b = xc + row * xrow_bytes + (lane >> 5) * 16;
-      inc = 32;
+      const int t = min(m0 / 32 + s, (m - 1) / 32);
+      b = xc + ((int64_t)t * KG * 64 + lane) * 16;
+      inc = 1024;
     };
     constexpr int NL = H ? C::NL_H : C::NL_R;
 #pragma unroll
@@ -547,11 +546,9 @@ static hipError_t launch_rt(const GemmArgs &a, hipStream_t s, int tpw) {
 
 hipError_t launch_dual_gemm(const GemmArgs &a, hipStream_t s) {
   if (a.m <= 16) return launch_dual_gemm_small(a, s);
-  // kernel family override for tuning sweeps: TQ_PATH=tile|wide
+  // kernel family override for tuning sweeps: TQ_PATH=tile|prefill
   const char *path = getenv("TQ_PATH");
-  if (path && path[0] == 's') return launch_dual_gemm_stream(a, s);
-  const bool wide = path ? path[0] == 'w' : a.m >= 1024;
-  if (wide) return launch_dual_gemm_wide(a, s);
+  if (path ? path[0] == 'p' : a.m >= 1024) return launch_dual_gemm_prefill(a, s);
   // tile shape override for tuning sweeps: TQ_TILE="TMxTN[:tiles_per_wg]"
   int tm = 0, tn = 0, tpw = 0;
   if (const char *env = getenv("TQ_TILE")) sscanf(env, "%dx%d:%d", &tm, &tn, &tpw);

@@ -1,0 +1,704 @@
+// Fused dual-component W4A4 layer (paper Sec. 4.3) for prefill-sized token
+// counts: the residual 4-bit GEMM, the stage-1 product H = Q(X) Q(L1) kept on
+// chip, its on-the-fly re-quantization, stage 2 Q_H Q(L2) and one epilogue,
+// in one kernel.
+//
+// Work decomposition.  A workgroup of 8 wavefronts (two per SIMD) owns a block
+// of 128 tokens and a run of 256-column blocks.  Wavefront w = 4 wr + wc
+// computes tokens [64 wr, +64) x columns [64 wc, +64) of a block: four 32x32
+// tiles.  During the first column block of its run the workgroup also forms H
+// for its 128 tokens: 4 x (r / 32) tiles of 32 tokens x 32 ranks, one or two
+// per wavefront, each accumulated in ascending K-group order (the oracle's
+// order, so H is bit-identical).  After that block H is re-quantized into LDS;
+// later blocks of the run reuse Q_H and s_H.
+//
+// K pipeline.  Everything a K-group needs -- the 128 activation rows, the 256
+// weight columns, the rank columns of L1 (first block only) and all their
+// scales -- arrives once per workgroup by direct global->LDS loads
+// (global_load_lds_dwordx4) into a D-slot ring, D - 1 groups ahead; the loads
+// of a group are spread over the 8 wavefronts.  One workgroup barrier per
+// group publishes the group and frees the slot read in the previous step.
+// Each step issues the matrix-core products of group g first, then passes the
+// barrier, starts the loads of group g + D, reads and expands group g + 1's
+// operands, and applies group g's fp32 rescaling fmas, so the matrix core and
+// the vector ALU overlap inside a wavefront and across the two wavefronts of
+// a SIMD.
+//
+// Arithmetic per 32x32 tile and group (Eq. 2): the exact integer group sum of
+// code products comes from v_mfma_scale_f32_32x32x64_f8f6f4 (codes as fp8
+// subnormals; block scales 2^8 and 2^9 return half of the integer sum), the
+// exact scale product from v_mfma_f32_32x32x8f16 with both scale operands
+// placed in k = 0 and k = 4 (twice the product), and one fma adds their
+// product -- exactly I * s_x * s_w -- to the fp32 accumulator in ascending
+// group order, the oracle's order for H and for the residual, so Y is
+// bit-identical to the oracle's rounded result.
+#include <stdio.h>
+#include <stdlib.h>
+
+#include <type_traits>
+
+#include "tq_device.hpp"
+#include "tq_kernels.hpp"
+
+namespace tq {
+namespace {
+
+typedef _Float16 v4h __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int PBM = 128;   // tokens per workgroup block (four 32-row tiles)
+constexpr int PBN = 256;   // columns per block (eight 32-column tiles)
+constexpr int PNW = 8;     // wavefronts per workgroup
+// one ring slot (one K-group).  Main loop: activation tiles, weight tiles,
+// activation and weight scales.  H pass: activation tiles, L1 rank tiles in
+// place of the weight tiles, activation and L1 scales.  Every load is one
+// 16-byte-per-lane wave load; the scale runs fill part of a 1 KiB region.
+constexpr int P_A = 0;          // 4 x 1 KiB activation tiles, matrix-core lane order
+constexpr int P_B = 4096;       // 8 x 1 KiB weight blocks as stored (H pass: L1 blocks)
+constexpr int P_SX = 12288;     // activation scales of the 128 tokens (256 B)
+constexpr int P_SW = 13312;     // weight scales of the 256 columns (H pass: L1 scales)
+constexpr int P_STAGE = 14336;
+
+template <int RT, int D>
+struct PCfg {
+  static constexpr int STAGE = P_STAGE;
+  static constexpr int RING = D * STAGE;
+  static constexpr int RB = (RT + 1) / 2;            // 64-rank blocks (= rank groups)
+  static constexpr int HSTR = RT * 32 + 1;           // fp32 H staging: row stride in floats
+  static constexpr int QSTR = RB * 64 + 16;          // Q_H bytes per token row
+  static constexpr int OFF_Q = RING;
+  static constexpr int OFF_SH = OFF_Q + (RT > 0 ? PBM * QSTR : 0);
+  // stage-2 operands of each wavefront, loaded while the K loop starts:
+  // its 2 x RB L2 blocks, then a 1 KiB scale region
+  static constexpr int L2W = 2 * RB * 1024 + 1024;
+  static constexpr int OFF_L2 = OFF_SH + (RT > 0 ? RB * PBM * 4 : 0);
+  static constexpr int LDS = OFF_L2 + (RT > 0 ? PNW * L2W : 0);
+  static constexpr int HT = RT >= 2 ? RT / 2 : 1;    // H tiles of an H wavefront
+  static_assert(PBM * HSTR * 4 <= RING, "H staging fits in the ring");
+  static_assert(LDS <= 160 * 1024, "fits the 160 KiB LDS of a CU");
+};
+
+// exact scale products of a 32x32 tile: lane l carries s[l % 32] in k = 0
+// (lanes 0-31) and k = 4 (lanes 32-63) of both operands, so the result is
+// 2 * s_row * s_col
+__device__ __forceinline__ v16f outer2(uint32_t sa, uint32_t sb) {
+  const v16f z = {0};
+  const u32x2 a2 = {sa, 0u}, b2 = {sb, 0u};
+  return __builtin_amdgcn_mfma_f32_32x32x8f16(__builtin_bit_cast(v4h, a2),
+                                              __builtin_bit_cast(v4h, b2), z, 0, 0, 0);
+}
+
+// half of the exact integer group sum of a 32x32 tile of code products
+__device__ __forceinline__ v16f codes_half(v8i a, v8i b) {
+  const v16f z = {0};
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, z, 0, 0, 0, kScale2p9 - 1, 0,
+                                                         kScale2p9);
+}
+
+__device__ __forceinline__ void fma16(v16f &acc, const v16f &c, const v16f &p) {
+#pragma unroll
+  for (int v = 0; v < 16; v++) acc[v] = fmaf(c[v], p[v], acc[v]);
+}
+
+__device__ __forceinline__ v8i join(u32x4 lo, u32x4 hi) {
+  return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+}
+
+// s_waitcnt vmcnt(n) (n < 64), leaving the other counters alone
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt has 6 bits");
+  __builtin_amdgcn_s_waitcnt((N & 0xf) | ((N >> 4) << 14) | (0x7 << 4) | (0xf << 8));
+}
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xc07f); }
+
+// direct global -> LDS load of 16 bytes per lane into lds + 16 * lane:
+// scalar base + 32-bit lane offset
+__device__ __forceinline__ void dma_s(uint32_t voff, const uint8_t *sbase, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase),
+               "s"(lds)
+               : "memory");
+}
+__device__ __forceinline__ void dma_v(const uint8_t *addr, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(addr), "s"(lds)
+               : "memory");
+}
+
+// wave-uniform 64-bit pointer, kept in scalar registers
+__device__ __forceinline__ const uint8_t *uniform_ptr(const uint8_t *p) {
+  const uint64_t v = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return reinterpret_cast<const uint8_t *>(((uint64_t)hi << 32) | lo);
+}
+
+// This wavefront's share of one K-group's loads: exactly two 16-byte-per-lane
+// wave loads, so every wavefront has the same number in flight per group and
+// the K loop has no branches.  Item t reads b[t] + g * inc[t] + v[t] (lane).
+struct PPlan {
+  const uint8_t *b1, *b2;     // wave-uniform bases of group 0
+  uint32_t inc1, inc2;        // bytes per K-group
+  uint32_t v1, v2;            // lane offsets
+  uint32_t l1, l2;            // LDS offsets within a slot
+};
+
+__device__ __forceinline__ void p_issue(const PPlan &P, int g, uint32_t slot_lds) {
+  dma_s(P.v1, uniform_ptr(P.b1 + (uint64_t)g * P.inc1), slot_lds + P.l1);
+  dma_s(P.v2, uniform_ptr(P.b2 + (uint64_t)g * P.inc2), slot_lds + P.l2);
+}
+
+// activation tile t of the block (clamped to the last tile): its group-0
+// block; the tile of one group is 1 KiB in matrix-core lane order
+__device__ __forceinline__ const uint8_t *act_tile(const GemmArgs &a, int m0, int t) {
+  const int tt = min(m0 / 32 + t, (a.m - 1) / 32);
+  return reinterpret_cast<const uint8_t *>(a.xc) + (int64_t)tt * (a.geo.k / kGroup) * 1024;
+}
+
+// activation scales of the block's 128 tokens: eight per lane for lanes 0-15
+// (the other lanes repeat lane 15's run), clamped to the padded row count ms
+__device__ __forceinline__ void plan_xs(const GemmArgs &a, int m0, int lane, const uint8_t *&b,
+                                        uint32_t &inc, uint32_t &v) {
+  b = reinterpret_cast<const uint8_t *>(a.xs) + (int64_t)m0 * 2;
+  inc = (uint32_t)a.ms * 2;
+  v = (uint32_t)(min(m0 + 8 * min(lane, 15), a.ms - 8) - m0) * 2;
+}
+
+// Main loop: wavefront w loads weight tile w and, as its second item,
+// activation tile w (w < 4), the weight scales of the 256 columns (w = 4,
+// eight per lane for lanes 0-31) or the activation scales (w >= 5; the three
+// wavefronts load the same bytes to the same place).
+__device__ __forceinline__ void plan_main(const GemmArgs &a, int lane, int wave, int m0, int n0,
+                                          PPlan &P) {
+  const Geometry &geo = a.geo;
+  const int KG = geo.k / kGroup;
+  const int ct = min(n0 / 32 + wave, geo.n_pad / 32 - 1);   // past the last tile: never stored
+  P.b1 = a.packed + geo.off_w + (int64_t)ct * KG * 1024;
+  P.inc1 = 1024;
+  P.v1 = lane * 16;
+  P.l1 = P_B + wave * 1024;
+  if (wave < 4) {
+    P.b2 = act_tile(a, m0, wave);
+    P.inc2 = 1024;
+    P.v2 = lane * 16;
+    P.l2 = P_A + wave * 1024;
+  } else if (wave == 4) {
+    P.b2 = a.packed + geo.off_ws + (int64_t)n0 * 2;
+    P.inc2 = (uint32_t)geo.n_pad * 2;
+    P.v2 = (uint32_t)(min(n0 + 8 * min(lane, 31), geo.n_pad - 8) - n0) * 2;
+    P.l2 = P_SW;
+  } else {
+    plan_xs(a, m0, lane, P.b2, P.inc2, P.v2);
+    P.l2 = P_SX;
+  }
+}
+
+// H pass.  A step covers HG consecutive K-groups (HG = 2 for up to 64 ranks,
+// 1 for 128), laid out in a slot as: activation tiles of group e at
+// 4096 e; L1 rank tile t of group e at P_B + 4096 + 1024 (e RT + t) -- P_B +
+// 1024 (e RT + t) for RT > 2 --; scales at P_SX: activation scales of group e
+// at P_SX + 512 e, L1 scales at P_SX + 256 + 512 e.  Every item is a wave load
+// whose lane l reads 16 bytes at base[l] + g(l) * stride[l], g(l) the lane's
+// group clamped to the last one.
+constexpr int H_L1 = 8192, H_S = 12288;
+
+struct HPlan {
+  const uint8_t *base[2];   // lane addresses for group 0
+  uint32_t stride[2];       // lane bytes per group
+  int e[2];                 // lane group offset within the step (0 .. HG-1)
+  uint32_t lds[2];          // wave-uniform LDS offset within a slot
+};
+
+__device__ __forceinline__ void h_issue(const HPlan &P, int g0, int KG, uint32_t slot_lds) {
+#pragma unroll
+  for (int t = 0; t < 2; t++) {
+    const int g = min(g0 + P.e[t], KG - 1);
+    dma_v(P.base[t] + (uint64_t)g * P.stride[t], slot_lds + P.lds[t]);
+  }
+}
+
+// items, in order: HG x 4 activation tiles, HG x RT L1 tiles, one scale item,
+// then repeats of earlier items (same bytes to the same place); wavefront w
+// takes items w and w + 8
+__device__ __forceinline__ void plan_h(const GemmArgs &a, int lane, int wave, int m0, int RT,
+                                       int HG, HPlan &P) {
+  const Geometry &geo = a.geo;
+  const int KG = geo.k / kGroup;
+  const int nitem = HG * 4 + HG * RT + 1;
+#pragma unroll
+  for (int t = 0; t < 2; t++) {
+    int it = wave + 8 * t;
+    if (it >= nitem) it -= 8;   // a repeat of item it - 8
+    if (it < HG * 4) {          // activation tile it % 4 of group it / 4
+      const int e = it >> 2, tt = it & 3;
+      P.base[t] = act_tile(a, m0, tt) + lane * 16;
+      P.stride[t] = 1024;
+      P.e[t] = e;
+      P.lds[t] = P_A + 4096 * e + 1024 * tt;
+    } else if (it < HG * 4 + HG * RT) {   // L1 rank tile tt of group e
+      const int q = it - HG * 4, e = q / RT, tt = q % RT;
+      P.base[t] = a.packed + geo.off_l1 + (int64_t)tt * KG * 1024 + lane * 16;
+      P.stride[t] = 1024;
+      P.e[t] = e;
+      P.lds[t] = (RT > 2 ? P_B : H_L1) + 1024 * (e * RT + tt);
+    } else {   // scales: lanes 16 e + (0-15): activation (even) or L1 (odd) runs
+      const int q = lane >> 4, e = min(q >> 1, HG - 1), r = lane & 15;
+      if ((q & 1) == 0) {
+        P.base[t] = reinterpret_cast<const uint8_t *>(a.xs) +
+                    (int64_t)min(m0 + 8 * r, a.ms - 8) * 2;
+        P.stride[t] = (uint32_t)a.ms * 2;
+      } else {
+        P.base[t] = a.packed + geo.off_l1s + (int64_t)min(8 * r, geo.r_pad32 - 8) * 2;
+        P.stride[t] = (uint32_t)geo.r_pad32 * 2;
+      }
+      P.e[t] = e;
+      P.lds[t] = H_S;
+    }
+  }
+}
+
+template <int RT, int D>
+struct PKernel {
+  using C = PCfg<RT, D>;
+
+  // prologue of a K loop: groups 0 .. D-1 into slots 0 .. D-1 (past the end:
+  // the last group again, so every step waits for the same count); returns
+  // when group 0 is visible to the workgroup
+  template <typename Pre>
+  __device__ __forceinline__ static void prologue(const PPlan &P, uint32_t ring_lds, int KG,
+                                                  Pre pre) {
+    // Every load the compiler itself issued (e.g. spill reloads) is complete
+    // here, so it has no reason to wait on the vector-memory counter inside
+    // the K loop -- a wait there would also drain the ring's loads.
+    wait_vm<0>();
+    pre();   // loads issued here complete before the ring's first group
+#pragma unroll
+    for (int s = 0; s < D; s++) p_issue(P, min(s, KG - 1), ring_lds + s * C::STAGE);
+    wait_vm<2 * (D - 1)>();
+    __syncthreads();
+  }
+
+  // one step's hand-over: group g + 1 has landed (own loads), this wavefront's
+  // reads are done, every wavefront is past step g - 1, so group g + 1 is
+  // visible and slot g % D is free for group g + D
+  __device__ __forceinline__ static void advance(const PPlan &P, uint32_t ring_lds, int g, int KG) {
+    wait_vm<2 * (D - 2)>();
+    wait_lgkm0();
+    __syncthreads();
+    p_issue(P, min(g + D, KG - 1), ring_lds + (g % D) * C::STAGE);
+  }
+
+  struct Raw {
+    u32x4 a[2], b[2];
+    uint32_t sa[2], sb[2];
+  };
+
+  __device__ __forceinline__ static void read_raw(const uint8_t *S, int lane, int wr, int wc,
+                                                  Raw &R) {
+    const int l32 = lane & 31;
+#pragma unroll
+    for (int i = 0; i < 2; i++) {
+      const int ti = 2 * wr + i;
+      R.a[i] = *reinterpret_cast<const u32x4 *>(S + P_A + ti * 1024 + lane * 16);
+      R.sa[i] = *reinterpret_cast<const uint16_t *>(S + P_SX + (32 * ti + l32) * 2);
+    }
+#pragma unroll
+    for (int j = 0; j < 2; j++) {
+      const int tj = 2 * wc + j;
+      R.b[j] = *reinterpret_cast<const u32x4 *>(S + P_B + tj * 1024 + lane * 16);
+      R.sb[j] = *reinterpret_cast<const uint16_t *>(S + P_SW + (32 * tj + l32) * 2);
+    }
+  }
+
+  // The residual K loop of one column block: this wavefront's 2 x 2 tiles,
+  // ascending K-groups.  The eight matrix-core instructions of a group (code
+  // product c and scale product p of tiles 00, 01, 10, 11) are each followed
+  // by independent vector work -- operand expansion, or the fmas of a tile
+  // whose products were issued two matrix instructions earlier -- so the
+  // matrix core and the vector ALU overlap inside the wavefront without
+  // dependency stalls.  Only tile 11's products are carried into the next
+  // group.  Each accumulator still receives its fmas in ascending group order.
+  // (Each region between scheduling barriers is pinned to "one matrix-core
+  // instruction, then the vector work".)
+  template <typename Pre>
+  __device__ __forceinline__ static void main_loop(const PPlan &P, uint8_t *smem,
+                                                   uint32_t ring_lds, int KG, int lane, int wr,
+                                                   int wc, v16f (&acc)[2][2], Pre pre) {
+    prologue(P, ring_lds, KG, pre);
+    Raw R;
+    read_raw(smem, lane, wr, wc, R);
+    v8i a0 = unpack32(R.a[0]);
+    v8i b0 = unpack32(R.b[0]);
+    // tile 11's products of the previous group (none yet: fma(0, 0, +0)
+    // leaves the accumulator at +0)
+    v16f c11 = v16f{0}, p11 = v16f{0};
+    for (int g = 0; g < KG; g++) {
+      const v16f c00 = codes_half(a0, b0);
+      fma16(acc[1][1], c11, p11);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      const v16f p00 = outer2(R.sa[0], R.sb[0]);
+      const v8i b1 = unpack32(R.b[1]);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 12, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      const v16f c01 = codes_half(a0, b1);
+      const v8i a1 = unpack32(R.a[1]);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 12, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      const v16f p01 = outer2(R.sa[0], R.sb[1]);
+      fma16(acc[0][0], c00, p00);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      advance(P, ring_lds, g, KG);
+      Raw Rn;
+      read_raw(smem + ((g + 1) % D) * C::STAGE, lane, wr, wc, Rn);
+      asm volatile("" ::: "memory");   // issue the reads here, ahead of their use
+      __builtin_amdgcn_sched_barrier(0);
+      const v16f c10 = codes_half(a1, b0);
+      __builtin_amdgcn_sched_barrier(0);
+      const v16f p10 = outer2(R.sa[1], R.sb[0]);
+      fma16(acc[0][1], c01, p01);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      c11 = codes_half(a1, b1);
+      a0 = unpack32(Rn.a[0]);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 12, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      p11 = outer2(R.sa[1], R.sb[1]);
+      fma16(acc[1][0], c10, p10);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      b0 = unpack32(Rn.b[0]);
+      R = Rn;
+    }
+    fma16(acc[1][1], c11, p11);
+    wait_vm<0>();   // the refills past the end have landed before the ring is reused
+  }
+
+  // The stage-1 pass: H tiles of 32 tokens x 32 ranks, accumulated over all
+  // K-groups in ascending order (token tile ti, rank tiles hrt[]), HG groups
+  // per ring slot and step.
+  static constexpr int HG = RT > 2 ? 1 : 2;
+  __device__ __forceinline__ static void h_loop(const HPlan &P, uint8_t *smem, uint32_t ring_lds,
+                                                int KG, int lane, bool hw, int ti,
+                                                const int (&hrt)[C::HT], v16f (&hacc)[C::HT]) {
+    const int NS = (KG + HG - 1) / HG;   // steps
+    wait_vm<0>();
+#pragma unroll
+    for (int s = 0; s < D; s++) h_issue(P, min(s, NS - 1) * HG, KG, ring_lds + s * C::STAGE);
+    wait_vm<2 * (D - 1)>();
+    __syncthreads();
+    const int l32 = lane & 31;
+    for (int s = 0; s < NS; s++) {
+      const uint8_t *S = smem + (s % D) * C::STAGE;
+      u32x4 ra[HG], rl[HG][C::HT];
+      uint32_t sa[HG], sl[HG][C::HT];
+      if (hw) {
+#pragma unroll
+        for (int e = 0; e < HG; e++) {
+          ra[e] = *reinterpret_cast<const u32x4 *>(S + P_A + 4096 * e + ti * 1024 + lane * 16);
+          sa[e] = *reinterpret_cast<const uint16_t *>(S + H_S + 512 * e + (32 * ti + l32) * 2);
+#pragma unroll
+          for (int h = 0; h < C::HT; h++) {
+            rl[e][h] = *reinterpret_cast<const u32x4 *>(
+                S + (RT > 2 ? P_B : H_L1) + 1024 * (e * RT + hrt[h]) + lane * 16);
+            sl[e][h] = *reinterpret_cast<const uint16_t *>(S + H_S + 256 + 512 * e +
+                                                           (32 * hrt[h] + l32) * 2);
+          }
+        }
+      }
+      // step s + 1 has landed and every wavefront is done with slot s
+      wait_vm<2 * (D - 2)>();
+      wait_lgkm0();
+      __syncthreads();
+      h_issue(P, min(s + D, NS - 1) * HG, KG, ring_lds + (s % D) * C::STAGE);
+      if (hw) {
+#pragma unroll
+        for (int e = 0; e < HG; e++) {
+          if (s * HG + e < KG) {
+            const v8i av = unpack32(ra[e]);
+#pragma unroll
+            for (int h = 0; h < C::HT; h++) {
+              const v16f ch = codes_half(av, unpack32(rl[e][h]));
+              const v16f ph = outer2(sa[e], sl[e][h]);
+              fma16(hacc[h], ch, ph);
+            }
+          }
+        }
+      }
+    }
+    wait_vm<0>();
+  }
+};
+
+template <int RT, int D>
+__global__ __launch_bounds__(64 * PNW, 1) void dual_gemm_prefill_kernel(GemmArgs a, int m_tiles,
+                                                                        int n_tiles, int n_chunks,
+                                                                        int cpw, int band) {
+  using K = PKernel<RT, D>;
+  using C = PCfg<RT, D>;
+  extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
+  const Geometry &geo = a.geo;
+  const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wr = wave >> 2, wc = wave & 3;
+  const int KG = geo.k / kGroup;
+  const int m = a.m;
+  const int ctiles = geo.n_pad / 32;
+  const uint32_t ring_lds = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)smem);
+
+  // Workgroups are dealt round-robin to the 8 XCDs: give each XCD a
+  // contiguous run of logical ids, ordered in bands of `band` token blocks,
+  // column chunk by column chunk, so the workgroups of an XCD share their
+  // activation rows and weight columns in its L2.
+  int logical;
+  {
+    const int nwg = gridDim.x, per = nwg / 8, rem = nwg % 8;
+    const int x = blockIdx.x % 8, s = blockIdx.x / 8;
+    logical = (x < rem ? x * (per + 1) : rem * (per + 1) + (x - rem) * per) + s;
+  }
+  const int bsz = band * n_chunks;
+  const int bidx = logical / bsz, brem = logical % bsz;
+  const int rows_in_band = min(band, m_tiles - bidx * band);
+  const int chunk = brem / rows_in_band;
+  const int m_tile = bidx * band + brem % rows_in_band;
+  const int m0 = m_tile * PBM;
+  const int cb_begin = chunk * cpw;
+  const int cb_end = min(cb_begin + cpw, n_tiles);
+
+  // H tiles of this wavefront in the stage-1 pass: token tile hti, rank
+  // tiles hrt[] (RT = 1: wavefronts 0-3, one per SIMD)
+  const int hti = wave & 3;
+  const bool hw = RT >= 2 || (RT == 1 && wave < 4);
+  int hrt[C::HT];
+#pragma unroll
+  for (int h = 0; h < C::HT; h++) hrt[h] = RT >= 2 ? (wave >> 2) + 2 * h : 0;
+
+  const uint8_t *l2codes = a.packed + geo.off_l2;
+  const uint16_t *l2scales = reinterpret_cast<const uint16_t *>(a.packed + geo.off_l2s);
+
+  for (int cb = cb_begin; cb < cb_end; cb++) {
+    const int n0 = cb * PBN;
+    if constexpr (RT > 0) {
+      if (cb == cb_begin) {
+        // ---- stage 1: H for the block's 128 tokens, then Q_H and s_H in LDS ----
+        HPlan HP;
+        plan_h(a, lane, wave, m0, RT, K::HG, HP);
+        v16f hacc[C::HT];
+#pragma unroll
+        for (int h = 0; h < C::HT; h++) hacc[h] = v16f{0};
+        K::h_loop(HP, smem, ring_lds, KG, lane, hw, hti, hrt, hacc);
+        __syncthreads();   // every wavefront is done with the ring
+        float *HS = reinterpret_cast<float *>(smem);
+        uint8_t *QS = smem + C::OFF_Q;
+        float *SHS = reinterpret_cast<float *>(smem + C::OFF_SH);
+        const int r = geo.r, gr = geo.gr, rg = r / gr;
+        if (hw) {
+#pragma unroll
+          for (int h = 0; h < C::HT; h++) {
+#pragma unroll
+            for (int v = 0; v < 16; v++) {
+              const int row = 32 * hti + row_of_32x32(lane, v);
+              HS[row * C::HSTR + hrt[h] * 32 + l32] = hacc[h][v];
+            }
+          }
+        }
+        if (r < C::RB * 64) {   // zero the fp8 padding ranks [r, 64 RB) of Q_H
+          for (int idx = tid; idx < PBM * C::RB * 64; idx += 64 * PNW) {
+            const int row = idx / (C::RB * 64), j = idx % (C::RB * 64);
+            if (j >= r) QS[row * C::QSTR + j] = 0;
+          }
+        }
+        __syncthreads();
+        // per-token, per-rank-group re-quantization (s_H in fp32)
+        const int subs = gr / 8;   // lanes per (token, rank group): 1, 2, 4 or 8
+        const int work = PBM * rg * subs;
+        const bool dbg = a.dbg_h != nullptr && chunk == 0;
+        for (int base = 0; base < work; base += 64 * PNW) {
+          const int idx = base + tid;
+          const bool valid = idx < work;
+          const int pair = idx / subs, sub = idx % subs;
+          const int row = pair / rg, hg = pair % rg;
+          const int j0 = hg * gr + sub * 8;
+          float hv[8];
+          float amax = 0.0f;
+#pragma unroll
+          for (int e = 0; e < 8; e++) {
+            hv[e] = valid ? HS[row * C::HSTR + j0 + e] : 0.0f;
+            amax = fmaxf(amax, fabsf(hv[e]));
+          }
+          for (int msk = 1; msk < subs; msk <<= 1) amax = fmaxf(amax, __shfl_xor(amax, msk));
+          const float s = amax / 7.0f;   // IEEE division; s_H stays fp32
+          if (valid) {
+            uint32_t w0 = 0, w1 = 0;
+#pragma unroll
+            for (int e = 0; e < 8; e++) {
+              int q = 0;
+              if (s != 0.0f) {
+                float tq = __builtin_rintf(hv[e] / s);
+                tq = tq > 7.0f ? 7.0f : (tq < -7.0f ? -7.0f : tq);
+                q = (int)tq;
+              }
+              const uint32_t b = code_to_fp8(q);
+              if (e < 4) w0 |= b << (8 * e); else w1 |= b << (8 * (e - 4));
+              if (dbg && m0 + row < m) {
+                a.dbg_h[(int64_t)(m0 + row) * r + j0 + e] = hv[e];
+                a.dbg_qh[(int64_t)(m0 + row) * r + j0 + e] = (int8_t)q;
+              }
+            }
+            *reinterpret_cast<uint32_t *>(QS + row * C::QSTR + j0) = w0;
+            *reinterpret_cast<uint32_t *>(QS + row * C::QSTR + j0 + 4) = w1;
+            if (sub == 0) {
+              SHS[hg * PBM + row] = s;
+              if (dbg && m0 + row < m) a.dbg_sh[(int64_t)(m0 + row) * rg + hg] = s;
+            }
+          }
+        }
+        __syncthreads();   // Q_H and s_H are published; the ring is free
+      }
+    }
+
+    // ---- residual 4-bit GEMM of the block ----
+    PPlan P;
+    plan_main(a, lane, wave, m0, n0, P);
+    v16f acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; i++)
+#pragma unroll
+      for (int j = 0; j < 2; j++) acc[i][j] = v16f{0};
+    // the stage-2 operands of this wavefront's two column tiles (L2 blocks
+    // and scales) travel with the first groups of the K loop
+    const uint32_t l2_lds = ring_lds + C::OFF_L2 + wave * C::L2W;
+    auto pre = [&]() {
+      if constexpr (RT > 0) {
+#pragma unroll
+        for (int j = 0; j < 2; j++) {
+          const int ct = min(n0 / 32 + 2 * wc + j, ctiles - 1);
+#pragma unroll
+          for (int rbk = 0; rbk < C::RB; rbk++)
+            dma_s(lane * 16, uniform_ptr(l2codes + ((int64_t)ct * C::RB + rbk) * 1024),
+                  l2_lds + (j * C::RB + rbk) * 1024);
+        }
+        // lane q < 8 RB: 8 scales of column tile j = q / (4 RB), rank group
+        // (q / 4) % RB, columns 8 (q % 4) .. + 8
+        const int q = lane & (8 * C::RB - 1);
+        const int jj = q / (4 * C::RB), rbk = (q / 4) % C::RB;
+        const int ct = min(n0 / 32 + 2 * wc + jj, ctiles - 1);
+        dma_v(reinterpret_cast<const uint8_t *>(l2scales + (int64_t)rbk * geo.n_pad + ct * 32 +
+                                                8 * (q & 3)),
+              l2_lds + 2 * C::RB * 1024);
+      }
+    };
+    K::main_loop(P, smem, ring_lds, KG, lane, wr, wc, acc, pre);
+
+    // ---- stage 2 (Q_H Q(L2)) and the single epilogue ----
+    // (the index values are re-derived here, behind an opaque copy, so the
+    // compiler does not keep per-row addresses alive across the K loop)
+    int lane_e = lane, m0_e = m0;
+    asm volatile("" : "+v"(lane_e), "+s"(m0_e));
+    const int l32e = lane_e & 31;
+#pragma unroll
+    for (int i = 0; i < 2; i++) {
+      const int ti = 2 * wr + i;   // token tile within the block
+#pragma unroll
+      for (int j = 0; j < 2; j++) {
+        const int ct = n0 / 32 + 2 * wc + j;
+        const bool cvalid = ct < ctiles;
+        v16f ylr = v16f{0};
+        if constexpr (RT > 0) {
+          const uint8_t *QS = smem + C::OFF_Q;
+          const float *SHS = reinterpret_cast<const float *>(smem + C::OFF_SH);
+#pragma unroll
+          for (int rbk = 0; rbk < C::RB; rbk++) {
+            const uint8_t *qrow = QS + (32 * ti + l32e) * C::QSTR + rbk * 64 + (lane_e >> 5) * 32;
+            const v8i qa = join(*reinterpret_cast<const u32x4 *>(qrow),
+                                *reinterpret_cast<const u32x4 *>(qrow + 16));
+            const uint8_t *L2S = smem + C::OFF_L2 + wave * C::L2W;
+            const v8i lb = unpack32(*reinterpret_cast<const u32x4 *>(
+                L2S + (j * C::RB + rbk) * 1024 + lane_e * 16));
+            const float sl2 = half_bits_to_float(*reinterpret_cast<const uint16_t *>(
+                L2S + 2 * C::RB * 1024 + ((j * C::RB + rbk) * 32 + l32e) * 2));
+            const v16f cbv = mfma_codes_32x32x64(qa, lb);
+            const float *shrow = SHS + rbk * PBM + 32 * ti + 4 * (lane_e >> 5);
+#pragma unroll
+            for (int q = 0; q < 4; q++) {
+              const v4f sh4 = *reinterpret_cast<const v4f *>(shrow + 8 * q);
+#pragma unroll
+              for (int e = 0; e < 4; e++) {
+                const int v = 4 * q + e;
+                ylr[v] = fmaf(cbv[v], sh4[e] * sl2, ylr[v]);
+              }
+            }
+          }
+        }
+        const int col = ct * 32 + l32e;
+        if (cvalid && col < geo.n) {
+#pragma unroll
+          for (int v = 0; v < 16; v++) {
+            const int row = m0_e + 32 * ti + row_of_32x32(lane_e, v);
+            if (row < m) {
+              const float yv = acc[i][j][v] + ylr[v];
+              const uint16_t bits = a.bf16_out ? float_to_bf16_bits(yv) : float_to_half_bits(yv);
+              reinterpret_cast<uint16_t *>(a.y)[(int64_t)row * geo.n + col] = bits;
+            }
+          }
+        }
+      }
+    }
+    wait_vm<0>();      // stores drained before the next block's loads are counted
+    __syncthreads();   // the next block refills the ring
+  }
+}
+
+template <int RT, int D>
+hipError_t launch_prefill(const GemmArgs &a, hipStream_t s) {
+  using C = PCfg<RT, D>;
+  const int m_tiles = (a.m + PBM - 1) / PBM;
+  const int n_tiles = (a.geo.n_pad + PBN - 1) / PBN;
+  int cpw = 0, band = 0;
+  if (const char *env = getenv("TQ_PREFILL")) sscanf(env, "%d:%d", &cpw, &band);
+  if (cpw <= 0) {
+    cpw = (m_tiles * n_tiles) / 256;
+    if (cpw < 1) cpw = 1;
+  }
+  if (cpw > n_tiles) cpw = n_tiles;
+  const int n_chunks = (n_tiles + cpw - 1) / cpw;
+  if (band <= 0) band = 8;
+  if (band > m_tiles) band = m_tiles;
+  auto kern = dual_gemm_prefill_kernel<RT, D>;
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(kern, dim3(m_tiles * n_chunks), dim3(64 * PNW), C::LDS, s, a, m_tiles,
+                     n_tiles, n_chunks, cpw, band);
+  return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_prefill_rt(const GemmArgs &a, hipStream_t s) {
+  switch (a.geo.r_pad32 / 32) {
+    case 0: return launch_prefill<0, D>(a, s);
+    case 1: return launch_prefill<1, D>(a, s);
+    case 2: return launch_prefill<2, D>(a, s);
+    case 4: return launch_prefill<4, D>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_dual_gemm_prefill(const GemmArgs &a, hipStream_t s) {
+  // ring depth override for tuning sweeps: TQ_PREFILL_D=5|6
+  const char *env = getenv("TQ_PREFILL_D");
+  const int d = env ? atoi(env) : 6;
+  if (d == 5) return launch_prefill_rt<5>(a, s);
+  return launch_prefill_rt<6>(a, s);
+}
+
+}  // namespace tq

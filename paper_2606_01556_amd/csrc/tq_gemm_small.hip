@@ -107,13 +107,13 @@ __global__ __launch_bounds__(64 * DWAVE, 1) void dual_gemm_small_kernel(GemmArgs
   const uint8_t *l2codes = a.packed + geo.off_l2;
   const uint16_t *l2scales = reinterpret_cast<const uint16_t *>(a.packed + geo.off_l2s);
   const uint8_t *xc = reinterpret_cast<const uint8_t *>(a.xc);
-  const int64_t xrow_bytes = geo.k / 2;
   const int orow0 = 4 * q;                       // output rows 4q..4q+3 held by this lane
 
   // ---- this thread's share of a chunk load ----
-  // activation codes: row t / 32, 16-byte piece t % 32 (group t % 32 / 2, half t % 2)
+  // activation codes: row t / 32, 16-byte piece t % 32 (group t % 32 / 2, half t % 2),
+  // from the first 32-token activation tile of each group
   const int xl_row = tid >> 5, xl_gi = (tid & 31) >> 1, xl_half = tid & 1;
-  const uint8_t *xl_src = xc + (int64_t)min(xl_row, m - 1) * xrow_bytes + xl_half * 16;
+  const uint8_t *xl_src = xc + (int64_t)(32 * xl_half + min(xl_row, m - 1)) * 16;
   const int xl_dst = C::X_OFF + xl_row * XROW + xl_gi * 64 + xl_half * 32;
   // one scale piece: 8 fp16 from src + group * stride, to dst as 8 fp32
   const uint16_t *sp_src;
@@ -147,7 +147,7 @@ __global__ __launch_bounds__(64 * DWAVE, 1) void dual_gemm_small_kernel(GemmArgs
   auto chunk_load = [&](int c, Chunk &k) {
     c = min(c, NCH - 1);
     const int g0 = c * CHG;
-    k.x = *reinterpret_cast<const u32x4 *>(xl_src + min(g0 + xl_gi, KG - 1) * 32);
+    k.x = *reinterpret_cast<const u32x4 *>(xl_src + (int64_t)min(g0 + xl_gi, KG - 1) * 1024);
     k.s = *reinterpret_cast<const u32x4 *>(sp_src + (int64_t)min(g0 + sp_gi, KG - 1) * sp_stride);
   };
   auto chunk_store = [&](int buf, const Chunk &k) {

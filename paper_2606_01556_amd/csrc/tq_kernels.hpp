@@ -22,9 +22,9 @@ struct Geometry {
 struct GemmArgs {
   const uint8_t *packed;
   Geometry geo;
-  const uint32_t *xc;   // [m][k/8] TQ4 words
+  const uint32_t *xc;   // [m32/32][k/64] 1 KiB activation tiles (matrix-core lane order)
   const uint16_t *xs;   // [k/64][ms] fp16
-  int ms;               // row stride of xs: m rounded up to a multiple of 8
+  int ms;               // row stride of xs: m rounded up to a multiple of 32 (= m32)
   void *y;              // [m][n]
   int m;
   int bf16_out;
@@ -42,7 +42,6 @@ hipError_t launch_export(const Geometry &g, const uint8_t *packed, uint32_t *wc,
                          hipStream_t s);
 hipError_t launch_dual_gemm(const GemmArgs &a, hipStream_t s);
 hipError_t launch_dual_gemm_small(const GemmArgs &a, hipStream_t s);   // m <= 16
-hipError_t launch_dual_gemm_wide(const GemmArgs &a, hipStream_t s);    // prefill sizes
-hipError_t launch_dual_gemm_stream(const GemmArgs &a, hipStream_t s);  // prefill sizes
+hipError_t launch_dual_gemm_prefill(const GemmArgs &a, hipStream_t s); // prefill sizes
 
 }  // namespace tq

@@ -11,18 +11,25 @@ namespace tq {
 // ---------------------------------------------------------------------------
 // Activations: one thread per TQ4 word (8 consecutive values); the 8 threads
 // of a group are consecutive lanes of one wavefront and share the group max
-// through three butterfly shuffles.  Scales are stored group-major with the
-// token count padded to a multiple of 8 (padding entries are zero).
+// through three butterfly shuffles.  Codes go to the tile-major layout: 32
+// tokens x one K-group form one 1 KiB block in matrix-core operand lane
+// order (token 32 t + i, codes 32 h .. 32 h + 31 of group g at byte
+// ((t * KG + g) * 64 + 32 h + i) * 16); the padding tokens [m, m32) of the
+// last tile get zero codes.  Scales are stored group-major with the token
+// count padded to m32 (padding entries are zero).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void quant_act_kernel(const uint16_t *__restrict__ x, int m,
                                                         int k, uint32_t *__restrict__ codes,
                                                         uint16_t *__restrict__ scales) {
   const int64_t words_per_row = k >> 3;
-  const int64_t nwords = (int64_t)m * words_per_row;
+  const int m32 = (m + 31) / 32 * 32;
+  const int64_t nwords = (int64_t)m32 * words_per_row;
   const int64_t wid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t row = wid / words_per_row, w = wid % words_per_row;
   const bool valid = wid < nwords;
+  const bool real = row < m;   // uniform over the 8 lanes of a group
   u32x4 raw = {0, 0, 0, 0};
-  if (valid) raw = *reinterpret_cast<const u32x4 *>(x + wid * 8);
+  if (valid && real) raw = *reinterpret_cast<const u32x4 *>(x + wid * 8);
   float v[8];
 #pragma unroll
   for (int i = 0; i < 4; i++) {
@@ -41,22 +48,18 @@ __global__ __launch_bounds__(256) void quant_act_kernel(const uint16_t *__restri
 #pragma unroll
   for (int i = 0; i < 8; i++) c[i] = q4_code(v[i], s);
   if (valid) {
-    codes[wid] = tq4_pack8(c);
-    if ((wid & 7) == 0) {
-      const int64_t gi = wid >> 3;
-      const int64_t groups_per_row = k / kGroup;
-      const int64_t row = gi / groups_per_row, g = gi % groups_per_row;
-      const int64_t ms = (m + 7) / 8 * 8;
-      scales[g * ms + row] = s16;
-      if (row == m - 1)   // zero the padding tokens [m, ms) of this group
-        for (int64_t i = m; i < ms; i++) scales[g * ms + i] = 0;
-    }
+    const int64_t KG = k / kGroup;
+    const int64_t g = w >> 3, h = (w >> 2) & 1, wl = w & 3;
+    const int64_t t = row >> 5, i = row & 31;
+    codes[((t * KG + g) * 64 + 32 * h + i) * 4 + wl] = tq4_pack8(c);
+    if ((w & 7) == 0) scales[g * m32 + row] = real ? s16 : (uint16_t)0;
   }
 }
 
 hipError_t launch_quant_act(const uint16_t *x, int m, int k, uint32_t *codes, uint16_t *scales,
                             hipStream_t s) {
-  const int64_t nwords = (int64_t)m * (k / 8);
+  const int64_t m32 = (m + 31) / 32 * 32;
+  const int64_t nwords = m32 * (k / 8);
   const int64_t blocks = (nwords + 255) / 256;
   hipLaunchKernelGGL(quant_act_kernel, dim3((unsigned)blocks), dim3(256), 0, s, x, m, k, codes,
                      scales);

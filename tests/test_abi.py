@@ -119,3 +119,25 @@ def test_tq4_roundtrip():
     assert (word >> 4) & 7 == 5 and (word >> 11) & 1 == 0      # c4 = +5, sign in bit 11
     assert (word >> 12) & 7 == 6 and (word >> 19) & 1 == 1     # c5 = -6, sign in bit 19
     assert (word >> 28) & 7 == 0 and (word >> 3) & 1 == 0      # c7 = 0, sign in bit 3
+
+
+def test_act_codes_tile_layout_roundtrip():
+    """act_codes_rows inverts the tile-major activation layout of tq_quant_act:
+    token 32 t + i, codes 32 h .. 32 h + 31 of group g sit in 16-byte lane slot
+    32 h + i of the 1 KiB block (t, g)."""
+    rng = np.random.default_rng(5)
+    m, k = 45, 192
+    m32 = tq.padded_tokens(m)
+    codes = np.zeros((m32, k), np.int8)
+    codes[:m] = rng.integers(-7, 8, size=(m, k))
+    kg = k // 64
+    blocks = np.zeros((m32 // 32, kg, 64, 4), np.uint32)   # tile, group, lane slot, word
+    for t in range(m32 // 32):
+        for g in range(kg):
+            for h in range(2):
+                for i in range(32):
+                    seg = codes[32 * t + i, 64 * g + 32 * h: 64 * g + 32 * h + 32]
+                    blocks[t, g, 32 * h + i] = tq.tq4_encode(seg)
+    back = tq.act_codes_rows(blocks.reshape(m32 // 32, kg, 256), m)
+    np.testing.assert_array_equal(back, codes[:m])
+    assert tq.padded_tokens(1) == 32 and tq.padded_tokens(32) == 32 and tq.padded_tokens(33) == 64

@@ -73,8 +73,11 @@ def run_gpu(X, W, L1, L2, bf16=False, debug=True):
         ex += [l1c, l1s, l2c, l2s]
     tq.export_weights(d, lay.packed, *ex)
     torch.cuda.synchronize()
-    out["xq"] = tq.tq4_decode(xc.cpu().numpy())
-    out["xs"] = xs.cpu().numpy()[:, :M].T.copy()
+    out["xq"] = tq.act_codes_rows(xc.cpu().numpy(), M)
+    xs_all = xs.cpu().numpy()
+    assert np.all(xs_all[:, M:].view(np.uint16) == 0), "padding-token scales are zero"
+    assert np.all(tq.act_codes_rows(xc.cpu().numpy(), xs_all.shape[1])[M:] == 0), "padding codes"
+    out["xs"] = xs_all[:, :M].T.copy()
     out["wq"] = tq.tq4_decode(wc.cpu().numpy())
     out["ws"] = ws.cpu().numpy()
     if r:
