@@ -38,8 +38,8 @@ FP8_MFMA_PEAK_TFLOPS = 5000.0   # MI355X dense fp8 matrix peak (5.0 PFLOP/s)
 HBM_PEAK_GBS = 8000.0
 ROTATE_BYTES = 1 << 30
 CALIB_COPY_BYTES = 256 << 20
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_tile_kernel_m2048_llama3_8b_qo.json")
-TILE_SOURCE = os.path.join(ROOT, "paper_2606_01556_amd", "csrc", "tq_gemm.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_prefill_kernel_m2048_llama3_8b_qo.json")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2606_01556_amd", "csrc", "tq_gemm_prefill.hip")
 
 
 def measured_traffic():
@@ -51,7 +51,7 @@ def measured_traffic():
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
-        with open(TILE_SOURCE, "rb") as f:
+        with open(KERNEL_SOURCE, "rb") as f:
             sha = hashlib.sha256(f.read()).hexdigest()
     except (OSError, ValueError):
         return None

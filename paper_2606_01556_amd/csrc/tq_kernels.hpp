@@ -41,7 +41,7 @@ hipError_t launch_export(const Geometry &g, const uint8_t *packed, uint32_t *wc,
                          uint32_t *l1c, uint16_t *l1s, uint32_t *l2c, uint16_t *l2s,
                          hipStream_t s);
 hipError_t launch_dual_gemm(const GemmArgs &a, hipStream_t s);
-hipError_t launch_dual_gemm_small(const GemmArgs &a, hipStream_t s);   // m <= 16
+hipError_t launch_dual_gemm_decode(const GemmArgs &a, hipStream_t s);  // m <= 16
 hipError_t launch_dual_gemm_prefill(const GemmArgs &a, hipStream_t s); // prefill sizes
 
 }  // namespace tq

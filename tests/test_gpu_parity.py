@@ -2,9 +2,9 @@
 
 Bit-exact: activation codes and scales, weight codes and scales (via the
 canonical export), the on-chip low-rank intermediate H, its scales s_H and
-codes Q_H.  For m > 16 the tile kernel accumulates every output in the same
+codes Q_H.  For m > 16 the prefill kernel accumulates every output in the same
 ascending-group fma order as the oracle, so the rounded output Y is bit-exact
-too; the decode kernel (m <= 16) may split the residual K loop over its
+too; the decode kernel (m <= 16) splits the residual K loop over its
 wavefronts, which changes only the fp32 summation order of Y.  The
 spec tolerance (relative Frobenius 1e-3, max-abs 1e-2 * rms(Y)) is
 checked everywhere, against the oracle's fp64 result.
@@ -140,6 +140,7 @@ def test_tiny_workload(oracle_mod):
 @pytest.mark.parametrize("M,K,N,r", [
     (1, 64, 32, 8), (5, 128, 96, 16), (17, 192, 100, 32), (33, 256, 64, 64), (70, 128, 160, 128),
     (130, 320, 288, 64), (257, 128, 40, 0), (3, 64, 8, 0), (16, 512, 256, 128), (200, 256, 512, 32),
+    (32, 256, 7000, 128), (48, 576, 2080, 64),
 ])
 def test_ragged_shapes(oracle_mod, M, K, N, r):
     say(f"ragged M={M} K={K} N={N} r={r}")
