@@ -465,6 +465,9 @@ __global__ __launch_bounds__(64 * DW, 1) void dual_gemm_decode_kernel(GemmArgs a
           }
         }
       }
+      // the matrix-core products above read operands from every lane: keep
+      // them out of the per-lane store branch below
+      asm volatile("" : "+v"(ylr));
       const int col = ct * 16 + c16;
       if (col < geo.n) {
 #pragma unroll

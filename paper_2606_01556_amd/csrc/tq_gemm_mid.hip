@@ -1,0 +1,481 @@
+// Fused dual-component W4A4 layer (paper Sec. 4.3) for mid-sized token
+// counts (tens to about a thousand tokens): the residual 4-bit GEMM, the
+// stage-1 product H = Q(X) Q(L1) kept on chip, its on-the-fly
+// re-quantization, stage 2 Q_H Q(L2) and one epilogue, in one kernel.
+//
+// Work decomposition.  A workgroup of 8 wavefronts owns one block of 32
+// tokens and CT output tiles of 32 columns.  Since every output tile needs
+// all of H for its tokens, each workgroup forms the 32 x r block of H itself.
+//  * H wavefronts (wavefronts 0 .. RT-1, RT = r/32 rounded up) each own one
+//    32 x 32 tile of H and walk all K-groups in ascending order, so H and Q_H
+//    are bit-identical to the oracle's.
+//  * the other wavefronts share the residual tile-groups (CT tiles x the
+//    groups of each chunk of K); their partial sums are added in a fixed
+//    order at the end (only Y's fp32 summation order differs from the
+//    oracle's).  Wavefronts on SIMDs without an H wavefront take the larger
+//    shares.
+// Per tile and group (Eq. 2): v_mfma_scale_f32_32x32x64_f8f6f4 returns half
+// of the exact integer group sum (codes as fp8 subnormals), v_mfma_f32_32x32x8
+// f16 twice the exact scale product, and one fma per element applies their
+// product, exactly I * s_x * s_w.
+//
+// Data movement: direct global -> LDS loads (global_load_lds_dwordx4) with
+// explicit wait counts.  K runs in chunks of MCG groups through a ring of D
+// chunk slots, D - 1 chunks ahead.  A slot holds the chunk's raw activation
+// blocks, all its scales and every wavefront's own weight / L1 blocks.  Each
+// wavefront issues one shared load and its own block loads per chunk, so each
+// wait is one constant s_waitcnt.  One chunk ahead, the two least-loaded wavefronts expand the
+// activation codes to fp8 operand bytes, shared by all eight wavefronts.  One
+// workgroup barrier per chunk.
+#include <stdlib.h>
+
+#include <type_traits>
+
+#include "tq_device.hpp"
+#include "tq_kernels.hpp"
+
+namespace tq {
+namespace {
+
+typedef _Float16 v4h __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int MW = 8;                  // wavefronts per workgroup
+constexpr int MCG = 2;                 // K-groups per chunk
+constexpr int M_LDS = 160 * 1024;      // LDS of a CU
+
+template <int RT, int CT>
+struct MCfg {
+  static constexpr int NRW = MW - RT;                  // residual wavefronts
+  static constexpr int NITEM = MCG * CT;               // residual tile-groups per chunk
+  static constexpr int NF_MAX = (NITEM + NRW - 1) / NRW;
+  // scale pieces (16 bytes = 8 fp16) of a chunk: activation, weight, L1
+  static constexpr int NPX = MCG * 4, NPW = MCG * 4 * CT, NPL = MCG * 4 * RT;
+  static constexpr int NP = NPX + NPW + NPL;
+  static constexpr int NSI = (NP + 63) / 64;           // scale wave loads
+  static constexpr int NSH = MCG + NSI;                // shared wave loads per chunk
+  // chunk slot
+  static constexpr int S_X = 0;                        // MCG raw activation blocks
+  static constexpr int S_SC = MCG * 1024;              // scale pieces
+  static constexpr int S_FR = S_SC + NSI * 1024;       // blocks: H (RT x MCG), residual items
+  static constexpr int SLOT = S_FR + (RT * MCG + NITEM) * 1024;
+  // expanded activation operands: 2 buffers x MCG groups x 2 KiB of fp8 bytes
+  static constexpr int XEB = MCG * 2048;
+  // stage-2 operands: CT x RB L2 blocks and one scale region
+  static constexpr int RB = (RT + 1) / 2;              // 64-rank blocks (= rank groups)
+  static constexpr int L2B = RT > 0 ? CT * RB * 1024 + 1024 : 0;
+  static constexpr int DFIT = (M_LDS - 2 * XEB - L2B) / SLOT;
+  static constexpr int D = DFIT > 16 ? 16 : DFIT;      // chunk slots
+  static constexpr int OFF_XE = D * SLOT;
+  static constexpr int OFF_L2 = OFF_XE + 2 * XEB;
+  static constexpr int LDS = OFF_L2 + L2B;
+  // epilogue (aliases the ring)
+  static constexpr int HSTR = RT * 32 + 1;
+  static constexpr int QSTR = (RB > 0 ? RB : 1) * 64 + 16;
+  static constexpr int E_HS = 0;                                  // [32][HSTR] fp32
+  static constexpr int E_QS = E_HS + 32 * HSTR * 4;               // [32][QSTR] fp8 codes
+  static constexpr int E_SH = E_QS + 32 * QSTR;                   // [RB][32] fp32
+  static constexpr int E_RES = (E_SH + (RB > 0 ? RB : 1) * 128 + 255) / 256 * 256;
+  static constexpr int E_END = E_RES + NITEM * 4096;              // [NITEM][16][64] fp32
+  static_assert(NSH <= MW, "one shared load per wavefront and chunk");
+  static_assert(NF_MAX <= 2, "at most two residual items per wavefront and chunk");
+  static_assert(D >= 3, "at least two chunks in flight");
+  static_assert(MCG == 2, "two expansion wavefronts, one group each");
+  static_assert(LDS <= M_LDS, "fits the 160 KiB LDS of a CU");
+  static_assert(E_END <= D * SLOT, "the epilogue fits in the ring");
+};
+
+// Residual rank of wavefront w (w >= RT): wavefronts on SIMDs (w % 4) without
+// an H wavefront come first, so they take the larger shares.
+__host__ __device__ constexpr int res_index(int rt, int w) {
+  int i = 0;
+  for (int pass = 0; pass < 2; pass++)
+    for (int v = rt; v < MW; v++) {
+      const bool no_h = (v % 4) >= rt;
+      if ((pass == 0) == no_h) {
+        if (v == w) return i;
+        i++;
+      }
+    }
+  return -1;
+}
+
+template <int N>
+__device__ __forceinline__ void mwait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt has 6 bits");
+  __builtin_amdgcn_s_waitcnt((N & 0xf) | ((N >> 4) << 14) | (0x7 << 4) | (0xf << 8));
+}
+
+// 16 bytes per lane from addr into LDS at lds + 16 * lane
+__device__ __forceinline__ void mdma(const uint8_t *addr, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(addr), "s"(lds)
+               : "memory");
+}
+
+__device__ __forceinline__ v8i lds_v8i(const uint8_t *p) {
+  const u32x4 lo = *reinterpret_cast<const u32x4 *>(p);
+  const u32x4 hi = *reinterpret_cast<const u32x4 *>(p + 16);
+  return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+}
+
+// 2 * s_row * s_col of a 32x32 tile (both scales in k = 0 and k = 4)
+__device__ __forceinline__ v16f m_outer2(uint32_t sa, uint32_t sb) {
+  const v16f z = {0};
+  const u32x2 a2 = {sa, 0u}, b2 = {sb, 0u};
+  return __builtin_amdgcn_mfma_f32_32x32x8f16(__builtin_bit_cast(v4h, a2),
+                                              __builtin_bit_cast(v4h, b2), z, 0, 0, 0);
+}
+
+// half of the exact integer group sum of a 32x32 tile of code products
+__device__ __forceinline__ v16f m_codes_half(v8i a, v8i b) {
+  const v16f z = {0};
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, z, 0, 0, 0, kScale2p9 - 1, 0,
+                                                         kScale2p9);
+}
+
+template <int RT, int CT>
+__global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, int n_rb) {
+  using C = MCfg<RT, CT>;
+  constexpr int D = C::D;
+  extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
+  const Geometry &geo = a.geo;
+  const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int KG = geo.k / kGroup, NCH = (KG + MCG - 1) / MCG;
+  const int ct32 = geo.n_pad / 32;
+  const int m = a.m, ms = a.ms;
+
+  // Workgroups are dealt round-robin to the 8 XCDs: give each XCD a
+  // contiguous run of logical ids, token blocks fastest, so the workgroups of
+  // an XCD share weight columns in its L2.
+  int logical;
+  {
+    const int nwg = gridDim.x, per = nwg / 8, rem = nwg % 8;
+    const int x = blockIdx.x % 8, s = blockIdx.x / 8;
+    logical = (x < rem ? x * (per + 1) : rem * (per + 1) + (x - rem) * per) + s;
+  }
+  const int cb = logical / n_rb, tb = logical % n_rb;   // column block, token block
+  const uint32_t lds0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)smem);
+
+  const uint8_t *xc = reinterpret_cast<const uint8_t *>(a.xc) + (int64_t)tb * KG * 1024;
+  const uint8_t *xs = reinterpret_cast<const uint8_t *>(a.xs);
+  const uint8_t *wcodes = a.packed + geo.off_w;
+  const uint8_t *wscales = a.packed + geo.off_ws;
+  const uint8_t *l1codes = a.packed + geo.off_l1;
+  const uint8_t *l1scales = a.packed + geo.off_l1s;
+  const uint8_t *l2codes = a.packed + geo.off_l2;
+  const uint8_t *l2scales = a.packed + geo.off_l2s;
+
+  // ---- this wavefront's shared load: lane reads base + g * stride ----
+  const int sh = wave % C::NSH;   // wavefronts past NSH repeat a load (same bytes, same place)
+  const uint8_t *sbase;
+  uint32_t sstride, sdst;
+  int sgi;
+  if (sh < MCG) {                 // activation block of group sh of the chunk
+    sbase = xc + lane * 16;
+    sstride = 1024;
+    sgi = sh;
+    sdst = C::S_X + sh * 1024;
+  } else {                        // scale pieces 64 s + lane
+    const int s = sh - MCG;
+    const int p0 = 64 * s + lane;
+    const int p = p0 < C::NP ? p0 : 0;
+    sdst = C::S_SC + s * 1024;
+    if (p < C::NPX) {
+      sgi = p / 4;
+      sbase = xs + (int64_t)(32 * tb + 8 * (p % 4)) * 2;
+      sstride = (uint32_t)ms * 2;
+    } else if (p < C::NPX + C::NPW) {
+      const int q = p - C::NPX;
+      sgi = q / (4 * CT);
+      sbase = wscales + (int64_t)min(32 * CT * cb + 8 * (q % (4 * CT)), geo.n_pad - 8) * 2;
+      sstride = (uint32_t)geo.n_pad * 2;
+    } else {
+      const int q = p - C::NPX - C::NPW;
+      sgi = q / (4 * (RT > 0 ? RT : 1));
+      sbase = l1scales + (int64_t)(8 * (q % (4 * (RT > 0 ? RT : 1)))) * 2;
+      sstride = (uint32_t)geo.r_pad32 * 2;
+    }
+  }
+
+  // ---- roles ----
+  const bool hw = wave < RT;
+  const int ri = hw ? -1 : res_index(RT, wave);
+  const int nf = hw ? MCG : (ri < C::NITEM ? (C::NITEM - ri + C::NRW - 1) / C::NRW : 0);
+
+  // stage-2 operands, loaded first: wavefront j < CT the L2 blocks of tile j,
+  // the last wavefront the L2 scales of all CT tiles
+  auto stage2_loads = [&]() {
+    if constexpr (RT > 0) {
+      if (wave < CT) {
+        const int ct = min(cb * CT + wave, ct32 - 1);
+#pragma unroll
+        for (int rb = 0; rb < C::RB; rb++)
+          mdma(l2codes + (((int64_t)ct * C::RB + rb) * 64 + lane) * 16,
+               lds0 + C::OFF_L2 + (wave * C::RB + rb) * 1024);
+      }
+      if (wave == MW - 1) {
+        const int q0 = lane, q = q0 < C::RB * CT * 4 ? q0 : 0;
+        const int h = q / (4 * CT), j = (q / 4) % CT, part = q % 4;
+        const int col = min(32 * (cb * CT + j) + 8 * part, geo.n_pad - 8);
+        mdma(l2scales + ((int64_t)h * geo.n_pad + col) * 2, lds0 + C::OFF_L2 + CT * C::RB * 1024);
+      }
+    }
+  };
+
+  // expand chunk c's raw activation codes into fp8 operand bytes: the two
+  // residual wavefronts with the fewest items, one lane per 16-byte lane slot
+  const int ex = ri >= C::NRW - MCG ? ri - (C::NRW - MCG) : -1;   // expansion group (or none)
+  auto expand = [&](int c) {
+    if (ex >= 0) {
+      const u32x4 raw = *reinterpret_cast<const u32x4 *>(smem + (c % D) * C::SLOT + C::S_X +
+                                                         ex * 1024 + lane * 16);
+      const v8i u = unpack32(raw);
+      uint8_t *E = smem + C::OFF_XE + (c & 1) * C::XEB + ex * 2048 + lane * 32;
+      *reinterpret_cast<u32x4 *>(E) = u32x4{(uint32_t)u[0], (uint32_t)u[1], (uint32_t)u[2], (uint32_t)u[3]};
+      *reinterpret_cast<u32x4 *>(E + 16) = u32x4{(uint32_t)u[4], (uint32_t)u[5], (uint32_t)u[6], (uint32_t)u[7]};
+    }
+  };
+
+  // The K loop of one role with its per-chunk load count as a constant:
+  // H wavefronts walk their tile over the MCG groups of every chunk, residual
+  // wavefronts their NF items e = ri + NRW k (group e / CT, tile e % CT).
+  auto k_loop = [&](auto HC, auto NFC, v16f(&acc)[2]) {
+    constexpr bool H = decltype(HC)::value;
+    constexpr int NF = decltype(NFC)::value;
+    constexpr int PER = 1 + NF;   // loads per chunk
+    auto item_gi = [&](int k) { return H ? k : (ri + C::NRW * k) / CT; };
+    auto item_tile = [&](int k) { return (ri + C::NRW * k) % CT; };
+    auto item_frag = [&](int k) { return H ? wave * MCG + k : RT * MCG + ri + C::NRW * k; };
+    auto issue = [&](int c) {
+      const uint32_t slot = lds0 + (c % D) * C::SLOT;
+      mdma(sbase + (uint64_t)min(MCG * c + sgi, KG - 1) * sstride, slot + sdst);
+#pragma unroll
+      for (int k = 0; k < NF; k++) {
+        const int g = min(MCG * c + item_gi(k), KG - 1);
+        const uint8_t *src = H ? l1codes + (((int64_t)wave * KG + g) * 64 + lane) * 16
+                               : wcodes + (((int64_t)min(cb * CT + item_tile(k), ct32 - 1) * KG + g) * 64 + lane) * 16;
+        mdma(src, slot + C::S_FR + item_frag(k) * 1024);
+      }
+    };
+
+    mwait_vm<0>();
+    stage2_loads();
+#pragma unroll
+    for (int s = 0; s < D - 1; s++) issue(s);
+    mwait_vm<(D - 2) * PER>();   // chunk 0 has landed
+    __syncthreads();
+    expand(0);
+    for (int c = 0; c < NCH; c++) {
+      mwait_vm<(D - 3) * PER>();   // chunk c + 1 has landed
+      __syncthreads();             // chunk c's operands are visible; chunk c - 1 is consumed
+      issue(c + D - 1);            // into chunk c - 1's slot
+      if (c + 1 < NCH) expand(c + 1);
+      if constexpr (NF > 0) {
+        const uint8_t *S = smem + (c % D) * C::SLOT;
+        const uint8_t *XE = smem + C::OFF_XE + (c & 1) * C::XEB;
+        v8i av[NF];
+        u32x4 bv[NF];
+        uint32_t sa[NF], sb[NF];
+#pragma unroll
+        for (int k = 0; k < NF; k++) {
+          const int gi = item_gi(k);
+          av[k] = lds_v8i(XE + gi * 2048 + lane * 32);
+          bv[k] = *reinterpret_cast<const u32x4 *>(S + C::S_FR + item_frag(k) * 1024 + lane * 16);
+          const uint32_t s_a = *reinterpret_cast<const uint16_t *>(S + C::S_SC + (gi * 32 + l32) * 2);
+          sa[k] = MCG * c + gi < KG ? s_a : 0u;   // a group past K adds exactly zero
+          const int so = H ? (C::NPX + C::NPW) * 16 + (gi * 32 * RT + 32 * wave + l32) * 2
+                           : C::NPX * 16 + (gi * 32 * CT + 32 * item_tile(k) + l32) * 2;
+          sb[k] = *reinterpret_cast<const uint16_t *>(S + C::S_SC + so);
+        }
+        v16f cv[NF], pv[NF];
+#pragma unroll
+        for (int k = 0; k < NF; k++) {
+          cv[k] = m_codes_half(av[k], unpack32(bv[k]));
+          pv[k] = m_outer2(sa[k], sb[k]);
+        }
+#pragma unroll
+        for (int k = 0; k < NF; k++) {
+          v16f &t = acc[H ? 0 : k];
+#pragma unroll
+          for (int v = 0; v < 16; v++) t[v] = fmaf(cv[k][v], pv[k][v], t[v]);
+        }
+      }
+    }
+    mwait_vm<0>();   // the loads past the end have landed before the ring is reused
+  };
+
+  v16f acc[2];
+  acc[0] = v16f{0};
+  acc[1] = v16f{0};
+  if (hw) {
+    if constexpr (RT > 0) k_loop(std::true_type{}, std::integral_constant<int, MCG>{}, acc);
+  } else if (nf == 2) {
+    if constexpr (C::NF_MAX >= 2) k_loop(std::false_type{}, std::integral_constant<int, 2>{}, acc);
+  } else if (nf == 1) {
+    k_loop(std::false_type{}, std::integral_constant<int, 1>{}, acc);
+  } else {
+    k_loop(std::false_type{}, std::integral_constant<int, 0>{}, acc);
+  }
+  __syncthreads();   // every wavefront is done with the ring
+
+  // ---- H tiles and residual partials -> LDS ----
+  float *HS = reinterpret_cast<float *>(smem + C::E_HS);
+  uint8_t *QS = smem + C::E_QS;
+  float *SHS = reinterpret_cast<float *>(smem + C::E_SH);
+  float *RES = reinterpret_cast<float *>(smem + C::E_RES);
+  if (hw) {
+#pragma unroll
+    for (int v = 0; v < 16; v++) HS[row_of_32x32(lane, v) * C::HSTR + 32 * wave + l32] = acc[0][v];
+  } else {
+#pragma unroll
+    for (int k = 0; k < 2; k++) {
+      if (k < nf) {
+        const int e = ri + C::NRW * k;
+#pragma unroll
+        for (int v = 0; v < 16; v++) RES[(e * 16 + v) * 64 + lane] = acc[k][v];
+      }
+    }
+  }
+  if constexpr (RT > 0) {
+    const int r = geo.r;
+    if (r < C::RB * 64)
+      for (int idx = tid; idx < 32 * C::RB * 64; idx += 64 * MW) {
+        const int row = idx / (C::RB * 64), j = idx % (C::RB * 64);
+        if (j >= r) QS[row * C::QSTR + j] = 0;
+      }
+  }
+  __syncthreads();
+
+  // ---- re-quantize H per token and rank group (s_H stays fp32) ----
+  if constexpr (RT > 0) {
+    const int r = geo.r, gr = geo.gr, rg = r / gr;
+    const int subs = gr / 8;                // lanes per (token, rank group): 1, 2, 4 or 8
+    const int work = 32 * rg * subs;        // <= 512
+    const bool dbg = a.dbg_h != nullptr && cb == 0;
+    const bool valid = tid < work;
+    const int pair = tid / subs, sub = tid % subs;
+    const int row = pair / rg, hg = pair % rg;
+    const int j0 = hg * gr + sub * 8;
+    const int grow = 32 * tb + row;
+    float hv[8];
+    float amax = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 8; e++) {
+      hv[e] = valid ? HS[row * C::HSTR + j0 + e] : 0.0f;
+      amax = fmaxf(amax, fabsf(hv[e]));
+    }
+    for (int msk = 1; msk < subs; msk <<= 1) amax = fmaxf(amax, __shfl_xor(amax, msk));
+    const float shv = amax / 7.0f;   // IEEE division
+    if (valid) {
+      uint32_t w0 = 0, w1 = 0;
+#pragma unroll
+      for (int e = 0; e < 8; e++) {
+        int qv = 0;
+        if (shv != 0.0f) {
+          float tq = __builtin_rintf(hv[e] / shv);
+          tq = tq > 7.0f ? 7.0f : (tq < -7.0f ? -7.0f : tq);
+          qv = (int)tq;
+        }
+        const uint32_t bq = code_to_fp8(qv);
+        if (e < 4) w0 |= bq << (8 * e); else w1 |= bq << (8 * (e - 4));
+        if (dbg && grow < m) {
+          a.dbg_h[(int64_t)grow * r + j0 + e] = hv[e];
+          a.dbg_qh[(int64_t)grow * r + j0 + e] = (int8_t)qv;
+        }
+      }
+      *reinterpret_cast<uint32_t *>(QS + row * C::QSTR + j0) = w0;
+      *reinterpret_cast<uint32_t *>(QS + row * C::QSTR + j0 + 4) = w1;
+      if (sub == 0) {
+        SHS[hg * 32 + row] = shv;
+        if (dbg && grow < m) a.dbg_sh[(int64_t)grow * rg + hg] = shv;
+      }
+    }
+    __syncthreads();
+  }
+
+  // ---- stage 2 and the single epilogue: wavefront j < CT stores tile j ----
+  if (wave < CT) {
+    const int j = wave;
+    const int ct = cb * CT + j;
+    if (ct < ct32) {
+      v16f ylr = v16f{0};
+      if constexpr (RT > 0) {
+        const uint8_t *L2S = smem + C::OFF_L2;
+#pragma unroll
+        for (int rb = 0; rb < C::RB; rb++) {
+          const v8i qa = lds_v8i(QS + l32 * C::QSTR + rb * 64 + (lane >> 5) * 32);
+          const v8i lb = unpack32(*reinterpret_cast<const u32x4 *>(L2S + (j * C::RB + rb) * 1024 + lane * 16));
+          const float sl2 = half_bits_to_float(*reinterpret_cast<const uint16_t *>(
+              L2S + CT * C::RB * 1024 + ((rb * CT + j) * 32 + l32) * 2));
+          const v16f cbv = mfma_codes_32x32x64(qa, lb);
+#pragma unroll
+          for (int v = 0; v < 16; v++)
+            ylr[v] = fmaf(cbv[v], SHS[rb * 32 + row_of_32x32(lane, v)] * sl2, ylr[v]);
+        }
+      }
+      // the matrix-core products above read operands from every lane: keep
+      // them out of the per-lane store branch below
+      asm volatile("" : "+v"(ylr));
+      const int col = ct * 32 + l32;
+      if (col < geo.n) {
+#pragma unroll
+        for (int v = 0; v < 16; v++) {
+          const int row = 32 * tb + row_of_32x32(lane, v);
+          if (row < m) {
+            float yres = 0.0f;
+#pragma unroll
+            for (int gi = 0; gi < MCG; gi++) yres += RES[((gi * CT + j) * 16 + v) * 64 + lane];
+            const float yv = yres + ylr[v];
+            const uint16_t bits = a.bf16_out ? float_to_bf16_bits(yv) : float_to_half_bits(yv);
+            reinterpret_cast<uint16_t *>(a.y)[(int64_t)row * geo.n + col] = bits;
+          }
+        }
+      }
+    }
+  }
+}
+
+template <int RT, int CT>
+hipError_t launch_mid(const GemmArgs &a, hipStream_t s) {
+  using C = MCfg<RT, CT>;
+  const int n_rb = a.ms / 32;
+  const int n_cb = (a.geo.n_pad / 32 + CT - 1) / CT;
+  auto kern = dual_gemm_mid_kernel<RT, CT>;
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(kern, dim3(n_rb * n_cb), dim3(64 * MW), C::LDS, s, a, n_rb);
+  return hipGetLastError();
+}
+
+template <int CT>
+hipError_t launch_mid_rt(const GemmArgs &a, hipStream_t s) {
+  switch (a.geo.r_pad32 / 32) {
+    case 0: return launch_mid<0, CT>(a, s);
+    case 1: return launch_mid<1, CT>(a, s);
+    case 2: return launch_mid<2, CT>(a, s);
+    case 4: return launch_mid<4, CT>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+// time of one workgroup in tile-groups per SIMD and chunk: the H chain takes
+// MCG, the rest spreads over the 4 SIMDs
+int mid_cost(int rt, int ct, int n_wg) {
+  const int per_simd = (MCG * (rt + ct) + 3) / 4;
+  const int chain = rt > 0 ? MCG : 0;
+  const int rounds = (n_wg + 255) / 256;
+  return rounds * (per_simd > chain ? per_simd : chain);
+}
+
+}  // namespace
+
+hipError_t launch_dual_gemm_mid(const GemmArgs &a, hipStream_t s) {
+  const int rt = a.geo.r_pad32 / 32, ct32 = a.geo.n_pad / 32, n_rb = a.ms / 32;
+  int ct = mid_cost(rt, 4, n_rb * ((ct32 + 3) / 4)) < mid_cost(rt, 2, n_rb * ((ct32 + 1) / 2)) ? 4 : 2;
+  if (const char *env = getenv("TQ_MID_CT")) ct = atoi(env) == 4 ? 4 : 2;
+  return ct == 4 ? launch_mid_rt<4>(a, s) : launch_mid_rt<2>(a, s);
+}
+
+}  // namespace tq

@@ -637,6 +637,9 @@ __global__ __launch_bounds__(64 * PNW, 1) void dual_gemm_prefill_kernel(GemmArgs
             }
           }
         }
+        // the matrix-core products above read operands from every lane: keep
+        // them out of the per-lane store branch below
+        asm volatile("" : "+v"(ylr));
         const int col = ct * 32 + l32e;
         if (cvalid && col < geo.n) {
 #pragma unroll

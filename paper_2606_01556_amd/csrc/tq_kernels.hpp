@@ -42,6 +42,7 @@ hipError_t launch_export(const Geometry &g, const uint8_t *packed, uint32_t *wc,
                          hipStream_t s);
 hipError_t launch_dual_gemm(const GemmArgs &a, hipStream_t s);
 hipError_t launch_dual_gemm_decode(const GemmArgs &a, hipStream_t s);  // m <= 16
-hipError_t launch_dual_gemm_prefill(const GemmArgs &a, hipStream_t s); // prefill sizes
+hipError_t launch_dual_gemm_mid(const GemmArgs &a, hipStream_t s);      // mid sizes
+hipError_t launch_dual_gemm_prefill(const GemmArgs &a, hipStream_t s);  // prefill sizes
 
 }  // namespace tq

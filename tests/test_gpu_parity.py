@@ -2,12 +2,13 @@
 
 Bit-exact: activation codes and scales, weight codes and scales (via the
 canonical export), the on-chip low-rank intermediate H, its scales s_H and
-codes Q_H.  For m > 16 the prefill kernel accumulates every output in the same
-ascending-group fma order as the oracle, so the rounded output Y is bit-exact
-too; the decode kernel (m <= 16) splits the residual K loop over its
-wavefronts, which changes only the fp32 summation order of Y.  The
-spec tolerance (relative Frobenius 1e-3, max-abs 1e-2 * rms(Y)) is
-checked everywhere, against the oracle's fp64 result.
+codes Q_H.  The library serves m <= 16 with the decode kernel, m up to 512
+with the mid kernel and larger m with the prefill kernel.  The prefill kernel
+accumulates every output in the same ascending-group fma order as the oracle,
+so its rounded output Y is bit-exact too; the decode and mid kernels split the
+residual K loop over wavefronts, which changes only the fp32 summation order
+of Y.  The benchmark spec's tolerance (relative Frobenius 1e-3, max-abs
+1e-2 * rms(Y)) is checked everywhere, against the oracle's fp64 result.
 """
 import numpy as np
 import pytest
@@ -24,6 +25,8 @@ MAX_ABS_RMS = 1e-2
 # rounding of the output alone reaches ~1.1e-3 relative Frobenius error, so the
 # fp16 bounds are scaled by 8 for bf16 results.
 BF16_FACTOR = 8.0
+# smallest token count served by the prefill kernel (bit-exact Y)
+PREFILL_FROM = 513
 
 
 def say(*a):
@@ -122,7 +125,7 @@ def full_parity(oracle_mod, X, W, L1, L2, bf16=False):
         np.testing.assert_array_equal(g["H"].view(np.uint32), o["H"].view(np.uint32))
         np.testing.assert_array_equal(g["sH"].view(np.uint32), o["sH"].view(np.uint32))
         np.testing.assert_array_equal(g["qH"], o["qH"])
-    if X.shape[0] > 16:
+    if X.shape[0] >= PREFILL_FROM:
         if bf16:
             np.testing.assert_array_equal(g["Ybits"], o["Ybf"])
         else:
@@ -157,7 +160,20 @@ def test_decode_kernel_variants(oracle_mod, M, K, N, r):
     full_parity(oracle_mod, d["X"], d["W_res"], d["L1"], d["L2"])
 
 
-@pytest.mark.parametrize("M", [4, 100])
+@pytest.mark.parametrize("ct", ["2", "4"])
+@pytest.mark.parametrize("M,K,N,r", [(17, 192, 100, 32), (32, 320, 4096, 64), (64, 128, 1000, 128),
+                                     (100, 448, 520, 16), (128, 256, 4096, 64), (250, 64, 96, 8),
+                                     (40, 576, 8192, 0), (512, 128, 256, 64)])
+def test_mid_kernel_variants(oracle_mod, monkeypatch, ct, M, K, N, r):
+    """16 < m <= 512 with 2 and 4 column tiles per workgroup, odd K-group counts
+    (a half chunk at the end of K) and every rank-tile count."""
+    monkeypatch.setenv("TQ_MID_CT", ct)
+    say(f"mid ct={ct} M={M} K={K} N={N} r={r}")
+    d = random_codes_layer(M, K, N, r, seed=M * 7 + N + r)
+    full_parity(oracle_mod, d["X"], d["W_res"], d["L1"], d["L2"])
+
+
+@pytest.mark.parametrize("M", [4, 100, 600])
 def test_bf16_output(oracle_mod, M):
     say(f"bf16 M={M}")
     d = random_codes_layer(M, 256, 96, 64, seed=3)
@@ -221,7 +237,7 @@ def sampled_parity(oracle_mod, wl_name, layer_idx, M, rank=None, n_rows=6, n_col
     rows = np.unique(np.concatenate([[0, M - 1], rng.integers(0, M, n_rows)]))
     cols = np.unique(np.concatenate([[0, N - 1], rng.integers(0, N, n_cols)]))
     o = oracle_mod.layer(X, W, L1, L2, GROUP, rows=rows, cols=cols)
-    if M > 16:
+    if M >= PREFILL_FROM:
         np.testing.assert_array_equal(g["Ybits"][np.ix_(rows, cols)], o["Y16"].view(np.uint16))
     check_tolerance(g["Y"][np.ix_(rows, cols)], o["Y64"])
     if L1 is not None:
