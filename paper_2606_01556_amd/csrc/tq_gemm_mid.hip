@@ -41,7 +41,7 @@ typedef _Float16 v4h __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int MW = 8;                  // wavefronts per workgroup
-constexpr int MCG = 2;                 // K-groups per chunk
+constexpr int MCG = 4;                 // K-groups per chunk
 constexpr int M_LDS = 160 * 1024;      // LDS of a CU
 
 template <int RT, int CT>
@@ -76,11 +76,11 @@ struct MCfg {
   static constexpr int E_QS = E_HS + 32 * HSTR * 4;               // [32][QSTR] fp8 codes
   static constexpr int E_SH = E_QS + 32 * QSTR;                   // [RB][32] fp32
   static constexpr int E_RES = (E_SH + (RB > 0 ? RB : 1) * 128 + 255) / 256 * 256;
-  static constexpr int E_END = E_RES + NITEM * 4096;              // [NITEM][16][64] fp32
+  static constexpr int E_END = E_RES + NITEM * 4096;              // [NITEM][64 lanes][16] fp32
   static_assert(NSH <= MW, "one shared load per wavefront and chunk");
-  static_assert(NF_MAX <= 2, "at most two residual items per wavefront and chunk");
+  static_assert(NF_MAX <= 4, "at most four residual items per wavefront and chunk");
   static_assert(D >= 3, "at least two chunks in flight");
-  static_assert(MCG == 2, "two expansion wavefronts, one group each");
+  static_assert(MCG % 2 == 0 && NRW >= 2, "two expansion wavefronts, MCG / 2 groups each");
   static_assert(LDS <= M_LDS, "fits the 160 KiB LDS of a CU");
   static_assert(E_END <= D * SLOT, "the epilogue fits in the ring");
 };
@@ -110,6 +110,20 @@ __device__ __forceinline__ void mwait_vm() {
 __device__ __forceinline__ void mdma(const uint8_t *addr, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(addr), "s"(lds)
                : "memory");
+}
+
+// the same with a wave-uniform base and a 32-bit lane offset
+__device__ __forceinline__ void mdma_s(uint32_t voff, const uint8_t *sbase, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase), "s"(lds)
+               : "memory");
+}
+
+// a wave-uniform pointer, kept in scalar registers
+__device__ __forceinline__ const uint8_t *m_uniform(const uint8_t *p) {
+  const uint64_t v = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return reinterpret_cast<const uint8_t *>(((uint64_t)hi << 32) | lo);
 }
 
 __device__ __forceinline__ v8i lds_v8i(const uint8_t *p) {
@@ -224,55 +238,90 @@ __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, i
   };
 
   // expand chunk c's raw activation codes into fp8 operand bytes: the two
-  // residual wavefronts with the fewest items, one lane per 16-byte lane slot
-  const int ex = ri >= C::NRW - MCG ? ri - (C::NRW - MCG) : -1;   // expansion group (or none)
-  auto expand = [&](int c) {
+  // residual wavefronts with the fewest items, MCG / 2 groups each, one lane
+  // per 16-byte lane slot
+  const int ex = ri >= C::NRW - 2 ? ri - (C::NRW - 2) : -1;   // expansion wavefront (or none)
+  auto expand = [&](int c, uint32_t slot_off) {
     if (ex >= 0) {
-      const u32x4 raw = *reinterpret_cast<const u32x4 *>(smem + (c % D) * C::SLOT + C::S_X +
-                                                         ex * 1024 + lane * 16);
-      const v8i u = unpack32(raw);
-      uint8_t *E = smem + C::OFF_XE + (c & 1) * C::XEB + ex * 2048 + lane * 32;
-      *reinterpret_cast<u32x4 *>(E) = u32x4{(uint32_t)u[0], (uint32_t)u[1], (uint32_t)u[2], (uint32_t)u[3]};
-      *reinterpret_cast<u32x4 *>(E + 16) = u32x4{(uint32_t)u[4], (uint32_t)u[5], (uint32_t)u[6], (uint32_t)u[7]};
+#pragma unroll
+      for (int q = 0; q < MCG / 2; q++) {
+        const int gi = ex * (MCG / 2) + q;
+        const u32x4 raw = *reinterpret_cast<const u32x4 *>(smem + slot_off + C::S_X +
+                                                           gi * 1024 + lane * 16);
+        const v8i u = unpack32(raw);
+        uint8_t *E = smem + C::OFF_XE + (c & 1) * C::XEB + gi * 2048 + lane * 32;
+        *reinterpret_cast<u32x4 *>(E) = u32x4{(uint32_t)u[0], (uint32_t)u[1], (uint32_t)u[2], (uint32_t)u[3]};
+        *reinterpret_cast<u32x4 *>(E + 16) = u32x4{(uint32_t)u[4], (uint32_t)u[5], (uint32_t)u[6], (uint32_t)u[7]};
+      }
     }
   };
 
   // The K loop of one role with its per-chunk load count as a constant:
   // H wavefronts walk their tile over the MCG groups of every chunk, residual
   // wavefronts their NF items e = ri + NRW k (group e / CT, tile e % CT).
-  auto k_loop = [&](auto HC, auto NFC, v16f(&acc)[2]) {
+  auto k_loop = [&](auto HC, auto NFC, auto &acc) {
     constexpr bool H = decltype(HC)::value;
     constexpr int NF = decltype(NFC)::value;
     constexpr int PER = 1 + NF;   // loads per chunk
     auto item_gi = [&](int k) { return H ? k : (ri + C::NRW * k) / CT; };
     auto item_tile = [&](int k) { return (ri + C::NRW * k) % CT; };
     auto item_frag = [&](int k) { return H ? wave * MCG + k : RT * MCG + ri + C::NRW * k; };
-    auto issue = [&](int c) {
-      const uint32_t slot = lds0 + (c % D) * C::SLOT;
-      mdma(sbase + (uint64_t)min(MCG * c + sgi, KG - 1) * sstride, slot + sdst);
+    // Loads of one chunk.  Full chunks advance two streams: the shared load
+    // (a per-lane address and per-lane chunk stride) and this wavefront's
+    // block loads (wave-uniform bases in scalar registers, lane offset
+    // 16 * lane, MCG KiB per chunk).  A chunk that runs past the last K-group
+    // clamps its groups to the last one.
+    const uint8_t *sh_addr = sbase + (uint64_t)sgi * sstride;
+    const uint64_t sh_inc = (uint64_t)MCG * sstride;
+    const uint32_t lane16 = lane * 16;
+    const uint8_t *fb[NF > 0 ? NF : 1];
 #pragma unroll
-      for (int k = 0; k < NF; k++) {
-        const int g = min(MCG * c + item_gi(k), KG - 1);
-        const uint8_t *src = H ? l1codes + (((int64_t)wave * KG + g) * 64 + lane) * 16
-                               : wcodes + (((int64_t)min(cb * CT + item_tile(k), ct32 - 1) * KG + g) * 64 + lane) * 16;
-        mdma(src, slot + C::S_FR + item_frag(k) * 1024);
+    for (int k = 0; k < NF; k++)
+      fb[k] = m_uniform(H ? l1codes + ((int64_t)wave * KG + item_gi(k)) * 1024
+                          : wcodes + ((int64_t)min(cb * CT + item_tile(k), ct32 - 1) * KG + item_gi(k)) * 1024);
+    uint32_t islot = 0;   // ring offset of the next chunk to issue
+    auto issue = [&](int c) {
+      const uint32_t slot = lds0 + islot;
+      if (MCG * (c + 1) <= KG) {
+        mdma(sh_addr, slot + sdst);
+#pragma unroll
+        for (int k = 0; k < NF; k++) {
+          mdma_s(lane16, fb[k], slot + C::S_FR + item_frag(k) * 1024);
+          fb[k] += MCG * 1024;
+        }
+      } else {
+        mdma(sbase + (uint64_t)min(MCG * c + sgi, KG - 1) * sstride, slot + sdst);
+#pragma unroll
+        for (int k = 0; k < NF; k++) {
+          const int g = min(MCG * c + item_gi(k), KG - 1);
+          mdma_s(lane16, m_uniform(fb[k] - (MCG * c + item_gi(k) - g) * 1024),
+                 slot + C::S_FR + item_frag(k) * 1024);
+          fb[k] += MCG * 1024;
+        }
       }
+      sh_addr += sh_inc;
+      islot = islot + C::SLOT == D * C::SLOT ? 0 : islot + C::SLOT;
     };
 
     mwait_vm<0>();
     stage2_loads();
-#pragma unroll
-    for (int s = 0; s < D - 1; s++) issue(s);
-    mwait_vm<(D - 2) * PER>();   // chunk 0 has landed
+    for (int s = 0; s < D - 1; s++)
+      if (s < NCH) issue(s);
+    if (D - 1 <= NCH) mwait_vm<(D - 2) * PER>();   // chunk 0 has landed
+    else mwait_vm<0>();
     __syncthreads();
-    expand(0);
+    expand(0, 0);
+    uint32_t rslot = 0;   // ring offset of chunk c
     for (int c = 0; c < NCH; c++) {
-      mwait_vm<(D - 3) * PER>();   // chunk c + 1 has landed
+      // chunk c + 1 has landed (near the end of K nothing is issued past the
+      // last chunk, so everything issued is waited for)
+      if (c + D - 1 <= NCH) mwait_vm<(D - 3) * PER>();
+      else mwait_vm<0>();
       __syncthreads();             // chunk c's operands are visible; chunk c - 1 is consumed
-      issue(c + D - 1);            // into chunk c - 1's slot
-      if (c + 1 < NCH) expand(c + 1);
+      if (c + D - 1 < NCH) issue(c + D - 1);   // into chunk c - 1's slot
+      if (c + 1 < NCH) expand(c + 1, rslot + C::SLOT == D * C::SLOT ? 0 : rslot + C::SLOT);
       if constexpr (NF > 0) {
-        const uint8_t *S = smem + (c % D) * C::SLOT;
+        const uint8_t *S = smem + rslot;
         const uint8_t *XE = smem + C::OFF_XE + (c & 1) * C::XEB;
         v8i av[NF];
         u32x4 bv[NF];
@@ -288,28 +337,53 @@ __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, i
                            : C::NPX * 16 + (gi * 32 * CT + 32 * item_tile(k) + l32) * 2;
           sb[k] = *reinterpret_cast<const uint16_t *>(S + C::S_SC + so);
         }
-        v16f cv[NF], pv[NF];
+        // Every operand of the chunk is read before the first product; then
+        // item k's two products go to the matrix core while the vector ALU
+        // expands item k + 1's weight codes and applies item k - 1's fmas.
+        __builtin_amdgcn_sched_barrier(0);
+        v8i bu = unpack32(bv[0]);
+        v16f cp = m_codes_half(av[0], bu);
+        v16f pp = m_outer2(sa[0], sb[0]);
+        if constexpr (NF > 1) bu = unpack32(bv[1]);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int k = 0; k < NF; k++) {
-          cv[k] = m_codes_half(av[k], unpack32(bv[k]));
-          pv[k] = m_outer2(sa[k], sb[k]);
-        }
+        for (int k = 1; k <= NF; k++) {
+          v16f cn, pn;
+          if (k < NF) {
+            cn = m_codes_half(av[k], bu);
+            pn = m_outer2(sa[k], sb[k]);
+            if (k + 1 < NF) bu = unpack32(bv[k + 1]);
+          }
+          v16f &t = acc[H ? 0 : k - 1];
 #pragma unroll
-        for (int k = 0; k < NF; k++) {
-          v16f &t = acc[H ? 0 : k];
-#pragma unroll
-          for (int v = 0; v < 16; v++) t[v] = fmaf(cv[k][v], pv[k][v], t[v]);
+          for (int v = 0; v < 16; v++) t[v] = fmaf(cp[v], pp[v], t[v]);
+          if (k < NF) {
+            // one product, the next operand's expansion, the other product,
+            // the fmas
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            if (k + 1 < NF) __builtin_amdgcn_sched_group_barrier(0x002, 12, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            cp = cn;
+            pp = pn;
+          }
         }
       }
+      rslot = rslot + C::SLOT == D * C::SLOT ? 0 : rslot + C::SLOT;
     }
-    mwait_vm<0>();   // the loads past the end have landed before the ring is reused
   };
 
-  v16f acc[2];
-  acc[0] = v16f{0};
-  acc[1] = v16f{0};
+  constexpr int NACC = C::NF_MAX > 1 ? C::NF_MAX : 1;
+  v16f acc[NACC];
+#pragma unroll
+  for (int k = 0; k < NACC; k++) acc[k] = v16f{0};
   if (hw) {
     if constexpr (RT > 0) k_loop(std::true_type{}, std::integral_constant<int, MCG>{}, acc);
+  } else if (nf == 4) {
+    if constexpr (C::NF_MAX >= 4) k_loop(std::false_type{}, std::integral_constant<int, 4>{}, acc);
+  } else if (nf == 3) {
+    if constexpr (C::NF_MAX >= 3) k_loop(std::false_type{}, std::integral_constant<int, 3>{}, acc);
   } else if (nf == 2) {
     if constexpr (C::NF_MAX >= 2) k_loop(std::false_type{}, std::integral_constant<int, 2>{}, acc);
   } else if (nf == 1) {
@@ -329,11 +403,13 @@ __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, i
     for (int v = 0; v < 16; v++) HS[row_of_32x32(lane, v) * C::HSTR + 32 * wave + l32] = acc[0][v];
   } else {
 #pragma unroll
-    for (int k = 0; k < 2; k++) {
+    for (int k = 0; k < NACC; k++) {
       if (k < nf) {
         const int e = ri + C::NRW * k;
 #pragma unroll
-        for (int v = 0; v < 16; v++) RES[(e * 16 + v) * 64 + lane] = acc[k][v];
+        for (int v = 0; v < 16; v += 4)
+          *reinterpret_cast<v4f *>(RES + (e * 64 + lane) * 16 + v) =
+              v4f{acc[k][v], acc[k][v + 1], acc[k][v + 2], acc[k][v + 3]};
       }
     }
   }
@@ -417,16 +493,23 @@ __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, i
       // the matrix-core products above read operands from every lane: keep
       // them out of the per-lane store branch below
       asm volatile("" : "+v"(ylr));
+      v16f yres = v16f{0};
+#pragma unroll
+      for (int gi = 0; gi < MCG; gi++) {
+        const float *rp = RES + ((gi * CT + j) * 64 + lane) * 16;
+#pragma unroll
+        for (int v = 0; v < 16; v += 4) {
+          const v4f r4 = *reinterpret_cast<const v4f *>(rp + v);
+          yres[v] += r4[0]; yres[v + 1] += r4[1]; yres[v + 2] += r4[2]; yres[v + 3] += r4[3];
+        }
+      }
       const int col = ct * 32 + l32;
       if (col < geo.n) {
 #pragma unroll
         for (int v = 0; v < 16; v++) {
           const int row = 32 * tb + row_of_32x32(lane, v);
           if (row < m) {
-            float yres = 0.0f;
-#pragma unroll
-            for (int gi = 0; gi < MCG; gi++) yres += RES[((gi * CT + j) * 16 + v) * 64 + lane];
-            const float yv = yres + ylr[v];
+            const float yv = yres[v] + ylr[v];
             const uint16_t bits = a.bf16_out ? float_to_bf16_bits(yv) : float_to_half_bits(yv);
             reinterpret_cast<uint16_t *>(a.y)[(int64_t)row * geo.n + col] = bits;
           }
