@@ -100,7 +100,8 @@ tq_status tq_pack_weights(const tq_weight_desc *d, const void *w_res, const void
 
 /* Per-token, per-group activation quantizer (Sec. 2 Eq. 1; Sec. 4.3: the
  * activation is quantized once and shared by both branches).
- *   x         [m,k] fp16 row-major, m >= 0, k % group == 0, group == 64
+ *   x         [m,k] fp16 row-major, 0 <= m <= 2097120 (65535 tiles of 32),
+ *             k % group == 0, group == 64
  *   x_codes   m32 * k / 2 bytes, m32 = m rounded up to a multiple of 32:
  *             tile-major TQ4 codes.  The tokens are cut into tiles of 32 and
  *             K into groups of 64; tile t, group g is one 1 KiB block at byte

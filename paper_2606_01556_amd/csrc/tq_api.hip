@@ -82,7 +82,7 @@ tq_status tq_quant_act(const void *x, int m, int k, int group, void *x_codes, vo
                        void *stream) {
   if (x == nullptr || x_codes == nullptr || x_scales == nullptr) return TQ_ERR_NULL;
   if (group != 64) return TQ_ERR_GROUP;
-  if (m < 0 || k < 1 || k > (1 << 24)) return TQ_ERR_SHAPE;
+  if (m < 0 || m > 65535 * 32 || k < 1 || k > (1 << 24)) return TQ_ERR_SHAPE;
   if (k % group != 0) return TQ_ERR_GROUP;
   if (!aligned16(x) || !aligned16(x_codes) || !aligned16(x_scales)) return TQ_ERR_ALIGN;
   if ((int64_t)m * k >= ((int64_t)1 << 40)) return TQ_ERR_SHAPE;

@@ -9,60 +9,79 @@
 namespace tq {
 
 // ---------------------------------------------------------------------------
-// Activations: one thread per TQ4 word (8 consecutive values); the 8 threads
-// of a group are consecutive lanes of one wavefront and share the group max
-// through three butterfly shuffles.  Codes go to the tile-major layout: 32
-// tokens x one K-group form one 1 KiB block in matrix-core operand lane
-// order (token 32 t + i, codes 32 h .. 32 h + 31 of group g at byte
-// ((t * KG + g) * 64 + 32 h + i) * 16); the padding tokens [m, m32) of the
-// last tile get zero codes.  Scales are stored group-major with the token
-// count padded to m32 (padding entries are zero).
+// Activations: one work-group of 4 wavefronts per QG consecutive 1 KiB
+// matrix-core blocks of one token tile (32 tokens x QG K-groups).  Wavefront
+// w takes tokens 8 w .. 8 w + 7 of the tile; for each of the QG groups, lane
+// 8 j + 4 h + l quantizes codes 32 h + 8 l .. + 7 of the group for token
+// 8 w + j (16 bytes of the row) into one TQ4 word, and the 8 lanes of a token
+// share the group max through three DPP lane swizzles.  All QG loads of a
+// lane are issued before any is used.  Token 32 t + i, codes 32 h .. 32 h + 31
+// of group g land at byte ((t * KG + g) * 64 + 32 h + i) * 16 (the lane order
+// of one matrix-core operand), so each wavefront stores two contiguous
+// 128-byte runs per block.  The padding tokens [m, m32) of the last tile get
+// zero codes.  Scales are stored group-major with the token count padded to
+// m32 (padding entries are zero).
 // ---------------------------------------------------------------------------
+constexpr int QG = 1;
+
+// max over the 8 lanes 8 j .. 8 j + 7 with DPP lane swizzles: swap neighbours,
+// swap pairs, then mirror the two quads of the eight
+__device__ __forceinline__ float max8_dpp(float a) {
+  a = fmaxf(a, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, a), 0xB1, 0xF, 0xF, false)));
+  a = fmaxf(a, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, a), 0x4E, 0xF, 0xF, false)));
+  a = fmaxf(a, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, a), 0x141, 0xF, 0xF, false)));
+  return a;
+}
+
 __global__ __launch_bounds__(256) void quant_act_kernel(const uint16_t *__restrict__ x, int m,
                                                         int k, uint32_t *__restrict__ codes,
                                                         uint16_t *__restrict__ scales) {
-  const int64_t words_per_row = k >> 3;
-  const int m32 = (m + 31) / 32 * 32;
-  const int64_t nwords = (int64_t)m32 * words_per_row;
-  const int64_t wid = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t row = wid / words_per_row, w = wid % words_per_row;
-  const bool valid = wid < nwords;
-  const bool real = row < m;   // uniform over the 8 lanes of a group
-  u32x4 raw = {0, 0, 0, 0};
-  if (valid && real) raw = *reinterpret_cast<const u32x4 *>(x + wid * 8);
-  float v[8];
+  const int KG = k / kGroup;
+  const int g0 = blockIdx.x * QG, t = blockIdx.y;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int j = lane >> 3, h = (lane >> 2) & 1, l = lane & 3;
+  const int i = 8 * w + j;          // token within the tile
+  const int row = 32 * t + i;
+  const int m32 = (int)gridDim.y * 32;
+  u32x4 raw[QG];
 #pragma unroll
-  for (int i = 0; i < 4; i++) {
-    v[2 * i] = half_bits_to_float((uint16_t)(raw[i] & 0xffffu));
-    v[2 * i + 1] = half_bits_to_float((uint16_t)(raw[i] >> 16));
+  for (int q = 0; q < QG; q++) {
+    raw[q] = u32x4{0, 0, 0, 0};
+    if (row < m && g0 + q < KG)
+      raw[q] = *reinterpret_cast<const u32x4 *>(x + (int64_t)row * k + (g0 + q) * kGroup + 32 * h + 8 * l);
   }
-  float amax = 0.0f;
 #pragma unroll
-  for (int i = 0; i < 8; i++) amax = fmaxf(amax, fabsf(v[i]));
-  amax = fmaxf(amax, __shfl_xor(amax, 1));
-  amax = fmaxf(amax, __shfl_xor(amax, 2));
-  amax = fmaxf(amax, __shfl_xor(amax, 4));
-  uint16_t s16;
-  const float s = q4_scale(amax, s16);
-  int c[8];
+  for (int q = 0; q < QG; q++) {
+    const int g = g0 + q;
+    float v[8];
 #pragma unroll
-  for (int i = 0; i < 8; i++) c[i] = q4_code(v[i], s);
-  if (valid) {
-    const int64_t KG = k / kGroup;
-    const int64_t g = w >> 3, h = (w >> 2) & 1, wl = w & 3;
-    const int64_t t = row >> 5, i = row & 31;
-    codes[((t * KG + g) * 64 + 32 * h + i) * 4 + wl] = tq4_pack8(c);
-    if ((w & 7) == 0) scales[g * m32 + row] = real ? s16 : (uint16_t)0;
+    for (int e = 0; e < 4; e++) {
+      v[2 * e] = half_bits_to_float((uint16_t)(raw[q][e] & 0xffffu));
+      v[2 * e + 1] = half_bits_to_float((uint16_t)(raw[q][e] >> 16));
+    }
+    float amax = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 8; e++) amax = fmaxf(amax, fabsf(v[e]));
+    amax = max8_dpp(amax);
+    uint16_t s16;
+    const float s = q4_scale(amax, s16);
+    const float y = __builtin_amdgcn_rcpf(s);
+    int c[8];
+#pragma unroll
+    for (int e = 0; e < 8; e++) c[e] = q4_code_fp16(v[e], s, y);
+    if (g < KG) {
+      codes[(((int64_t)t * KG + g) * 64 + 32 * h + i) * 4 + l] = tq4_pack8(c);
+      if ((lane & 7) == 0) scales[(int64_t)g * m32 + row] = row < m ? s16 : (uint16_t)0;
+    }
   }
 }
 
 hipError_t launch_quant_act(const uint16_t *x, int m, int k, uint32_t *codes, uint16_t *scales,
                             hipStream_t s) {
-  const int64_t m32 = (m + 31) / 32 * 32;
-  const int64_t nwords = m32 * (k / 8);
-  const int64_t blocks = (nwords + 255) / 256;
-  hipLaunchKernelGGL(quant_act_kernel, dim3((unsigned)blocks), dim3(256), 0, s, x, m, k, codes,
-                     scales);
+  const int m32 = (m + 31) / 32 * 32;
+  const int KG = k / kGroup;
+  hipLaunchKernelGGL(quant_act_kernel, dim3((unsigned)((KG + QG - 1) / QG), (unsigned)(m32 / 32)),
+                     dim3(256), 0, s, x, m, k, codes, scales);
   return hipGetLastError();
 }
 

@@ -72,6 +72,7 @@ def test_quant_act_validation(L):
     assert L.tq_quant_act(FAKE, 4, 64, 32, FAKE, FAKE, None) == 3
     assert L.tq_quant_act(FAKE, 4, 100, 64, FAKE, FAKE, None) == 3
     assert L.tq_quant_act(FAKE, -1, 64, 64, FAKE, FAKE, None) == 2
+    assert L.tq_quant_act(FAKE, 65535 * 32 + 1, 64, 64, FAKE, FAKE, None) == 2   # more token tiles than the grid holds
     assert L.tq_quant_act(FAKE + 8, 4, 64, 64, FAKE, FAKE, None) == 6
     assert L.tq_quant_act(FAKE, 0, 64, 64, FAKE, FAKE, None) == 0      # empty: no launch
 

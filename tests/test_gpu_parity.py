@@ -195,6 +195,35 @@ def test_zero_groups(oracle_mod):
     assert np.all(g["qH"][3] == 0) and np.all(g["sH"][3] == 0)
 
 
+def test_activation_rounding_ties(oracle_mod):
+    """Activation groups whose values sit exactly on half-integer multiples of
+    the group scale (and one fp16 ulp to either side of them), with scales
+    whose reciprocals are inexact in fp32, normal and subnormal in fp16: the
+    codes must follow round-half-to-even of the exact quotient, as the oracle's
+    IEEE division does."""
+    say("activation rounding ties")
+    scales = [3.0, 5.0, 0.375, 1.25, 1.75, 3 * 2.0 ** -10, 5 * 2.0 ** -14, 3 * 2.0 ** -20,
+              11 * 2.0 ** -2, 13 * 2.0 ** -5, 9 * 2.0 ** -8, 6.0, 15 * 2.0 ** -12, 7 * 2.0 ** 3]
+    M, G = 40, 24
+    rng = np.random.default_rng(17)
+    X = np.zeros((M, 64 * G), dtype=np.float16)
+    for row in range(M):
+        for grp in range(G):
+            S = np.float16(scales[(row + 3 * grp) % len(scales)])
+            ties = np.array([(k + 0.5) * float(S) for k in range(-7, 7)], dtype=np.float16)
+            assert np.all(ties.astype(np.float64) == np.arange(-6.5, 7.0) * float(S))
+            up = np.nextafter(ties, np.float16(np.inf))
+            dn = np.nextafter(ties, np.float16(-np.inf))
+            pool = np.concatenate([ties, ties, up, dn])
+            vals = rng.choice(pool, 64)
+            vals[rng.integers(0, 64)] = np.float16(7 * float(S)) * np.float16(rng.choice([-1, 1]))
+            X[row, 64 * grp:64 * (grp + 1)] = vals
+    d = random_codes_layer(M, 64 * G, 96, 16, seed=23)
+    g, o = full_parity(oracle_mod, X, d["W_res"], d["L1"], d["L2"])
+    qx, _ = oracle_mod.quantize(X, GROUP)
+    assert np.count_nonzero(np.abs(qx) % 2 == 0) > 0   # ties resolved to even codes occur
+
+
 def test_integer_accumulators_exact(oracle_mod):
     """Every group max is 7, so all scales are 1 and Y is the exact integer sum
     of the code products: the integer accumulators show through unrounded."""
