@@ -543,21 +543,24 @@ hipError_t launch_mid_rt(const GemmArgs &a, hipStream_t s) {
   }
 }
 
-// time of one workgroup in tile-groups per SIMD and chunk: the H chain takes
-// MCG, the rest spreads over the 4 SIMDs
-int mid_cost(int rt, int ct, int n_wg) {
-  const int per_simd = (MCG * (rt + ct) + 3) / 4;
-  const int chain = rt > 0 ? MCG : 0;
-  const int rounds = (n_wg + 255) / 256;
-  return rounds * (per_simd > chain ? per_simd : chain);
+// Each work-group runs one serial K loop whose length grows with the
+// tile-groups it owns (H and residual), so the cost of a choice of CT is the
+// number of rounds of work-groups over the 256 CUs times the tile-groups per
+// work-group and chunk.
+int mid_cost(int rt, int ct, int n_rb, int ct32) {
+  const int n_wg = n_rb * ((ct32 + ct - 1) / ct);
+  return (n_wg + 255) / 256 * MCG * (rt + ct);
 }
 
 }  // namespace
 
 hipError_t launch_dual_gemm_mid(const GemmArgs &a, hipStream_t s) {
   const int rt = a.geo.r_pad32 / 32, ct32 = a.geo.n_pad / 32, n_rb = a.ms / 32;
-  int ct = mid_cost(rt, 4, n_rb * ((ct32 + 3) / 4)) < mid_cost(rt, 2, n_rb * ((ct32 + 1) / 2)) ? 4 : 2;
-  if (const char *env = getenv("TQ_MID_CT")) ct = atoi(env) == 4 ? 4 : 2;
+  int ct = 1;
+  for (int c : {2, 4})
+    if (mid_cost(rt, c, n_rb, ct32) < mid_cost(rt, ct, n_rb, ct32)) ct = c;
+  if (const char *env = getenv("TQ_MID_CT")) ct = atoi(env);
+  if (ct == 1) return launch_mid_rt<1>(a, s);
   return ct == 4 ? launch_mid_rt<4>(a, s) : launch_mid_rt<2>(a, s);
 }
 

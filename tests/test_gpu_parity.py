@@ -160,12 +160,12 @@ def test_decode_kernel_variants(oracle_mod, M, K, N, r):
     full_parity(oracle_mod, d["X"], d["W_res"], d["L1"], d["L2"])
 
 
-@pytest.mark.parametrize("ct", ["2", "4"])
+@pytest.mark.parametrize("ct", ["1", "2", "4"])
 @pytest.mark.parametrize("M,K,N,r", [(17, 192, 100, 32), (32, 320, 4096, 64), (64, 128, 1000, 128),
                                      (100, 448, 520, 16), (128, 256, 4096, 64), (250, 64, 96, 8),
                                      (40, 576, 8192, 0), (512, 128, 256, 64)])
 def test_mid_kernel_variants(oracle_mod, monkeypatch, ct, M, K, N, r):
-    """16 < m <= 512 with 2 and 4 column tiles per workgroup, odd K-group counts
+    """16 < m <= 512 with 1, 2 and 4 column tiles per workgroup, odd K-group counts
     (a half chunk at the end of K) and every rank-tile count."""
     monkeypatch.setenv("TQ_MID_CT", ct)
     say(f"mid ct={ct} M={M} K={K} N={N} r={r}")
