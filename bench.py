@@ -38,8 +38,8 @@ FP8_MFMA_PEAK_TFLOPS = 5000.0   # MI355X dense fp8 matrix peak (5.0 PFLOP/s)
 HBM_PEAK_GBS = 8000.0
 ROTATE_BYTES = 1 << 30
 CALIB_COPY_BYTES = 256 << 20
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_prefill_kernel_m2048_llama3_8b_qo.json")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2606_01556_amd", "csrc", "tq_gemm_prefill.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_large_kernel_m2048_llama3_8b_qo.json")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2606_01556_amd", "csrc", "tq_gemm_large.hip")
 
 
 def measured_traffic():

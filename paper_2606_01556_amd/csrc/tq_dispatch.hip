@@ -1,7 +1,9 @@
 // Kernel selection for the fused layer by token count: the decode kernel for
 // m <= 16 (bound by the weight bytes and by H's K-long chain), the mid kernel
-// (32-token blocks, H formed per block) up to a few hundred tokens, the
-// prefill kernel (128-token blocks) beyond.
+// (32-token blocks, H formed per block) up to a few hundred tokens, then the
+// large kernel (128 x 256 blocks, 16 wavefronts) while its blocks fit in one
+// round over the CUs, and the prefill kernel (H shared by runs of column
+// blocks) beyond.
 #include <stdlib.h>
 
 #include "tq_kernels.hpp"
@@ -9,10 +11,17 @@
 namespace tq {
 
 hipError_t launch_dual_gemm(const GemmArgs &a, hipStream_t s) {
-  const char *env = getenv("TQ_MID_MAX");   // crossover override for tuning sweeps
+  const char *env = getenv("TQ_MID_MAX");   // crossover overrides for tuning sweeps
   const int mid_max = env ? atoi(env) : 512;
   if (a.m <= 16) return launch_dual_gemm_decode(a, s);
   if (a.m <= mid_max) return launch_dual_gemm_mid(a, s);
+  // 128 x 256 blocks: while they fit in one round over the 256 CUs the large
+  // kernel (16 wavefronts, H formed in the main loop) is faster; beyond, the
+  // prefill kernel forms H once per run of column blocks
+  const int blocks = (a.m + 127) / 128 * ((a.geo.n_pad + 255) / 256);
+  int large = blocks <= 256;
+  if (const char *lenv = getenv("TQ_LARGE")) large = atoi(lenv);
+  if (large) return launch_dual_gemm_large(a, s);
   return launch_dual_gemm_prefill(a, s);
 }
 

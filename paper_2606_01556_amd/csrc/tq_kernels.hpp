@@ -44,5 +44,6 @@ hipError_t launch_dual_gemm(const GemmArgs &a, hipStream_t s);
 hipError_t launch_dual_gemm_decode(const GemmArgs &a, hipStream_t s);  // m <= 16
 hipError_t launch_dual_gemm_mid(const GemmArgs &a, hipStream_t s);      // mid sizes
 hipError_t launch_dual_gemm_prefill(const GemmArgs &a, hipStream_t s);  // prefill sizes
+hipError_t launch_dual_gemm_large(const GemmArgs &a, hipStream_t s);    // large token counts
 
 }  // namespace tq

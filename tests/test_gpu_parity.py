@@ -3,11 +3,11 @@
 Bit-exact: activation codes and scales, weight codes and scales (via the
 canonical export), the on-chip low-rank intermediate H, its scales s_H and
 codes Q_H.  The library serves m <= 16 with the decode kernel, m up to 512
-with the mid kernel and larger m with the prefill kernel.  The prefill kernel
-accumulates every output in the same ascending-group fma order as the oracle,
-so its rounded output Y is bit-exact too; the decode and mid kernels split the
-residual K loop over wavefronts, which changes only the fp32 summation order
-of Y.  The benchmark spec's tolerance (relative Frobenius 1e-3, max-abs
+with the mid kernel and larger m with the large kernel (one round of 128 x 256
+blocks) or the prefill kernel.  The large and prefill kernels accumulate every
+output in the same ascending-group fma order as the oracle, so their rounded
+output Y is bit-exact too; the decode and mid kernels split the residual K
+loop over wavefronts, which changes only the fp32 summation order of Y.  The benchmark spec's tolerance (relative Frobenius 1e-3, max-abs
 1e-2 * rms(Y)) is checked everywhere, against the oracle's fp64 result.
 """
 import numpy as np
@@ -25,7 +25,7 @@ MAX_ABS_RMS = 1e-2
 # rounding of the output alone reaches ~1.1e-3 relative Frobenius error, so the
 # fp16 bounds are scaled by 8 for bf16 results.
 BF16_FACTOR = 8.0
-# smallest token count served by the prefill kernel (bit-exact Y)
+# smallest token count served by the large / prefill kernels (bit-exact Y)
 PREFILL_FROM = 513
 
 
@@ -170,6 +170,19 @@ def test_mid_kernel_variants(oracle_mod, monkeypatch, ct, M, K, N, r):
     monkeypatch.setenv("TQ_MID_CT", ct)
     say(f"mid ct={ct} M={M} K={K} N={N} r={r}")
     d = random_codes_layer(M, K, N, r, seed=M * 7 + N + r)
+    full_parity(oracle_mod, d["X"], d["W_res"], d["L1"], d["L2"])
+
+
+@pytest.mark.parametrize("large", ["0", "1"])
+@pytest.mark.parametrize("M,K,N,r", [(600, 576, 1000, 64), (1100, 256, 520, 128), (700, 320, 300, 16),
+                                     (900, 128, 2000, 0), (530, 192, 4096, 32)])
+def test_large_m_kernels(oracle_mod, monkeypatch, large, M, K, N, r):
+    """m > 512 on both large-m kernels (16-wavefront blocks with H in the main
+    loop, and the prefill kernel with its separate H pass): ragged token and
+    column counts, odd K-group counts, every rank-tile count; Y bit-exact."""
+    monkeypatch.setenv("TQ_LARGE", large)
+    say(f"large={large} M={M} K={K} N={N} r={r}")
+    d = random_codes_layer(M, K, N, r, seed=M + 3 * N + r)
     full_parity(oracle_mod, d["X"], d["W_res"], d["L1"], d["L2"])
 
 
