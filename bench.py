@@ -150,7 +150,7 @@ def main():
         call[0] += 1
         if ev is not None:
             ev[0].record(stream)
-        tq.dual_gemm(desc, p, xc, xs, m, Y[m], stream=s)
+        tq.dual_gemm(desc, p, xc, xs, m, Y[m], lay.workspace, stream=s)
         if ev is not None:
             ev[1].record(stream)
 
@@ -197,7 +197,7 @@ def main():
         def g():
             p = copies[call[0] % ncopy]
             call[0] += 1
-            tq.dual_gemm(desc, p, xc, xs, m, Y[m], stream=s)
+            tq.dual_gemm(desc, p, xc, xs, m, Y[m], lay.workspace, stream=s)
         us_gemm = timed(g)
         def f16():
             wt = WTs[call[0] % nwt]

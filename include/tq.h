@@ -21,7 +21,8 @@
  *
  * Conventions for every entry point:
  *  - All array pointers are DEVICE pointers owned by the caller; the library
- *    never allocates, frees or synchronizes and keeps no global state.
+ *    never allocates, frees or synchronizes and keeps no global state (the
+ *    few bytes of state tq_dual_gemm needs live in the caller's workspace).
  *    Device pointers must be 16-byte aligned (TQ_ERR_ALIGN otherwise).
  *  - `stream` is a hipStream_t (NULL = the default stream).  Work is enqueued
  *    asynchronously on it; results are visible after the stream completes.
@@ -119,27 +120,39 @@ tq_status tq_pack_weights(const tq_weight_desc *d, const void *w_res, const void
 tq_status tq_quant_act(const void *x, int m, int k, int group, void *x_codes,
                        void *x_scales, void *stream);
 
+/* Size in bytes of the workspace that tq_dual_gemm takes (a constant of the
+ * library build; currently 8448). */
+size_t tq_workspace_bytes(void);
+
 /* The fused dual-component layer: residual 4-bit GEMM, low-rank stage 1
- * (H = Q(X) Q(L1), kept on chip), on-the-fly re-quantization of H, stage 2
- * (Q_H Q(L2)), and one epilogue that sums both branches and stores Y once.
+ * (H = Q(X) Q(L1)), on-the-fly re-quantization of H, stage 2 (Q_H Q(L2)),
+ * and one epilogue that sums both branches and stores Y once.
  *   packed            buffer written by tq_pack_weights for descriptor d
  *   x_codes/x_scales  written by tq_quant_act for the same k (m tokens)
  *   y                 [m,n] output, fp16 or bf16 per y_dtype, row-major
- * One kernel launch, no workspace, no global intermediate.  m == 0 is a
- * no-op.  Errors: TQ_ERR_NULL, TQ_ERR_SHAPE, TQ_ERR_BUFFER, TQ_ERR_DTYPE,
- * TQ_ERR_ALIGN, TQ_ERR_HIP. */
+ *   workspace         device buffer of tq_workspace_bytes() bytes, owned by
+ *                     the caller, zero-filled before its first use.  Every
+ *                     call leaves it zero-filled again.  Calls that share a
+ *                     workspace must not run concurrently (calls on one
+ *                     stream never do); give each stream its own.  At
+ *                     m <= 16 the work-groups of the launch hand H from the
+ *                     ones that form it to the others through it; larger m
+ *                     keep H on chip and do not touch it.
+ * One kernel launch.  m == 0 is a no-op.  Errors: TQ_ERR_NULL, TQ_ERR_SHAPE,
+ * TQ_ERR_BUFFER, TQ_ERR_DTYPE, TQ_ERR_ALIGN, TQ_ERR_HIP. */
 tq_status tq_dual_gemm(const tq_weight_desc *d, const void *packed, const void *x_codes,
-                       const void *x_scales, int m, void *y, tq_dtype y_dtype, void *stream);
+                       const void *x_scales, int m, void *y, tq_dtype y_dtype, void *workspace,
+                       void *stream);
 
 /* Same computation and kernel as tq_dual_gemm, for tests: additionally
- * copies the on-chip low-rank intermediate of every token out of the kernel.
+ * copies the low-rank intermediate of every token out of the kernel.
  *   h   [m,r] fp32     H before re-quantization
  *   sh  [m,r/group_r]  fp32 scales s_H
  *   qh  [m,r] int8     codes Q_H in [-7, 7]
  * Errors as tq_dual_gemm; additionally TQ_ERR_RANK when r == 0. */
 tq_status tq_dual_gemm_debug(const tq_weight_desc *d, const void *packed, const void *x_codes,
                              const void *x_scales, int m, void *y, tq_dtype y_dtype,
-                             void *h, void *sh, void *qh, void *stream);
+                             void *h, void *sh, void *qh, void *workspace, void *stream);
 
 /* Copy the packed weights out in the canonical layout (for tests/debug):
  *   w_codes  [n, k/8] TQ4 words      w_scales  [n, k/group] fp16

@@ -38,7 +38,7 @@ class WeightDesc(ctypes.Structure):
 
 
 EXPORTS = ("tq_weight_desc_init", "tq_pack_weights", "tq_quant_act", "tq_dual_gemm",
-           "tq_dual_gemm_debug", "tq_export_weights", "tq_status_string")
+           "tq_dual_gemm_debug", "tq_export_weights", "tq_workspace_bytes", "tq_status_string")
 
 _lib = None
 
@@ -56,13 +56,16 @@ def lib() -> ctypes.CDLL:
         L.tq_weight_desc_init.argtypes = [I, I, I, I, D]
         L.tq_pack_weights.argtypes = [D, P, P, P, P, P]
         L.tq_quant_act.argtypes = [P, I, I, I, P, P, P]
-        L.tq_dual_gemm.argtypes = [D, P, P, P, I, P, I, P]
-        L.tq_dual_gemm_debug.argtypes = [D, P, P, P, I, P, I, P, P, P, P]
+        L.tq_dual_gemm.argtypes = [D, P, P, P, I, P, I, P, P]
+        L.tq_dual_gemm_debug.argtypes = [D, P, P, P, I, P, I, P, P, P, P, P]
+        L.tq_workspace_bytes.argtypes = []
+        L.tq_workspace_bytes.restype = ctypes.c_size_t
         L.tq_export_weights.argtypes = [D, P, P, P, P, P, P, P, P]
         L.tq_status_string.argtypes = [I]
         L.tq_status_string.restype = ctypes.c_char_p
-        for name in EXPORTS[:-1]:
-            getattr(L, name).restype = I
+        for name in EXPORTS:
+            if name not in ("tq_workspace_bytes", "tq_status_string"):
+                getattr(L, name).restype = I
         _lib = L
     return _lib
 
@@ -108,16 +111,22 @@ def quant_act(x, x_codes, x_scales, group: int = GROUP, stream=None):
            "tq_quant_act")
 
 
-def dual_gemm(desc: WeightDesc, packed, x_codes, x_scales, m: int, y, bf16: bool = False, stream=None):
+def workspace_bytes() -> int:
+    return int(lib().tq_workspace_bytes())
+
+
+def dual_gemm(desc: WeightDesc, packed, x_codes, x_scales, m: int, y, workspace, bf16: bool = False,
+              stream=None):
     _check(lib().tq_dual_gemm(ctypes.byref(desc), _ptr(packed), _ptr(x_codes), _ptr(x_scales), m,
-                              _ptr(y), TQ_BF16 if bf16 else TQ_F16, _stream(stream)), "tq_dual_gemm")
+                              _ptr(y), TQ_BF16 if bf16 else TQ_F16, _ptr(workspace), _stream(stream)),
+           "tq_dual_gemm")
 
 
-def dual_gemm_debug(desc: WeightDesc, packed, x_codes, x_scales, m: int, y, h, sh, qh,
+def dual_gemm_debug(desc: WeightDesc, packed, x_codes, x_scales, m: int, y, h, sh, qh, workspace,
                     bf16: bool = False, stream=None):
     _check(lib().tq_dual_gemm_debug(ctypes.byref(desc), _ptr(packed), _ptr(x_codes), _ptr(x_scales), m,
                                     _ptr(y), TQ_BF16 if bf16 else TQ_F16, _ptr(h), _ptr(sh), _ptr(qh),
-                                    _stream(stream)), "tq_dual_gemm_debug")
+                                    _ptr(workspace), _stream(stream)), "tq_dual_gemm_debug")
 
 
 def export_weights(desc: WeightDesc, packed, w_codes, w_scales, l1_codes=None, l1_scales=None,
@@ -131,6 +140,12 @@ def export_weights(desc: WeightDesc, packed, w_codes, w_scales, l1_codes=None, l
 def empty_packed(desc: WeightDesc, device="cuda"):
     import torch
     return torch.empty(int(desc.packed_bytes), dtype=torch.uint8, device=device)
+
+
+def empty_workspace(device="cuda"):
+    """A zero-filled workspace for tq_dual_gemm (one per stream that runs layers)."""
+    import torch
+    return torch.zeros(workspace_bytes(), dtype=torch.uint8, device=device)
 
 
 def padded_tokens(m: int) -> int:
@@ -149,7 +164,9 @@ def empty_act(m: int, k: int, device="cuda"):
 
 
 class Layer:
-    """One packed layer: descriptor + packed device buffer (device memory from torch)."""
+    """One packed layer: descriptor, packed device buffer and a workspace (device
+    memory from torch).  Calls of one Layer must not overlap in time: run them
+    on one stream, or pass each stream's own workspace to dual_gemm."""
 
     def __init__(self, w_res, l1=None, l2=None, group: int = GROUP, stream=None):
         n, k = w_res.shape
@@ -158,6 +175,7 @@ class Layer:
         self.packed = empty_packed(self.desc, w_res.device)
         pack_weights(self.desc, w_res.contiguous(), None if l1 is None else l1.contiguous(),
                      None if l2 is None else l2.contiguous(), self.packed, stream)
+        self.workspace = empty_workspace(w_res.device)
         self.n, self.k, self.rank = n, k, r
 
     def __call__(self, x, bf16: bool = False, stream=None):
@@ -166,7 +184,7 @@ class Layer:
         xc, xs = empty_act(m, self.k, x.device)
         y = torch.empty((m, self.n), dtype=torch.bfloat16 if bf16 else torch.float16, device=x.device)
         quant_act(x.contiguous(), xc, xs, stream=stream)
-        dual_gemm(self.desc, self.packed, xc, xs, m, y, bf16, stream)
+        dual_gemm(self.desc, self.packed, xc, xs, m, y, self.workspace, bf16, stream)
         return y
 
 

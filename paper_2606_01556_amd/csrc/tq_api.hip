@@ -95,13 +95,15 @@ tq_status tq_quant_act(const void *x, int m, int k, int group, void *x_codes, vo
 
 static tq_status dual_gemm_impl(const tq_weight_desc *d, const void *packed, const void *x_codes,
                                 const void *x_scales, int m, void *y, tq_dtype y_dtype, void *h,
-                                void *sh, void *qh, void *stream) {
-  if (d == nullptr || packed == nullptr || x_codes == nullptr || x_scales == nullptr || y == nullptr)
+                                void *sh, void *qh, void *workspace, void *stream) {
+  if (d == nullptr || packed == nullptr || x_codes == nullptr || x_scales == nullptr ||
+      y == nullptr || workspace == nullptr)
     return TQ_ERR_NULL;
   if (!desc_ok(d)) return TQ_ERR_BUFFER;
   if (m < 0 || m > (1 << 24)) return TQ_ERR_SHAPE;
   if (y_dtype != TQ_F16 && y_dtype != TQ_BF16) return TQ_ERR_DTYPE;
-  if (!aligned16(packed) || !aligned16(x_codes) || !aligned16(x_scales) || !aligned16(y))
+  if (!aligned16(packed) || !aligned16(x_codes) || !aligned16(x_scales) || !aligned16(y) ||
+      !aligned16(workspace))
     return TQ_ERR_ALIGN;
   if (h != nullptr && (!aligned16(h) || !aligned16(sh) || !aligned16(qh))) return TQ_ERR_ALIGN;
   if (m == 0) return TQ_OK;
@@ -117,21 +119,25 @@ static tq_status dual_gemm_impl(const tq_weight_desc *d, const void *packed, con
   a.dbg_h = static_cast<float *>(h);
   a.dbg_sh = static_cast<float *>(sh);
   a.dbg_qh = static_cast<int8_t *>(qh);
+  a.ws = static_cast<uint32_t *>(workspace);
   return hip_status(tq::launch_dual_gemm(a, static_cast<hipStream_t>(stream)));
 }
 
+size_t tq_workspace_bytes(void) { return tq::kWorkspaceBytes; }
+
 tq_status tq_dual_gemm(const tq_weight_desc *d, const void *packed, const void *x_codes,
-                       const void *x_scales, int m, void *y, tq_dtype y_dtype, void *stream) {
+                       const void *x_scales, int m, void *y, tq_dtype y_dtype, void *workspace,
+                       void *stream) {
   return dual_gemm_impl(d, packed, x_codes, x_scales, m, y, y_dtype, nullptr, nullptr, nullptr,
-                        stream);
+                        workspace, stream);
 }
 
 tq_status tq_dual_gemm_debug(const tq_weight_desc *d, const void *packed, const void *x_codes,
                              const void *x_scales, int m, void *y, tq_dtype y_dtype, void *h,
-                             void *sh, void *qh, void *stream) {
+                             void *sh, void *qh, void *workspace, void *stream) {
   if (h == nullptr || sh == nullptr || qh == nullptr) return TQ_ERR_NULL;
   if (d != nullptr && d->rank == 0) return TQ_ERR_RANK;
-  return dual_gemm_impl(d, packed, x_codes, x_scales, m, y, y_dtype, h, sh, qh, stream);
+  return dual_gemm_impl(d, packed, x_codes, x_scales, m, y, y_dtype, h, sh, qh, workspace, stream);
 }
 
 tq_status tq_export_weights(const tq_weight_desc *d, const void *packed, void *w_codes,

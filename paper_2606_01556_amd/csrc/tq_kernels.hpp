@@ -6,6 +6,11 @@
 
 namespace tq {
 
+// Largest supported rank, and the size of the caller's workspace of
+// tq_dual_gemm (its layout is private to the decode kernel).
+constexpr int kMaxRank = 128;
+constexpr size_t kWorkspaceBytes = 20480;
+
 // Geometry shared by the packing, export and GEMM kernels.
 //  W_res codes: [n_pad/32][k/64] blocks of 1 KiB; block lane L (16 bytes,
 //               4 TQ4 words) holds column 32*t + L%32, k in [32*(L/32), +32)
@@ -31,6 +36,7 @@ struct GemmArgs {
   float *dbg_h;         // optional [m][r]
   float *dbg_sh;        // optional [m][r/gr]
   int8_t *dbg_qh;       // optional [m][r]
+  uint32_t *ws;         // kWorkspaceBytes, zero between calls (decode kernel)
 };
 
 hipError_t launch_quant_act(const uint16_t *x, int m, int k, uint32_t *codes, uint16_t *scales,

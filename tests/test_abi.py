@@ -81,19 +81,23 @@ def test_dual_gemm_validation(L):
     d = tq.weight_desc_init(128, 128, 16)
     bad = tq.WeightDesc()
     D = ctypes.byref
-    assert L.tq_dual_gemm(D(d), None, FAKE, FAKE, 4, FAKE, 0, None) == 1
-    assert L.tq_dual_gemm(D(bad), FAKE, FAKE, FAKE, 4, FAKE, 0, None) == 7
-    assert L.tq_dual_gemm(D(d), FAKE, FAKE, FAKE, 4, FAKE, 7, None) == 5
-    assert L.tq_dual_gemm(D(d), FAKE, FAKE, FAKE, -2, FAKE, 0, None) == 2
-    assert L.tq_dual_gemm(D(d), FAKE, FAKE + 4, FAKE, 4, FAKE, 0, None) == 6
-    assert L.tq_dual_gemm(D(d), FAKE, FAKE, FAKE, 0, FAKE, 0, None) == 0
+    assert L.tq_dual_gemm(D(d), None, FAKE, FAKE, 4, FAKE, 0, FAKE, None) == 1
+    assert L.tq_dual_gemm(D(bad), FAKE, FAKE, FAKE, 4, FAKE, 0, FAKE, None) == 7
+    assert L.tq_dual_gemm(D(d), FAKE, FAKE, FAKE, 4, FAKE, 7, FAKE, None) == 5
+    assert L.tq_dual_gemm(D(d), FAKE, FAKE, FAKE, -2, FAKE, 0, FAKE, None) == 2
+    assert L.tq_dual_gemm(D(d), FAKE, FAKE + 4, FAKE, 4, FAKE, 0, FAKE, None) == 6
+    assert L.tq_dual_gemm(D(d), FAKE, FAKE, FAKE, 0, FAKE, 0, FAKE, None) == 0
     d0 = tq.weight_desc_init(128, 128, 0)
-    assert L.tq_dual_gemm_debug(D(d0), FAKE, FAKE, FAKE, 4, FAKE, 0, FAKE, FAKE, FAKE, None) == 4
-    assert L.tq_dual_gemm_debug(D(d), FAKE, FAKE, FAKE, 4, FAKE, 0, None, FAKE, FAKE, None) == 1
+    assert L.tq_dual_gemm_debug(D(d0), FAKE, FAKE, FAKE, 4, FAKE, 0, FAKE, FAKE, FAKE, FAKE, None) == 4
+    assert L.tq_dual_gemm_debug(D(d), FAKE, FAKE, FAKE, 4, FAKE, 0, None, FAKE, FAKE, FAKE, None) == 1
+    # the workspace is required and 16-byte aligned
+    assert L.tq_dual_gemm(D(d), FAKE, FAKE, FAKE, 4, FAKE, 0, None, None) == 1
+    assert L.tq_dual_gemm(D(d), FAKE, FAKE, FAKE, 4, FAKE, 0, FAKE + 8, None) == 6
+    assert L.tq_workspace_bytes() >= 256 + 16 * 128 * 5 and L.tq_workspace_bytes() % 256 == 0
     # a descriptor edited after init is rejected
     d3 = tq.weight_desc_init(128, 128, 16)
     d3.n_pad = 64
-    assert L.tq_dual_gemm(D(d3), FAKE, FAKE, FAKE, 4, FAKE, 0, None) == 7
+    assert L.tq_dual_gemm(D(d3), FAKE, FAKE, FAKE, 4, FAKE, 0, FAKE, None) == 7
 
 
 def test_pack_export_validation(L):

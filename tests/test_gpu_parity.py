@@ -61,10 +61,10 @@ def run_gpu(X, W, L1, L2, bf16=False, debug=True):
         h = torch.empty((M, r), dtype=torch.float32, device="cuda")
         sh = torch.empty((M, r // d.group_r), dtype=torch.float32, device="cuda")
         qh = torch.empty((M, r), dtype=torch.int8, device="cuda")
-        tq.dual_gemm_debug(d, lay.packed, xc, xs, M, y, h, sh, qh, bf16)
+        tq.dual_gemm_debug(d, lay.packed, xc, xs, M, y, h, sh, qh, lay.workspace, bf16)
         out.update(H=h, sH=sh, qH=qh)
     else:
-        tq.dual_gemm(d, lay.packed, xc, xs, M, y, bf16)
+        tq.dual_gemm(d, lay.packed, xc, xs, M, y, lay.workspace, bf16)
     wc = torch.empty((N, K // 8), dtype=torch.int32, device="cuda")
     ws = torch.empty((N, K // GROUP), dtype=torch.float16, device="cuda")
     ex = [wc, ws]
@@ -76,6 +76,8 @@ def run_gpu(X, W, L1, L2, bf16=False, debug=True):
         ex += [l1c, l1s, l2c, l2s]
     tq.export_weights(d, lay.packed, *ex)
     torch.cuda.synchronize()
+    # the call leaves its workspace counters (ticket, ready, done, error) at zero
+    assert lay.workspace[:16].cpu().numpy().tolist() == [0] * 16
     out["xq"] = tq.act_codes_rows(xc.cpu().numpy(), M)
     xs_all = xs.cpu().numpy()
     assert np.all(xs_all[:, M:].view(np.uint16) == 0), "padding-token scales are zero"
