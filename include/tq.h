@@ -131,8 +131,9 @@ size_t tq_workspace_bytes(void);
  *   x_codes/x_scales  written by tq_quant_act for the same k (m tokens)
  *   y                 [m,n] output, fp16 or bf16 per y_dtype, row-major
  *   workspace         device buffer of tq_workspace_bytes() bytes, owned by
- *                     the caller, zero-filled before its first use.  Every
- *                     call leaves it zero-filled again.  Calls that share a
+ *                     the caller and zero-filled before its first use; every
+ *                     call leaves its counters at zero, so it stays ready
+ *                     for the next call of any layer.  Calls that share a
  *                     workspace must not run concurrently (calls on one
  *                     stream never do); give each stream its own.  At
  *                     m <= 16 the work-groups of the launch hand H from the

@@ -13,21 +13,25 @@
 //    running before any work-group that waits for them; they wait for nothing
 //    themselves.  (The wait is bounded all the same: a work-group that gives
 //    up sets an error word in the workspace instead of hanging.)
-//  * Each producer writes its fp32 H tile to the caller's workspace; the last
-//    producer to finish re-quantizes the whole of H there (per token and rank
-//    group, s_H in fp32) and publishes Q_H (fp8 operand bytes) and s_H, then
-//    raises a ready flag (copied on 32 cache lines, so that few work-groups
-//    poll any one line).
+//  * Each producer writes its fp32 H tile to the caller's workspace and then
+//    counts itself on a ready counter kept on up to 32 cache lines; column
+//    work-group c polls line c mod 32 (so that few work-groups poll any one
+//    line).
 //  * Every other work-group owns CT 16-column tiles of Y.  It forms its
-//    residual tiles, waits for the flag, reads its 32-byte Q_H operand and
-//    s_H, runs stage 2 with its L2 columns and stores Y once.
-//  * Cross-work-group data moves only through device-scope loads and stores,
-//    which bypass the per-XCD caches (no cache invalidation or write-back,
-//    which would touch every other work-group's lines); a writer waits for its
-//    stores to complete before it raises a flag.
-//  * A two-level count (32 lines, then one) finds the last work-group to
-//    finish, which clears the flags and counts, so every call leaves the
-//    workspace as it found it (zero).
+//    residual tiles, waits until every producer has counted, reads H,
+//    re-quantizes it in LDS (per token and rank group, s_H in fp32; every
+//    column work-group computes the same Q_H from the same H), runs stage 2
+//    with its L2 columns and stores Y once.
+//  * Flags and H are written with device-scope stores, which complete at the
+//    device's point of coherence; a writer waits for its stores to complete
+//    before it counts itself (no cache write-back, which would touch every
+//    other work-group's lines).  Flags are polled with device-scope loads.  H
+//    is read with ordinary loads: its lines are first touched in this launch
+//    after the count is complete and every launch starts with invalidated
+//    caches, so the column work-groups on one XCD share a fresh copy in L2.
+//  * Column work-groups also count themselves on their line once they have
+//    read H; the last one on a line clears the line's two counts, so every
+//    call leaves the workspace as it found it (zero).
 //
 // Products.  16 x 16 x 128 fp8 MFMAs over a K-group pair (codes as fp8
 // subnormals, block scales 2^9: exact integer sums); a group's own sum uses
@@ -36,9 +40,10 @@
 // the scales in k = 0.  Wavefront w of a work-group takes the group pairs
 // w, w + 8, w + 16, ... and fetches their operands from global memory straight
 // into registers, four pairs ahead: there is no LDS staging and no barrier in
-// the residual loop.  A producer stages its per-group products in LDS, 32
-// groups at a time, and four wavefronts (one for each of a lane's four
-// outputs) run the ascending-group fma chain over them.
+// the residual loop.  A producer stages the integer products of up to 64
+// groups and their fp32 scales in LDS; four wavefronts (one for each of a
+// lane's four outputs) then run the ascending-group fma chain over them,
+// forming each scale product s_x s_L1 exactly in fp32 as they go.
 #include <stdlib.h>
 
 #include "tq_device.hpp"
@@ -52,18 +57,14 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int SW = 8;      // wavefronts per work-group
 constexpr int SPD = 4;     // group pairs in flight per wavefront
-constexpr int SCG = 32;    // K-groups per producer chunk
+constexpr int SCG = 64;    // K-groups per producer chunk
 
 // Workspace layout (bytes; every counter on its own 128-byte line):
 constexpr int WS_LINE = 128;
 constexpr int WS_NL = 32;                              // flag / count copies
-constexpr int WS_PCOUNT = 0;                           // producers finished; error word at +4
-constexpr int WS_READY = WS_LINE;                      // [WS_NL] ready flags
-constexpr int WS_DONE1 = WS_READY + WS_NL * WS_LINE;   // [WS_NL] work-groups finished
-constexpr int WS_DONE2 = WS_DONE1 + WS_NL * WS_LINE;   // lines of WS_DONE1 complete
-constexpr int WS_QH = WS_DONE2 + WS_LINE;              // [16][kMaxRank] fp8 codes of Q_H
-constexpr int WS_SH = WS_QH + 16 * kMaxRank;           // [2][16] fp32 s_H
-constexpr int WS_H = WS_SH + 256;                      // [16][kMaxRank] fp32 H
+constexpr int WS_ERR = 0;                              // set when a wait gave up
+constexpr int WS_READY = WS_LINE;   // line x: producers finished (word 0), column work-groups done (word 1)
+constexpr int WS_H = WS_READY + WS_NL * WS_LINE;       // [16][kMaxRank] fp32 H
 constexpr int WS_END = WS_H + 16 * kMaxRank * 4;
 static_assert(WS_END <= (int)kWorkspaceBytes, "the workspace holds the layout");
 constexpr int kSpinLimit = 1 << 20;   // polls (~1 s at most) before giving up
@@ -80,6 +81,41 @@ __device__ __forceinline__ void st_dev(uint32_t *p, uint32_t v) {
 __device__ __forceinline__ uint32_t add_dev(uint32_t *p) {
   return __hip_atomic_fetch_add(p, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+__device__ __forceinline__ void add_dev_nr(uint32_t *p) {   // result unused: no return trip
+  (void)__hip_atomic_fetch_add(p, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// max over runs of n = 8, 16 or 32 lanes (aligned), in every lane of the run:
+// quad permutes and row mirrors (DPP) within a row of 16, the two rows of a
+// 32-lane half from scalar reads
+__device__ __forceinline__ float dpp_max(float a, int ctrl_sel) {
+  int b;
+  switch (ctrl_sel) {
+    case 0: b = __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, a), 0xB1, 0xF, 0xF, false); break;
+    case 1: b = __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, a), 0x4E, 0xF, 0xF, false); break;
+    case 2: b = __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, a), 0x141, 0xF, 0xF, false); break;
+    default: b = __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, a), 0x140, 0xF, 0xF, false); break;
+  }
+  return fmaxf(a, __builtin_bit_cast(float, b));
+}
+__device__ __forceinline__ float run_max(float a, int n, int lane) {
+  a = dpp_max(a, 0);   // lane ^ 1
+  a = dpp_max(a, 1);   // lane ^ 2
+  a = dpp_max(a, 2);   // half-row mirror: 8 lanes
+  if (n >= 16) a = dpp_max(a, 3);   // row mirror: 16 lanes
+  if (n >= 32) {
+    const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, a), 0));
+    const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, a), 16));
+    const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, a), 32));
+    const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, a), 48));
+    a = lane < 32 ? fmaxf(r0, r1) : fmaxf(r2, r3);
+  }
+  return a;
+}
+__device__ __forceinline__ v8i lds_v8i(const uint8_t *p) {
+  const u32x4 lo = *reinterpret_cast<const u32x4 *>(p);
+  const u32x4 hi = *reinterpret_cast<const u32x4 *>(p + 16);
+  return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+}
 // Release for device-scope stores: every store the other work-groups read is a
 // device-scope store, which completes at the device's point of coherence, so
 // waiting for this wavefront's stores to complete orders them before a later
@@ -90,11 +126,23 @@ __device__ __forceinline__ void wait_dev_stores() {
 
 template <int CT>
 struct SCfg {
-  // producer: [SCG groups][c, p][4 quad elements][64 lanes] fp32
-  static constexpr int P_CP = 64 * 1024;
+  // producer: integer products [4 outputs][SCG / 4][64 lanes][4 groups] fp32,
+  // then scales [16 tokens][SSTR] and [16 ranks][SSTR] fp32 (groups
+  // contiguous, so that the chain reads 4 groups per 16-byte load)
+  static constexpr int SSTR = SCG + 4;
+  static constexpr int P_C = 0;
+  static constexpr int P_SX = SCG * 1024;
+  static constexpr int P_SL = P_SX + 16 * SSTR * 4;
+  static constexpr int P_END = P_SL + 16 * SSTR * 4;
   // column work-group (aliases the producer region)
   static constexpr int RES = SW * CT * 1024;                   // [SW][CT][4][64] fp32
-  static constexpr int LDS = (P_CP > RES ? P_CP : RES) + 16;   // + a broadcast word
+  static constexpr int HSTR = kMaxRank + 1;
+  static constexpr int E_HS = RES;                             // [16][HSTR] fp32
+  static constexpr int QSTR = kMaxRank + 16;
+  static constexpr int E_QS = E_HS + 16 * HSTR * 4;            // [16][QSTR] fp8 codes
+  static constexpr int E_SH = E_QS + 16 * QSTR;                // [2][16] fp32
+  static constexpr int E_END = E_SH + 2 * 16 * 4;
+  static constexpr int LDS = P_END > E_END ? P_END : E_END;
   static_assert(LDS <= 80 * 1024, "two work-groups fit in the 160 KiB LDS of a CU");
 };
 
@@ -119,7 +167,7 @@ struct PairOps {
 };
 
 template <int CT>
-__global__ __launch_bounds__(64 * SW, 4) void dual_gemm_decode_kernel(GemmArgs a, int nprod) {
+__global__ __launch_bounds__(64 * SW, 4) void dual_gemm_decode_kernel(GemmArgs a, int nprod, int cdelay) {
   using C = SCfg<CT>;
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
   const Geometry &geo = a.geo;
@@ -143,7 +191,6 @@ __global__ __launch_bounds__(64 * SW, 4) void dual_gemm_decode_kernel(GemmArgs a
   const uint16_t *l2scales = reinterpret_cast<const uint16_t *>(a.packed + geo.off_l2s);
   const int wg = blockIdx.x;
   const bool producer = wg < nprod;
-  uint32_t *bcast = reinterpret_cast<uint32_t *>(smem + C::LDS - 16);
 
   // fetch the operands of pair p (p < NP) into o: activation fragment and NB
   // fragments of the 16-column blocks col16 + j of `blocks`, with their scales
@@ -196,55 +243,77 @@ __global__ __launch_bounds__(64 * SW, 4) void dual_gemm_decode_kernel(GemmArgs a
   if (producer) {
     // ================= H producer: 16-rank tile `wg` =================
     const int p16 = wg;
-    float *CP = reinterpret_cast<float *>(smem);
+    float *CV = reinterpret_cast<float *>(smem + C::P_C);
+    float *SXL = reinterpret_cast<float *>(smem + C::P_SX);
+    float *SLL = reinterpret_cast<float *>(smem + C::P_SL);
     const int nchunk = (KG + SCG - 1) / SCG;
+    constexpr int PPC = SCG / 2 / SW;   // pairs per wavefront and chunk (= SPD)
+    static_assert(PPC == SPD, "one chunk of pairs in flight");
     PairOps<1> F[SPD];
-    // wavefront pair sequence i -> pair SW i + wave; chunk c holds i = 2c, 2c + 1
-    const int npw = 2 * nchunk;
+    // wavefront pair sequence i -> pair SW i + wave; chunk c holds i in [SPD c, SPD c + SPD)
+    const int npw = SPD * nchunk;
 #pragma unroll
     for (int s = 0; s < SPD; s++)
-      if (s < npw && SW * s + wave < NP)
-        fetch(F[s], SW * s + wave, l1codes, l1scales, geo.r_pad32, p16, geo.r_pad32 / 16);
+      if (SW * s + wave < NP) fetch(F[s], SW * s + wave, l1codes, l1scales, geo.r_pad32, p16, geo.r_pad32 / 16);
     float hacc = 0.0f;
     for (int c = 0; c < nchunk; c++) {
 #pragma unroll
-      for (int h = 0; h < 2; h++) {
-        const int i = 2 * c + h;
+      for (int s = 0; s < SPD; s++) {
+        const int i = SPD * c + s;
         const int p = SW * i + wave;
+        if (p < NP) {
+          const PairOps<1> &o = F[s];
+          const v8i av = unpack32(o.x);
+          const v8i z = {0, 0, 0, 0, 0, 0, 0, 0};
+          const v8i b = unpack32(o.b[0]);
+          const v4f m1 = mfma_codes_16x16x128(q < 2 ? av : z, b);
+          const v4f m2 = mfma_codes_16x16x128(q < 2 ? z : av, b);
+          const int gl1 = 2 * p - SCG * c, gl2 = gl1 + 1;
+          auto cidx = [&](int v, int gl) { return ((v * (SCG / 4) + gl / 4) * 64 + lane) * 4 + gl % 4; };
 #pragma unroll
-        for (int s = 0; s < SPD; s++) {
-          if ((i % SPD) != s) continue;
-          if (p < NP) {
-            products(F[s], p, [&](int, int g, const v4f &cv, const v4f &pv) {
-              const int gl = g - SCG * c;
+          for (int v = 0; v < 4; v++) CV[cidx(v, gl1)] = m1[v];
+          if (2 * p + 1 < KG) {
 #pragma unroll
-              for (int v = 0; v < 4; v++) {
-                CP[((gl * 2 + 0) * 4 + v) * 64 + lane] = cv[v];
-                CP[((gl * 2 + 1) * 4 + v) * 64 + lane] = pv[v];
-              }
-            });
+            for (int v = 0; v < 4; v++) CV[cidx(v, gl2)] = m2[v];
           }
-          const int pn = SW * (i + SPD) + wave;
-          if (i + SPD < npw && pn < NP)
-            fetch(F[s], pn, l1codes, l1scales, geo.r_pad32, p16, geo.r_pad32 / 16);
+          if (lane < 16) {
+            SXL[c16 * C::SSTR + gl1] = half_bits_to_float((uint16_t)o.sx1);
+            SXL[c16 * C::SSTR + gl2] = half_bits_to_float((uint16_t)o.sx2);
+            SLL[c16 * C::SSTR + gl1] = half_bits_to_float((uint16_t)o.sb1[0]);
+            SLL[c16 * C::SSTR + gl2] = half_bits_to_float((uint16_t)o.sb2[0]);
+          }
         }
+        const int pn = SW * (i + SPD) + wave;
+        if (i + SPD < npw && pn < NP)
+          fetch(F[s], pn, l1codes, l1scales, geo.r_pad32, p16, geo.r_pad32 / 16);
       }
-      __syncthreads();   // the chunk's products are in LDS
+      __syncthreads();   // the chunk's products and scales are in LDS
       if (wave < 4) {
-        // element v = wave of every lane's output quad, groups in ascending
-        // order; the reads of 8 groups are issued before their fmas
+        // output v = wave of every lane (token 4q + v, rank 16 p16 + c16),
+        // groups in ascending order, in batches of 8 whose reads (six
+        // 16-byte loads) go before their fmas
+        const int row = 4 * q + wave;
         const int ng = min(SCG, KG - SCG * c);
-        for (int g0 = 0; g0 < ng; g0 += 8) {
-          float cv[8], pv[8];
+        const float4 *CV4 = reinterpret_cast<const float4 *>(CV) + (wave * (SCG / 4)) * 64 + lane;
+        const float4 *SX4 = reinterpret_cast<const float4 *>(SXL + row * C::SSTR);
+        const float4 *SL4 = reinterpret_cast<const float4 *>(SLL + c16 * C::SSTR);
+        int g0 = 0;
+        for (; g0 + 8 <= ng; g0 += 8) {
+          float4 cv[2], sv[2], lv[2];
 #pragma unroll
-          for (int e = 0; e < 8; e++) {
-            const int gl = min(g0 + e, SCG - 1);
-            cv[e] = CP[((gl * 2 + 0) * 4 + wave) * 64 + lane];
-            pv[e] = CP[((gl * 2 + 1) * 4 + wave) * 64 + lane];
+          for (int e = 0; e < 2; e++) {
+            cv[e] = CV4[(g0 / 4 + e) * 64];
+            sv[e] = SX4[g0 / 4 + e];
+            lv[e] = SL4[g0 / 4 + e];
           }
 #pragma unroll
-          for (int e = 0; e < 8; e++)
-            if (g0 + e < ng) hacc = fmaf(cv[e], pv[e], hacc);
+          for (int e = 0; e < 8; e++)   // s_x s_L1 is exact in fp32
+            hacc = fmaf(cv[e / 4][e % 4], sv[e / 4][e % 4] * lv[e / 4][e % 4], hacc);
+        }
+        for (; g0 < ng; g0++) {
+          const int gl = g0;
+          hacc = fmaf(CV[((wave * (SCG / 4) + gl / 4) * 64 + lane) * 4 + gl % 4],
+                      SXL[row * C::SSTR + gl] * SLL[c16 * C::SSTR + gl], hacc);
         }
       }
       __syncthreads();   // the chunk's products are consumed
@@ -257,67 +326,12 @@ __global__ __launch_bounds__(64 * SW, 4) void dual_gemm_decode_kernel(GemmArgs a
                          __HIP_MEMORY_SCOPE_AGENT);
     wait_dev_stores();
     __syncthreads();
-    if (tid == 0) bcast[0] = add_dev(ws_word(ws, WS_PCOUNT));
-    __syncthreads();
-    if (bcast[0] == (uint32_t)(nprod - 1)) {
-      // ---- the last producer: re-quantize H per token and rank group ----
-      const int gr = geo.gr, rg = r / gr;
-      const int subs = gr / 8;                // lanes per (token, rank group): 1, 2, 4 or 8
-      const int work = 16 * rg * subs;        // <= 256
-      const bool valid = tid < work;
-      const int pair = tid / subs, sub = tid % subs;
-      const int row = pair / rg, hg = pair % rg;
-      const int j0 = hg * gr + sub * 8;
-      float hv[8];
-      float amax = 0.0f;
-#pragma unroll
-      for (int e = 0; e < 8; e++) {
-        hv[e] = valid ? __hip_atomic_load(wsH + row * kMaxRank + j0 + e, __ATOMIC_RELAXED,
-                                          __HIP_MEMORY_SCOPE_AGENT)
-                      : 0.0f;
-        amax = fmaxf(amax, fabsf(hv[e]));
-      }
-      for (int msk = 1; msk < subs; msk <<= 1) amax = fmaxf(amax, __shfl_xor(amax, msk));
-      const float sh = amax / 7.0f;   // IEEE division
-      const bool dbg = a.dbg_h != nullptr;
-      if (valid) {
-        uint32_t w0 = 0, w1 = 0;
-#pragma unroll
-        for (int e = 0; e < 8; e++) {
-          int qv = 0;
-          if (sh != 0.0f) {
-            float tq = __builtin_rintf(hv[e] / sh);
-            tq = tq > 7.0f ? 7.0f : (tq < -7.0f ? -7.0f : tq);
-            qv = (int)tq;
-          }
-          const uint32_t bq = code_to_fp8(qv);
-          if (e < 4) w0 |= bq << (8 * e); else w1 |= bq << (8 * (e - 4));
-          if (dbg && row < m) {
-            a.dbg_h[(int64_t)row * r + j0 + e] = hv[e];
-            a.dbg_qh[(int64_t)row * r + j0 + e] = (int8_t)qv;
-          }
-        }
-        st_dev(ws_word(ws, WS_QH + row * kMaxRank + j0), w0);
-        st_dev(ws_word(ws, WS_QH + row * kMaxRank + j0 + 4), w1);
-        if (sub == 0) {
-          __hip_atomic_store(reinterpret_cast<float *>(wsb + WS_SH) + hg * 16 + row, sh,
-                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          if (dbg && row < m) a.dbg_sh[(int64_t)row * rg + hg] = sh;
-        }
-      }
-      // ranks r .. 64 RB - 1 of Q_H are zero operand bytes
-      for (int idx = tid; idx < 16 * RB * 16; idx += 64 * SW) {
-        const int row2 = idx / (RB * 16), w4 = idx % (RB * 16);
-        if (4 * w4 >= r) st_dev(ws_word(ws, WS_QH + row2 * kMaxRank + 4 * w4), 0u);
-      }
-      wait_dev_stores();
-      __syncthreads();
-      if (tid < WS_NL) st_dev(ws_word(ws, WS_READY + tid * WS_LINE), 1u);
-      if (tid == 0) st_dev(ws_word(ws, WS_PCOUNT), 0u);   // every producer has counted
-    }
+    const int ncol = (int)gridDim.x - nprod;
+    if (tid < WS_NL && tid < ncol) add_dev_nr(ws_word(ws, WS_READY + tid * WS_LINE));
   } else {
     // ================= column work-group =================
     const int c0 = (wg - nprod) * CT;   // first 16-column tile
+    for (int d = 0; d < cdelay; d++) __builtin_amdgcn_s_sleep(16);
     // stage-2 operands (wavefront j < CT, tile c0 + j), fetched before the
     // residual loop: rank blocks in pairs, lanes q < 2 carry block 0, lanes
     // q >= 2 block 1
@@ -365,6 +379,97 @@ __global__ __launch_bounds__(64 * SW, 4) void dual_gemm_decode_kernel(GemmArgs a
       for (int v = 0; v < 4; v++) RES[((wave * CT + j) * 4 + v) * 64 + lane] = acc[j][v];
     __syncthreads();
 
+    float *HS = reinterpret_cast<float *>(smem + C::E_HS);
+    uint8_t *QS = smem + C::E_QS;
+    float *SHS = reinterpret_cast<float *>(smem + C::E_SH);
+    if (nprod > 0) {
+      // ---- wait for every producer's H tile ----
+      if (wave == 0) {
+        const uint32_t *cnt = ws_word(ws, WS_READY + ((wg - nprod) % WS_NL) * WS_LINE);
+        int spins = 0;
+        while (ld_dev(cnt) < (uint32_t)nprod) {
+          __builtin_amdgcn_s_sleep(2);
+          if (++spins > kSpinLimit) {
+            st_dev(ws_word(ws, WS_ERR), 1u);
+            break;
+          }
+        }
+      }
+      __syncthreads();
+      // all of a thread's loads are issued before any is used
+      const float *wsH = reinterpret_cast<const float *>(wsb + WS_H);
+      const int rp = 16 * nprod;
+      constexpr int HPT = 16 * kMaxRank / (64 * SW);   // H values per thread at most
+      float hl[HPT];
+#pragma unroll
+      for (int e = 0; e < HPT; e++) {
+        const int idx = tid + 64 * SW * e;
+        const int row = idx / rp, j = idx % rp;
+        hl[e] = idx < 16 * rp && row < m ? wsH[row * kMaxRank + j] : 0.0f;
+      }
+#pragma unroll
+      for (int e = 0; e < HPT; e++) {
+        const int idx = tid + 64 * SW * e;
+        if (idx < 16 * rp) HS[(idx / rp) * C::HSTR + idx % rp] = hl[e];
+      }
+      for (int idx = tid; idx < 16 * RB * 64; idx += 64 * SW) {
+        const int row = idx / (RB * 64), j = idx % (RB * 64);
+        if (j >= r) QS[row * C::QSTR + j] = 0;
+      }
+      __syncthreads();
+
+      // ---- re-quantize H per token and rank group (s_H stays fp32) ----
+      // Half a wavefront per token row (wavefront w: rows 2w, 2w + 1); lane j
+      // of the half takes ranks epl j .. epl j + epl - 1, so a rank group is a
+      // run of gr / epl lanes and its max is a shuffle reduction over them.
+      {
+        const int gr = geo.gr, rg = r / gr;
+        const int epl = r >= 32 ? r / 32 : 1;      // ranks per lane: 1, 2 or 4
+        const int row = 2 * wave + (lane >> 5), j = lane & 31;
+        const int lpg = gr / epl;                  // lanes per rank group (<= 32)
+        const int hg = j / lpg;
+        const bool valid = j * epl < r;
+        const bool dbg = a.dbg_h != nullptr && wg == nprod;
+        float hv[4];
+        float amax = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 4; e++) {
+          hv[e] = valid && e < epl ? HS[row * C::HSTR + j * epl + e] : 0.0f;
+          amax = fmaxf(amax, fabsf(hv[e]));
+        }
+        amax = run_max(amax, lpg, lane);
+        const float sh = amax / 7.0f;   // IEEE division
+        if (valid) {
+          uint32_t w = 0;
+#pragma unroll
+          for (int e = 0; e < 4; e++) {
+            if (e < epl) {
+              int qv = 0;
+              if (sh != 0.0f) {
+                float tq = __builtin_rintf(hv[e] / sh);
+                tq = tq > 7.0f ? 7.0f : (tq < -7.0f ? -7.0f : tq);
+                qv = (int)tq;
+              }
+              w |= code_to_fp8(qv) << (8 * e);
+              if (dbg && row < m) {
+                a.dbg_h[(int64_t)row * r + j * epl + e] = hv[e];
+                a.dbg_qh[(int64_t)row * r + j * epl + e] = (int8_t)qv;
+              }
+            }
+          }
+          uint8_t *qd = QS + row * C::QSTR + j * epl;
+          if (epl == 4) *reinterpret_cast<uint32_t *>(qd) = w;
+          else if (epl == 2) *reinterpret_cast<uint16_t *>(qd) = (uint16_t)w;
+          else *qd = (uint8_t)w;
+          if (j % lpg == 0) {
+            SHS[hg * 16 + row] = sh;
+            if (dbg && row < m) a.dbg_sh[(int64_t)row * rg + hg] = sh;
+          }
+        }
+      }
+      __syncthreads();
+    }
+
     // ---- stage 2 and the single epilogue: wavefront j < CT stores tile j ----
     if (wave < CT) {
       const int j = wave;
@@ -373,27 +478,13 @@ __global__ __launch_bounds__(64 * SW, 4) void dual_gemm_decode_kernel(GemmArgs a
         v4f ylr = v4f{0, 0, 0, 0};
         const int orow0 = 4 * q;   // output rows 4q .. 4q + 3 of this lane
         if (nprod > 0) {
-          // Q_H: wait for the flag (this work-group's copy), then read it
-          const uint32_t *flag = ws_word(ws, WS_READY + (wg % WS_NL) * WS_LINE);
-          int spins = 0;
-          while (ld_dev(flag) == 0u) {
-            __builtin_amdgcn_s_sleep(2);
-            if (++spins > kSpinLimit) {
-              st_dev(ws_word(ws, WS_PCOUNT + 4), 1u);
-              break;
-            }
-          }
           const int rbq = min(q >> 1, RB - 1);
-          const uint32_t *qp = ws_word(ws, WS_QH + c16 * kMaxRank + rbq * 64 + (q & 1) * 32);
-          v8i qa;
-#pragma unroll
-          for (int e = 0; e < 8; e++) qa[e] = (int)ld_dev(qp + e);
-          const uint32_t *shp = ws_word(ws, WS_SH + orow0 * 4);
+          const v8i qa = lds_v8i(QS + c16 * C::QSTR + rbq * 64 + (q & 1) * 32);
           float sh0[4], sh1[4];
 #pragma unroll
           for (int v = 0; v < 4; v++) {
-            sh0[v] = __builtin_bit_cast(float, ld_dev(shp + v));
-            sh1[v] = RB > 1 ? __builtin_bit_cast(float, ld_dev(shp + 16 + v)) : 0.0f;
+            sh0[v] = SHS[orow0 + v];
+            sh1[v] = RB > 1 ? SHS[16 + orow0 + v] : 0.0f;
           }
           const v8i lb = unpack32(l2raw);
           const v8i zero = {0, 0, 0, 0, 0, 0, 0, 0};
@@ -431,20 +522,15 @@ __global__ __launch_bounds__(64 * SW, 4) void dual_gemm_decode_kernel(GemmArgs a
     }
   }
 
-  // ---- the last work-group to finish clears the flags and counts ----
-  if (nprod > 0) {
-    __syncthreads();
+  // ---- the last column work-group of a line clears the line ----
+  if (nprod > 0 && !producer) {
+    __syncthreads();   // every read of the line and of H is done
     if (tid == 0) {
-      const int x = wg % WS_NL;
-      const uint32_t per = (uint32_t)((gridDim.x - x + WS_NL - 1) / WS_NL);   // work-groups on line x
-      const uint32_t lines = gridDim.x < (uint32_t)WS_NL ? gridDim.x : (uint32_t)WS_NL;
-      if (add_dev(ws_word(ws, WS_DONE1 + x * WS_LINE)) == per - 1 &&
-          add_dev(ws_word(ws, WS_DONE2)) == lines - 1) {
-        for (int l = 0; l < WS_NL; l++) {
-          st_dev(ws_word(ws, WS_READY + l * WS_LINE), 0u);
-          st_dev(ws_word(ws, WS_DONE1 + l * WS_LINE), 0u);
-        }
-        st_dev(ws_word(ws, WS_DONE2), 0u);
+      const int x = (wg - nprod) % WS_NL, ncol = (int)gridDim.x - nprod;
+      const uint32_t per = (uint32_t)((ncol - x + WS_NL - 1) / WS_NL);   // column work-groups on line x
+      if (add_dev(ws_word(ws, WS_READY + x * WS_LINE + 4)) == per - 1) {
+        st_dev(ws_word(ws, WS_READY + x * WS_LINE), 0u);
+        st_dev(ws_word(ws, WS_READY + x * WS_LINE + 4), 0u);
       }
     }
   }
@@ -460,7 +546,9 @@ hipError_t launch_decode(const GemmArgs &a, hipStream_t s) {
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, dim3(nprod + ncol), dim3(64 * SW), C::LDS, s, a, nprod);
+  int cdelay = 0;
+  if (const char *env = getenv("TQ_DECODE_DELAY")) cdelay = atoi(env);
+  hipLaunchKernelGGL(kern, dim3(nprod + ncol), dim3(64 * SW), C::LDS, s, a, nprod, nprod > 0 ? cdelay : 0);
   return hipGetLastError();
 }
 
