@@ -167,7 +167,7 @@ struct PairOps {
 };
 
 template <int CT>
-__global__ __launch_bounds__(64 * SW, 4) void dual_gemm_decode_kernel(GemmArgs a, int nprod, int cdelay) {
+__global__ __launch_bounds__(64 * SW, 4) void dual_gemm_decode_kernel(GemmArgs a, int nprod) {
   using C = SCfg<CT>;
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
   const Geometry &geo = a.geo;
@@ -331,7 +331,6 @@ __global__ __launch_bounds__(64 * SW, 4) void dual_gemm_decode_kernel(GemmArgs a
   } else {
     // ================= column work-group =================
     const int c0 = (wg - nprod) * CT;   // first 16-column tile
-    for (int d = 0; d < cdelay; d++) __builtin_amdgcn_s_sleep(16);
     // stage-2 operands (wavefront j < CT, tile c0 + j), fetched before the
     // residual loop: rank blocks in pairs, lanes q < 2 carry block 0, lanes
     // q >= 2 block 1
@@ -546,9 +545,7 @@ hipError_t launch_decode(const GemmArgs &a, hipStream_t s) {
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
   if (e != hipSuccess) return e;
-  int cdelay = 0;
-  if (const char *env = getenv("TQ_DECODE_DELAY")) cdelay = atoi(env);
-  hipLaunchKernelGGL(kern, dim3(nprod + ncol), dim3(64 * SW), C::LDS, s, a, nprod, nprod > 0 ? cdelay : 0);
+  hipLaunchKernelGGL(kern, dim3(nprod + ncol), dim3(64 * SW), C::LDS, s, a, nprod);
   return hipGetLastError();
 }
 

@@ -547,9 +547,14 @@ hipError_t launch_mid_rt(const GemmArgs &a, hipStream_t s) {
 // tile-groups it owns (H and residual), so the cost of a choice of CT is the
 // number of rounds of work-groups over the 256 CUs times the tile-groups per
 // work-group and chunk.
+// Relative time of a launch with CT column tiles per work-group: rounds of
+// work-groups over the 256 CUs x (per-chunk tile-groups of a work-group plus
+// a fixed latency worth about three tile-groups per chunk, measured at
+// K = N = 4096: 9.5 / 14.5 / 18 us per round for r = 0 and CT = 1 / 2 / 4,
+// 16 / 18.5 / 22 us for r = 64).
 int mid_cost(int rt, int ct, int n_rb, int ct32) {
   const int n_wg = n_rb * ((ct32 + ct - 1) / ct);
-  return (n_wg + 255) / 256 * MCG * (rt + ct);
+  return (n_wg + 255) / 256 * (3 + rt + ct);
 }
 
 }  // namespace
