@@ -103,15 +103,21 @@ tq_status tq_pack_weights(const tq_weight_desc *d, const void *w_res, const void
  * activation is quantized once and shared by both branches).
  *   x         [m,k] fp16 row-major, 0 <= m <= 2097120 (65535 tiles of 32),
  *             k % group == 0, group == 64
- *   x_codes   m32 * k / 2 bytes, m32 = m rounded up to a multiple of 32:
- *             tile-major TQ4 codes.  The tokens are cut into tiles of 32 and
- *             K into groups of 64; tile t, group g is one 1 KiB block at byte
- *             (t * (k / 64) + g) * 1024, whose 16-byte lane slot 32 h + i
- *             (h = 0, 1; i = 0 .. 31) holds the four TQ4 words of codes
- *             32 h .. 32 h + 31 of the group for token 32 t + i (the order in
- *             which the matrix cores take one operand of a 32 x 32 x 64
- *             product, so each block is one coalesced load).  Tokens
- *             [m, m32) get zero codes.
+ *   x_codes   tq_act_codes_bytes(m, k) bytes, tile-major.  The tokens are
+ *             cut into tiles of 32 (m32 = m rounded up to a multiple of 32)
+ *             and K into groups of 64.  For m <= 512 each code is a TQ4
+ *             nibble (m32 * k / 2 bytes): tile t, group g is one 1 KiB block
+ *             at byte (t * (k / 64) + g) * 1024, whose 16-byte lane slot
+ *             32 h + i (h = 0, 1; i = 0 .. 31) holds the four TQ4 words of
+ *             codes 32 h .. 32 h + 31 of the group for token 32 t + i (the
+ *             order in which the matrix cores take one operand of a
+ *             32 x 32 x 64 product, so each block is one coalesced load).
+ *             For m > 512 each code is its fp8 e4m3 operand byte,
+ *             sign << 7 | |q| (m32 * k bytes): tile t, group g is a 2 KiB
+ *             block at byte (t * (k / 64) + g) * 2048 made of two 1 KiB
+ *             halves p = 0, 1; lane slot 32 h + i of half p holds the bytes
+ *             of codes 32 h + 16 p .. 32 h + 16 p + 15 of the group for token
+ *             32 t + i.  Tokens [m, m32) get zero codes.
  *   x_scales  [k/group, m32] fp16: the scale of token i, group g is
  *             x_scales[g*m32 + i] (group-major, so one group's scales of a
  *             token tile are contiguous); entries i in [m, m32) are 0
@@ -120,8 +126,12 @@ tq_status tq_pack_weights(const tq_weight_desc *d, const void *w_res, const void
 tq_status tq_quant_act(const void *x, int m, int k, int group, void *x_codes,
                        void *x_scales, void *stream);
 
+/* Size in bytes of the x_codes buffer of m tokens with reduction size k
+ * (0 if m or k is out of range or k % 64 != 0).  Host-only. */
+size_t tq_act_codes_bytes(int m, int k);
+
 /* Size in bytes of the workspace that tq_dual_gemm takes (a constant of the
- * library build; currently 8448). */
+ * library build; currently 20480). */
 size_t tq_workspace_bytes(void);
 
 /* The fused dual-component layer: residual 4-bit GEMM, low-rank stage 1

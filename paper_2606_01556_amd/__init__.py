@@ -38,7 +38,8 @@ class WeightDesc(ctypes.Structure):
 
 
 EXPORTS = ("tq_weight_desc_init", "tq_pack_weights", "tq_quant_act", "tq_dual_gemm",
-           "tq_dual_gemm_debug", "tq_export_weights", "tq_workspace_bytes", "tq_status_string")
+           "tq_dual_gemm_debug", "tq_export_weights", "tq_workspace_bytes", "tq_act_codes_bytes",
+           "tq_status_string")
 
 _lib = None
 
@@ -60,11 +61,13 @@ def lib() -> ctypes.CDLL:
         L.tq_dual_gemm_debug.argtypes = [D, P, P, P, I, P, I, P, P, P, P, P]
         L.tq_workspace_bytes.argtypes = []
         L.tq_workspace_bytes.restype = ctypes.c_size_t
+        L.tq_act_codes_bytes.argtypes = [I, I]
+        L.tq_act_codes_bytes.restype = ctypes.c_size_t
         L.tq_export_weights.argtypes = [D, P, P, P, P, P, P, P, P]
         L.tq_status_string.argtypes = [I]
         L.tq_status_string.restype = ctypes.c_char_p
         for name in EXPORTS:
-            if name not in ("tq_workspace_bytes", "tq_status_string"):
+            if name not in ("tq_workspace_bytes", "tq_act_codes_bytes", "tq_status_string"):
                 getattr(L, name).restype = I
         _lib = L
     return _lib
@@ -153,13 +156,23 @@ def padded_tokens(m: int) -> int:
     return max((m + 31) // 32 * 32, 32)
 
 
+def act_codes_bytes(m: int, k: int) -> int:
+    """Bytes of the x_codes buffer of m tokens (tq_act_codes_bytes)."""
+    return int(lib().tq_act_codes_bytes(m, k))
+
+
 def empty_act(m: int, k: int, device="cuda"):
     """(x_codes, x_scales) buffers for tq_quant_act / tq_dual_gemm:
-    x_codes [m32/32, k/64, 256] int32 (one 1 KiB tile-major block per 32
-    tokens and K-group), x_scales [k/64, m32] fp16, m32 = padded_tokens(m)."""
+    x_codes [m32/32, k/64, W] int32, one tile-major block per 32 tokens and
+    K-group (W = 256: 1 KiB of TQ4 nibbles for m <= 512; W = 512: 2 KiB of fp8
+    operand bytes for larger m), x_scales [k/64, m32] fp16, m32 =
+    padded_tokens(m)."""
     import torch
     m32 = padded_tokens(m)
-    return (torch.empty((m32 // 32, k // GROUP, 256), dtype=torch.int32, device=device),
+    nbytes = act_codes_bytes(max(m, 1), k)
+    words = nbytes // (m32 // 32 * (k // GROUP) * 4)
+    assert words in (256, 512), (m, k, nbytes)
+    return (torch.empty((m32 // 32, k // GROUP, words), dtype=torch.int32, device=device),
             torch.empty((k // GROUP, m32), dtype=torch.float16, device=device))
 
 
@@ -219,11 +232,25 @@ def tq4_encode(codes) -> np.ndarray:
     return w
 
 
+def fp8_code_decode(b) -> np.ndarray:
+    """fp8 operand bytes sign << 7 | |q| (uint8 array) -> int8 codes (host side)."""
+    b = np.ascontiguousarray(b).view(np.uint8)
+    mag = (b & 0x7F).astype(np.int16)
+    assert np.all(mag <= 7), "not a code byte"
+    return np.where(b >> 7 == 1, -mag, mag).astype(np.int8)
+
+
 def act_codes_rows(x_codes, m: int) -> np.ndarray:
-    """Tile-major activation codes (host copy of x_codes) -> int8 codes [m, k]
-    (host side, for inspection and tests)."""
+    """Tile-major activation codes (host copy of x_codes [tiles, k/64, W]
+    int32, TQ4 blocks for W = 256 and fp8 blocks for W = 512) -> int8 codes
+    [m, k] (host side, for inspection and tests)."""
     w = np.ascontiguousarray(x_codes).view(np.uint32)
-    tiles, kg = w.shape[0], w.shape[1]
-    w = w.reshape(tiles, kg, 2, 32, 4)            # tile, group, half, token, word
-    w = w.transpose(0, 3, 1, 2, 4)                 # tile, token, group, half, word
-    return tq4_decode(w.reshape(tiles * 32, kg * 8))[:m]
+    tiles, kg, words = w.shape[0], w.shape[1], w.shape[2]
+    if words == 256:
+        w = w.reshape(tiles, kg, 2, 32, 4)            # tile, group, half, token, word
+        w = w.transpose(0, 3, 1, 2, 4)                 # tile, token, group, half, word
+        return tq4_decode(w.reshape(tiles * 32, kg * 8))[:m]
+    assert words == 512, words
+    b = w.view(np.uint8).reshape(tiles, kg, 2, 2, 32, 16)   # tile, group, part, half, token, byte
+    b = b.transpose(0, 4, 1, 3, 2, 5)                        # tile, token, group, half, part, byte
+    return fp8_code_decode(b.reshape(tiles * 32, kg * 64))[:m]

@@ -125,6 +125,11 @@ static tq_status dual_gemm_impl(const tq_weight_desc *d, const void *packed, con
 
 size_t tq_workspace_bytes(void) { return tq::kWorkspaceBytes; }
 
+size_t tq_act_codes_bytes(int m, int k) {
+  if (m < 0 || m > 65535 * 32 || k < 1 || k > (1 << 24) || k % 64 != 0) return 0;
+  return tq::act_codes_bytes(m, k);
+}
+
 tq_status tq_dual_gemm(const tq_weight_desc *d, const void *packed, const void *x_codes,
                        const void *x_scales, int m, void *y, tq_dtype y_dtype, void *workspace,
                        void *stream) {

@@ -11,10 +11,9 @@
 namespace tq {
 
 hipError_t launch_dual_gemm(const GemmArgs &a, hipStream_t s) {
-  const char *env = getenv("TQ_MID_MAX");   // crossover overrides for tuning sweeps
-  const int mid_max = env ? atoi(env) : 512;
+  // the activation code format follows the same token-count split
   if (a.m <= 16) return launch_dual_gemm_decode(a, s);
-  if (a.m <= mid_max) return launch_dual_gemm_mid(a, s);
+  if (!act_codes_fp8(a.m)) return launch_dual_gemm_mid(a, s);
   // 128 x 256 blocks: while they fit in one round over the 256 CUs the large
   // kernel (16 wavefronts, H formed in the main loop) is faster; beyond, the
   // prefill kernel forms H once per run of column blocks

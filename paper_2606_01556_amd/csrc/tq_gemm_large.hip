@@ -4,26 +4,32 @@
 // kernel.
 //
 // Work decomposition.  A work-group of 16 wavefronts (four per SIMD) owns a
-// block of 128 tokens x 256 columns.  Wavefront w = 4 ti + cp computes the
-// two 32 x 32 output tiles of token tile ti and column pair cp; the 4 x RT
-// tiles of H (RT = r / 32 rounded up) are spread over the wavefronts so that
-// every SIMD forms the same number, in the same K loop.  Each tile walks the K-groups in ascending order with one
-// fma per group, the oracle's order, so H, Q_H and Y are bit-identical to it.
-// Four wavefronts per SIMD with one tile in flight each hide the latency of
-// the matrix-core results better than fewer wavefronts with more tiles.
+// block of 128 tokens x 256 columns.  Wavefront w = 8 tp + cc computes the
+// two 32 x 32 output tiles of token tiles 2 tp and 2 tp + 1 and column tile
+// cc, so it expands one weight operand per group and reads its two activation
+// operands ready-made: at these token counts the activation codes arrive as
+// fp8 operand bytes, and the kernel is bound by vector-ALU work (4-bit
+// expansion and the per-group rescaling fmas).  The 4 x RT tiles of H
+// (RT = r / 32 rounded up) are spread over the wavefronts so that every SIMD
+// forms the same number, in the same K loop.  Each tile walks the K-groups in
+// ascending order with one fma per group, the oracle's order, so H, Q_H and Y
+// are bit-identical to it.  Four wavefronts per SIMD with one tile in flight
+// each hide the latency of the matrix-core results better than fewer
+// wavefronts with more tiles.
 //
 // Per tile and group (Eq. 2): v_mfma_scale_f32_32x32x64_f8f6f4 returns half
 // of the exact integer group sum (codes as fp8 subnormals), v_mfma_f32_32x32x8
 // f16 twice the exact scale product, and one fma per element applies their
 // product, exactly I * s_x * s_w.
 //
-// Data movement: everything a K-group needs -- 4 activation tiles, 8 weight
-// tiles, RT L1 tiles and all their scales -- arrives by direct global -> LDS
-// loads (global_load_lds_dwordx4) into a D-slot ring, D - 1 groups ahead, one
-// 1 KiB wave load per wavefront and group (two for two wavefronts when
-// r = 128), so every wait is one constant s_waitcnt.  One work-group barrier
-// per group.  The stage-2 operands (L2 blocks and scales of the 8 column
-// tiles) are loaded at the start into a region of their own.
+// Data movement: everything a K-group needs -- 4 activation tiles (2 KiB
+// each), 8 weight tiles, RT L1 tiles and all their scales -- arrives by direct
+// global -> LDS loads (global_load_lds_dwordx4) into a D-slot ring, one 1 KiB
+// wave load per wavefront and group (two for the first 2 + RT wavefronts), so
+// every wait is one constant s_waitcnt.  A step consumes two K-groups behind
+// one work-group barrier and refills their slots D groups ahead.  The stage-2
+// operands (L2 blocks and scales of the 8 column tiles) are loaded at the
+// start into a region of their own.
 #include <stdlib.h>
 
 #include <type_traits>
@@ -46,13 +52,13 @@ template <int RT>
 struct LCfg {
   static constexpr int RB = (RT + 1) / 2;              // 64-rank blocks (= rank groups)
   // one ring slot (one K-group)
-  static constexpr int S_A = 0;                        // 4 activation tiles
-  static constexpr int S_B = 4096;                     // 8 weight tiles
-  static constexpr int S_L = 12288;                    // RT L1 tiles
+  static constexpr int S_A = 0;                        // 4 activation tiles x 2 halves
+  static constexpr int S_B = 8192;                     // 8 weight tiles
+  static constexpr int S_L = 16384;                    // RT L1 tiles
   static constexpr int S_SX = S_L + RT * 1024;         // activation scales (256 B used)
   static constexpr int S_SW = S_SX + 1024;             // weight scales 512 B, then L1 64 RT B
   static constexpr int SLOT = S_SW + 1024;
-  static constexpr int NI = 14 + RT;                   // wave loads per group
+  static constexpr int NI = 18 + RT;                   // wave loads per group
   // stage-2 operands: 8 x RB L2 blocks, then their scales
   static constexpr int L2B = RT > 0 ? 8 * RB * 1024 + 1024 : 0;
   static constexpr int DFIT = (L_LDS - L2B) / SLOT;
@@ -69,7 +75,7 @@ struct LCfg {
   static_assert(LDS <= L_LDS, "fits the 160 KiB LDS of a CU");
   static_assert(E_END <= D * SLOT, "the epilogue fits in the ring");
   static_assert(NI <= 2 * LW, "at most two wave loads per wavefront and group");
-  static_assert(D >= 3, "at least two groups in flight");
+  static_assert(D >= 4, "two groups consumed per step, two more in flight");
 };
 
 template <int N>
@@ -96,6 +102,13 @@ __device__ __forceinline__ const uint8_t *l_uniform(const uint8_t *p) {
   const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
   const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
   return reinterpret_cast<const uint8_t *>(((uint64_t)hi << 32) | lo);
+}
+
+// one fp8 activation operand: the lane's two 16-byte halves, 1 KiB apart
+__device__ __forceinline__ v8i l_v8h(const uint8_t *p) {
+  const u32x4 lo = *reinterpret_cast<const u32x4 *>(p);
+  const u32x4 hi = *reinterpret_cast<const u32x4 *>(p + 1024);
+  return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
 }
 
 __device__ __forceinline__ v8i l_v8i(const uint8_t *p) {
@@ -134,24 +147,24 @@ __device__ __forceinline__ LItem l_item(const GemmArgs &a, int it, int lane, int
   const Geometry &geo = a.geo;
   const int KG = geo.k / kGroup;
   LItem d;
-  if (it < 4) {                       // activation tile it
-    const int t = min(m0 / 32 + it, a.ms / 32 - 1);
-    d.base = reinterpret_cast<const uint8_t *>(a.xc) + (int64_t)t * KG * 1024;
+  if (it < 8) {                       // activation tile it / 2, half it % 2 (fp8 bytes)
+    const int t = min(m0 / 32 + it / 2, a.ms / 32 - 1);
+    d.base = reinterpret_cast<const uint8_t *>(a.xc) + (int64_t)t * KG * 2048 + (it & 1) * 1024;
     d.off = lane * 16;
-    d.stride = 1024;
+    d.stride = 2048;
     d.dst = C::S_A + it * 1024;
-  } else if (it < 12) {               // weight tile it - 4
-    const int ct = min(n0 / 32 + it - 4, geo.n_pad / 32 - 1);
+  } else if (it < 16) {               // weight tile it - 8
+    const int ct = min(n0 / 32 + it - 8, geo.n_pad / 32 - 1);
     d.base = a.packed + geo.off_w + (int64_t)ct * KG * 1024;
     d.off = lane * 16;
     d.stride = 1024;
-    d.dst = C::S_B + (it - 4) * 1024;
-  } else if (it < 12 + RT) {          // L1 rank tile it - 12
-    d.base = a.packed + geo.off_l1 + (int64_t)(it - 12) * KG * 1024;
+    d.dst = C::S_B + (it - 8) * 1024;
+  } else if (it < 16 + RT) {          // L1 rank tile it - 16
+    d.base = a.packed + geo.off_l1 + (int64_t)(it - 16) * KG * 1024;
     d.off = lane * 16;
     d.stride = 1024;
-    d.dst = C::S_L + (it - 12) * 1024;
-  } else if (it == 12 + RT) {         // activation scales of the 128 tokens: lanes 0-15
+    d.dst = C::S_L + (it - 16) * 1024;
+  } else if (it == 16 + RT) {         // activation scales of the 128 tokens: lanes 0-15
     const int l = lane < 16 ? lane : 0;   // other lanes repeat lane 0's piece into their own place
     d.base = reinterpret_cast<const uint8_t *>(a.xs);
     d.off = (uint32_t)min(m0 + 8 * l, a.ms - 8) * 2;
@@ -182,7 +195,7 @@ __global__ __launch_bounds__(64 * LW, 1) void dual_gemm_large_kernel(GemmArgs a,
   const Geometry &geo = a.geo;
   const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int ti = wave >> 2, cp = wave & 3;
+  const int tp = wave >> 3, cc = wave & 7;   // token tile pair, column tile
   const int KG = geo.k / kGroup;
   const int m = a.m;
   const int ct32 = geo.n_pad / 32;
@@ -205,10 +218,10 @@ __global__ __launch_bounds__(64 * LW, 1) void dual_gemm_large_kernel(GemmArgs a,
   const int mb = bidx * band + brem % rows_in_band;
   const int m0 = mb * LBM, n0 = nb * LBN;
 
-  // ---- this wavefront's loads: item `wave`, and for r = 128 wavefront 0
-  // also item 16 ----
-  const LItem it0 = l_item<RT>(a, wave < C::NI ? wave : wave % C::NI, lane, m0, n0);
-  const bool two = wave + LW < C::NI;   // r = 128: wavefronts 0 and 1 load a second item
+  // ---- this wavefront's loads: item `wave`, and for wavefronts below
+  // NI - 16 also item wave + 16 ----
+  const LItem it0 = l_item<RT>(a, wave, lane, m0, n0);
+  const bool two = wave + LW < C::NI;
 
   // stage-2 operands: wavefront j < 8 the L2 blocks of column tile j,
   // wavefront 8 the L2 scales of the 8 tiles
@@ -230,10 +243,18 @@ __global__ __launch_bounds__(64 * LW, 1) void dual_gemm_large_kernel(GemmArgs a,
     }
   };
 
-  // H tile (ti, rt) goes to the wavefront with column pair (rt + RT ti) mod 4,
-  // so every SIMD (wavefront w runs on SIMD w mod 4 = cp) gets the same share
-  const int hrt = (cp - RT * ti) & 3;
-  const bool hw = hrt < RT;  // this wavefront also forms H tile (ti, hrt)
+  // H tiles: wavefront w runs on SIMD w mod 4 = cc mod 4.  RT = 1: the four
+  // tiles (ti, 0) go to wavefronts (tp, cc) = (ti / 2, ti); RT = 2: tile
+  // (2 tp + cc / 2, cc % 2) to wavefront (tp, cc < 4); RT = 4: tile
+  // (2 tp + cc % 2, cc / 2) to every wavefront -- the same number per SIMD.
+  // The token tile of this wavefront's H tile is its first tile tA, the other
+  // one tB.
+  int hsel = 0, hrt = 0;
+  bool hw = false;
+  if constexpr (RT == 1) { hw = cc < 4 && tp == (cc >> 1); hsel = cc & 1; }
+  if constexpr (RT == 2) { hw = cc < 4; hsel = (cc >> 1) & 1; hrt = cc & 1; }
+  if constexpr (RT == 4) { hw = true; hsel = cc & 1; hrt = cc >> 1; }
+  const int tA = 2 * tp + hsel, tB = 2 * tp + 1 - hsel;
   v16f acc0 = v16f{0}, acc1 = v16f{0}, hacc = v16f{0};
 
   auto k_loop = [&](auto PC, auto HC) {
@@ -247,55 +268,58 @@ __global__ __launch_bounds__(64 * LW, 1) void dual_gemm_large_kernel(GemmArgs a,
         ldma_s(it1.off + (uint32_t)g * it1.stride, l_uniform(it1.base), slot + it1.dst);
       }
     };
-    lwait_vm<0>();
-    stage2_loads();
-    for (int s = 0; s < D - 1; s++)
-      if (s < KG) issue(s);
-    for (int g = 0; g < KG; g++) {
-      // group g has landed (near the end of K nothing is issued past the
-      // last group, so everything issued is waited for)
-      if (g + D - 2 < KG) lwait_vm<(D - 2) * PER>();
-      else lwait_vm<0>();
-      __syncthreads();   // group g is visible; group g - 1 is consumed everywhere
-      if (g + D - 1 < KG) issue(g + D - 1);   // into group g - 1's slot
+    auto group = [&](int g) {
       const uint8_t *S = smem + (g % D) * C::SLOT;
-      const v8i av = unpack32(*reinterpret_cast<const u32x4 *>(S + C::S_A + ti * 1024 + lane * 16));
-      const uint32_t sa = *reinterpret_cast<const uint16_t *>(S + C::S_SX + (32 * ti + l32) * 2);
+      const v8i a0 = l_v8h(S + C::S_A + tA * 2048 + lane * 16);
+      const v8i a1 = l_v8h(S + C::S_A + tB * 2048 + lane * 16);
+      const uint32_t sa0 = *reinterpret_cast<const uint16_t *>(S + C::S_SX + (32 * tA + l32) * 2);
+      const uint32_t sa1 = *reinterpret_cast<const uint16_t *>(S + C::S_SX + (32 * tB + l32) * 2);
+      const v8i b = unpack32(*reinterpret_cast<const u32x4 *>(S + C::S_B + cc * 1024 + lane * 16));
+      const uint32_t sb = *reinterpret_cast<const uint16_t *>(S + C::S_SW + (32 * cc + l32) * 2);
       {
-        const v8i b = unpack32(*reinterpret_cast<const u32x4 *>(S + C::S_B + (2 * cp) * 1024 + lane * 16));
-        const uint32_t sb = *reinterpret_cast<const uint16_t *>(S + C::S_SW + (64 * cp + l32) * 2);
-        const v16f c = l_codes_half(av, b);
-        const v16f p = l_outer2(sa, sb);
+        const v16f c = l_codes_half(a0, b);
+        const v16f p = l_outer2(sa0, sb);
 #pragma unroll
         for (int v = 0; v < 16; v++) acc0[v] = fmaf(c[v], p[v], acc0[v]);
       }
       {
-        const v8i b = unpack32(*reinterpret_cast<const u32x4 *>(S + C::S_B + (2 * cp + 1) * 1024 + lane * 16));
-        const uint32_t sb = *reinterpret_cast<const uint16_t *>(S + C::S_SW + (64 * cp + 32 + l32) * 2);
-        const v16f c = l_codes_half(av, b);
-        const v16f p = l_outer2(sa, sb);
+        const v16f c = l_codes_half(a1, b);
+        const v16f p = l_outer2(sa1, sb);
 #pragma unroll
         for (int v = 0; v < 16; v++) acc1[v] = fmaf(c[v], p[v], acc1[v]);
       }
       if constexpr (HW) {
-        {
-          const v8i b = unpack32(*reinterpret_cast<const u32x4 *>(S + C::S_L + hrt * 1024 + lane * 16));
-          const uint32_t sb = *reinterpret_cast<const uint16_t *>(S + C::S_SW + 512 + (32 * hrt + l32) * 2);
-          const v16f c = l_codes_half(av, b);
-          const v16f p = l_outer2(sa, sb);
+        const v8i bl = unpack32(*reinterpret_cast<const u32x4 *>(S + C::S_L + hrt * 1024 + lane * 16));
+        const uint32_t sl = *reinterpret_cast<const uint16_t *>(S + C::S_SW + 512 + (32 * hrt + l32) * 2);
+        const v16f c = l_codes_half(a0, bl);
+        const v16f p = l_outer2(sa0, sl);
 #pragma unroll
-          for (int v = 0; v < 16; v++) hacc[v] = fmaf(c[v], p[v], hacc[v]);
-        }
+        for (int v = 0; v < 16; v++) hacc[v] = fmaf(c[v], p[v], hacc[v]);
       }
+    };
+    lwait_vm<0>();
+    stage2_loads();
+    for (int s = 0; s < D - 2; s++)
+      if (s < KG) issue(s);
+    for (int g2 = 0; g2 < KG; g2 += 2) {
+      // groups g2 and g2 + 1 have landed (loads complete in issue order; near
+      // the end of K fewer groups are in flight, so everything is waited for)
+      if (g2 + D - 3 < KG) lwait_vm<(D - 4) * PER>();
+      else lwait_vm<0>();
+      __syncthreads();   // groups g2, g2 + 1 are visible; g2 - 2, g2 - 1 are consumed everywhere
+      if (g2 + D - 2 < KG) issue(g2 + D - 2);   // into group g2 - 2's slot
+      if (g2 + D - 1 < KG) issue(g2 + D - 1);   // into group g2 - 1's slot
+      group(g2);
+      if (g2 + 1 < KG) group(g2 + 1);
     }
   };
   if constexpr (RT == 0) {
-    k_loop(std::integral_constant<int, 1>{}, std::false_type{});
-  } else if constexpr (C::NI > LW) {   // every wavefront forms an H tile (RT = 4)
-    if (two) k_loop(std::integral_constant<int, 2>{}, std::true_type{});
-    else k_loop(std::integral_constant<int, 1>{}, std::true_type{});
+    if (two) k_loop(std::integral_constant<int, 2>{}, std::false_type{});
+    else k_loop(std::integral_constant<int, 1>{}, std::false_type{});
   } else {
-    if (hw) k_loop(std::integral_constant<int, 1>{}, std::true_type{});
+    if (two && hw) k_loop(std::integral_constant<int, 2>{}, std::true_type{});
+    else if (two) k_loop(std::integral_constant<int, 2>{}, std::false_type{});
+    else if (hw) k_loop(std::integral_constant<int, 1>{}, std::true_type{});
     else k_loop(std::integral_constant<int, 1>{}, std::false_type{});
   }
   __syncthreads();   // every wavefront is done with the ring
@@ -307,7 +331,7 @@ __global__ __launch_bounds__(64 * LW, 1) void dual_gemm_large_kernel(GemmArgs a,
   if constexpr (RT > 0) {
     if (hw) {
 #pragma unroll
-      for (int v = 0; v < 16; v++) HS[(32 * ti + row_of_32x32(lane, v)) * C::HSTR + 32 * hrt + l32] = hacc[v];
+      for (int v = 0; v < 16; v++) HS[(32 * tA + row_of_32x32(lane, v)) * C::HSTR + 32 * hrt + l32] = hacc[v];
     }
     const int r = geo.r, gr = geo.gr, rg = r / gr;
     if (r < C::RB * 64)
@@ -366,7 +390,8 @@ __global__ __launch_bounds__(64 * LW, 1) void dual_gemm_large_kernel(GemmArgs a,
   // ---- stage 2 and the single epilogue: this wavefront's two tiles ----
 #pragma unroll
   for (int j = 0; j < 2; j++) {
-    const int jt = 2 * cp + j;          // column tile within the block
+    const int ti = j == 0 ? tA : tB;    // token tile within the block
+    const int jt = cc;                  // column tile within the block
     const int ct = n0 / 32 + jt;
     v16f ylr = v16f{0};
     if constexpr (RT > 0) {

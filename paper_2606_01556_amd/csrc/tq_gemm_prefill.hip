@@ -12,9 +12,11 @@
 // order, so H is bit-identical).  After that block H is re-quantized into LDS;
 // later blocks of the run reuse Q_H and s_H.
 //
-// K pipeline.  Everything a K-group needs -- the 128 activation rows, the 256
-// weight columns, the rank columns of L1 (first block only) and all their
-// scales -- arrives once per workgroup by direct global->LDS loads
+// K pipeline.  Everything a K-group needs -- the 128 activation rows (fp8
+// operand bytes: at these token counts the quantizer writes the codes
+// expanded, so no wavefront unpacks an activation operand), the 256 weight
+// columns, the rank columns of L1 (first block only) and all their scales --
+// arrives once per workgroup by direct global->LDS loads
 // (global_load_lds_dwordx4) into a D-slot ring, D - 1 groups ahead; the loads
 // of a group are spread over the 8 wavefronts.  One workgroup barrier per
 // group publishes the group and frees the slot read in the previous step.
@@ -50,14 +52,14 @@ constexpr int PBM = 128;   // tokens per workgroup block (four 32-row tiles)
 constexpr int PBN = 256;   // columns per block (eight 32-column tiles)
 constexpr int PNW = 8;     // wavefronts per workgroup
 // one ring slot (one K-group).  Main loop: activation tiles, weight tiles,
-// activation and weight scales.  H pass: activation tiles, L1 rank tiles in
+// weight and activation scales.  H pass: activation tiles, L1 rank tiles in
 // place of the weight tiles, activation and L1 scales.  Every load is one
 // 16-byte-per-lane wave load; the scale runs fill part of a 1 KiB region.
-constexpr int P_A = 0;          // 4 x 1 KiB activation tiles, matrix-core lane order
-constexpr int P_B = 4096;       // 8 x 1 KiB weight blocks as stored (H pass: L1 blocks)
-constexpr int P_SX = 12288;     // activation scales of the 128 tokens (256 B)
-constexpr int P_SW = 13312;     // weight scales of the 256 columns (H pass: L1 scales)
-constexpr int P_STAGE = 14336;
+constexpr int P_A = 0;          // 4 x 2 KiB fp8 activation tiles (two 1 KiB halves each)
+constexpr int P_B = 8192;       // 8 x 1 KiB weight blocks as stored (H pass: L1 blocks)
+constexpr int P_SW = 16384;     // weight scales of the 256 columns (H pass: all scales)
+constexpr int P_SX = 16896;     // activation scales of the 128 tokens (256 B)
+constexpr int P_STAGE = 17408;
 
 template <int RT, int D>
 struct PCfg {
@@ -132,41 +134,38 @@ __device__ __forceinline__ const uint8_t *uniform_ptr(const uint8_t *p) {
   return reinterpret_cast<const uint8_t *>(((uint64_t)hi << 32) | lo);
 }
 
-// This wavefront's share of one K-group's loads: exactly two 16-byte-per-lane
-// wave loads, so every wavefront has the same number in flight per group and
-// the K loop has no branches.  Item t reads b[t] + g * inc[t] + v[t] (lane).
+// This wavefront's share of one K-group's loads: two 16-byte-per-lane wave
+// loads (item t reads b[t] + g * inc[t] + v[t] (lane)), and for wavefront 0 a
+// third one, the scales of the group: lane l reads 16 bytes at
+// s3[l] + g * inc3[l].
 struct PPlan {
   const uint8_t *b1, *b2;     // wave-uniform bases of group 0
   uint32_t inc1, inc2;        // bytes per K-group
   uint32_t v1, v2;            // lane offsets
   uint32_t l1, l2;            // LDS offsets within a slot
+  const uint8_t *s3;          // lane address of group 0 (wavefront 0)
+  uint32_t inc3;              // lane bytes per K-group
 };
 
-__device__ __forceinline__ void p_issue(const PPlan &P, int g, uint32_t slot_lds) {
+__device__ __forceinline__ void p_issue(const PPlan &P, bool three, int g, uint32_t slot_lds) {
   dma_s(P.v1, uniform_ptr(P.b1 + (uint64_t)g * P.inc1), slot_lds + P.l1);
   dma_s(P.v2, uniform_ptr(P.b2 + (uint64_t)g * P.inc2), slot_lds + P.l2);
+  if (three) dma_v(P.s3 + (uint64_t)g * P.inc3, slot_lds + P_SW);
 }
 
 // activation tile t of the block (clamped to the last tile): its group-0
-// block; the tile of one group is 1 KiB in matrix-core lane order
+// block; the tile of one group is 2 KiB of fp8 operand bytes, two 1 KiB
+// halves in matrix-core lane order
 __device__ __forceinline__ const uint8_t *act_tile(const GemmArgs &a, int m0, int t) {
   const int tt = min(m0 / 32 + t, (a.m - 1) / 32);
-  return reinterpret_cast<const uint8_t *>(a.xc) + (int64_t)tt * (a.geo.k / kGroup) * 1024;
+  return reinterpret_cast<const uint8_t *>(a.xc) + (int64_t)tt * (a.geo.k / kGroup) * 2048;
 }
 
-// activation scales of the block's 128 tokens: eight per lane for lanes 0-15
-// (the other lanes repeat lane 15's run), clamped to the padded row count ms
-__device__ __forceinline__ void plan_xs(const GemmArgs &a, int m0, int lane, const uint8_t *&b,
-                                        uint32_t &inc, uint32_t &v) {
-  b = reinterpret_cast<const uint8_t *>(a.xs) + (int64_t)m0 * 2;
-  inc = (uint32_t)a.ms * 2;
-  v = (uint32_t)(min(m0 + 8 * min(lane, 15), a.ms - 8) - m0) * 2;
-}
-
-// Main loop: wavefront w loads weight tile w and, as its second item,
-// activation tile w (w < 4), the weight scales of the 256 columns (w = 4,
-// eight per lane for lanes 0-31) or the activation scales (w >= 5; the three
-// wavefronts load the same bytes to the same place).
+// Main loop: wavefront w loads weight tile w and, as its second item, half
+// w % 2 of activation tile w / 2.  Wavefront 0 also loads the scales: the weight
+// scales of the 256 columns (lanes 0-31, eight each, to P_SW) and the
+// activation scales of the 128 tokens (lanes 32-47, to P_SX; lanes 48-63
+// repeat lane 32's run into unused bytes), clamped to the padded sizes.
 __device__ __forceinline__ void plan_main(const GemmArgs &a, int lane, int wave, int m0, int n0,
                                           PPlan &P) {
   const Geometry &geo = a.geo;
@@ -176,72 +175,60 @@ __device__ __forceinline__ void plan_main(const GemmArgs &a, int lane, int wave,
   P.inc1 = 1024;
   P.v1 = lane * 16;
   P.l1 = P_B + wave * 1024;
-  if (wave < 4) {
-    P.b2 = act_tile(a, m0, wave);
-    P.inc2 = 1024;
-    P.v2 = lane * 16;
-    P.l2 = P_A + wave * 1024;
-  } else if (wave == 4) {
-    P.b2 = a.packed + geo.off_ws + (int64_t)n0 * 2;
-    P.inc2 = (uint32_t)geo.n_pad * 2;
-    P.v2 = (uint32_t)(min(n0 + 8 * min(lane, 31), geo.n_pad - 8) - n0) * 2;
-    P.l2 = P_SW;
+  P.b2 = act_tile(a, m0, wave >> 1) + (wave & 1) * 1024;
+  P.inc2 = 2048;
+  P.v2 = lane * 16;
+  P.l2 = P_A + wave * 1024;
+  if (lane < 32) {
+    P.s3 = a.packed + geo.off_ws + (int64_t)min(n0 + 8 * lane, geo.n_pad - 8) * 2;
+    P.inc3 = (uint32_t)geo.n_pad * 2;
   } else {
-    plan_xs(a, m0, lane, P.b2, P.inc2, P.v2);
-    P.l2 = P_SX;
+    const int l = lane < 48 ? lane - 32 : 0;
+    P.s3 = reinterpret_cast<const uint8_t *>(a.xs) + (int64_t)min(m0 + 8 * l, a.ms - 8) * 2;
+    P.inc3 = (uint32_t)a.ms * 2;
   }
 }
 
-// H pass.  A step covers HG consecutive K-groups (HG = 2 for up to 64 ranks,
-// 1 for 128), laid out in a slot as: activation tiles of group e at
-// 4096 e; L1 rank tile t of group e at P_B + 4096 + 1024 (e RT + t) -- P_B +
-// 1024 (e RT + t) for RT > 2 --; scales at P_SX: activation scales of group e
-// at P_SX + 512 e, L1 scales at P_SX + 256 + 512 e.  Every item is a wave load
-// whose lane l reads 16 bytes at base[l] + g(l) * stride[l], g(l) the lane's
-// group clamped to the last one.
-constexpr int H_L1 = 8192, H_S = 12288;
+// H pass.  A step covers one K-group, laid out in a slot as: the activation
+// tiles at P_A (as in the main loop), L1 rank tile t at P_B + 1024 t, and at
+// H_S the activation scales of the 128 tokens (256 B) followed by the L1
+// scales (256 B).  Every item is a wave load whose lane l reads 16 bytes at
+// base[l] + g * stride[l].
+constexpr int H_S = P_SW;
 
 struct HPlan {
   const uint8_t *base[2];   // lane addresses for group 0
   uint32_t stride[2];       // lane bytes per group
-  int e[2];                 // lane group offset within the step (0 .. HG-1)
   uint32_t lds[2];          // wave-uniform LDS offset within a slot
 };
 
-__device__ __forceinline__ void h_issue(const HPlan &P, int g0, int KG, uint32_t slot_lds) {
+__device__ __forceinline__ void h_issue(const HPlan &P, int g, uint32_t slot_lds) {
 #pragma unroll
-  for (int t = 0; t < 2; t++) {
-    const int g = min(g0 + P.e[t], KG - 1);
-    dma_v(P.base[t] + (uint64_t)g * P.stride[t], slot_lds + P.lds[t]);
-  }
+  for (int t = 0; t < 2; t++) dma_v(P.base[t] + (uint64_t)g * P.stride[t], slot_lds + P.lds[t]);
 }
 
-// items, in order: HG x 4 activation tiles, HG x RT L1 tiles, one scale item,
-// then repeats of earlier items (same bytes to the same place); wavefront w
-// takes items w and w + 8
+// items, in order: the 8 activation halves, RT L1 tiles, one scale item, then
+// repeats of earlier items (same bytes to the same place); wavefront w takes
+// items w and w + 8
 __device__ __forceinline__ void plan_h(const GemmArgs &a, int lane, int wave, int m0, int RT,
-                                       int HG, HPlan &P) {
+                                       HPlan &P) {
   const Geometry &geo = a.geo;
   const int KG = geo.k / kGroup;
-  const int nitem = HG * 4 + HG * RT + 1;
+  const int nitem = 8 + RT + 1;
 #pragma unroll
   for (int t = 0; t < 2; t++) {
     int it = wave + 8 * t;
     if (it >= nitem) it -= 8;   // a repeat of item it - 8
-    if (it < HG * 4) {          // activation tile it % 4 of group it / 4
-      const int e = it >> 2, tt = it & 3;
-      P.base[t] = act_tile(a, m0, tt) + lane * 16;
+    if (it < 8) {               // half it % 2 of activation tile it / 2
+      P.base[t] = act_tile(a, m0, it >> 1) + (it & 1) * 1024 + lane * 16;
+      P.stride[t] = 2048;
+      P.lds[t] = P_A + 1024 * it;
+    } else if (it < 8 + RT) {   // L1 rank tile it - 8
+      P.base[t] = a.packed + geo.off_l1 + (int64_t)(it - 8) * KG * 1024 + lane * 16;
       P.stride[t] = 1024;
-      P.e[t] = e;
-      P.lds[t] = P_A + 4096 * e + 1024 * tt;
-    } else if (it < HG * 4 + HG * RT) {   // L1 rank tile tt of group e
-      const int q = it - HG * 4, e = q / RT, tt = q % RT;
-      P.base[t] = a.packed + geo.off_l1 + (int64_t)tt * KG * 1024 + lane * 16;
-      P.stride[t] = 1024;
-      P.e[t] = e;
-      P.lds[t] = (RT > 2 ? P_B : H_L1) + 1024 * (e * RT + tt);
-    } else {   // scales: lanes 16 e + (0-15): activation (even) or L1 (odd) runs
-      const int q = lane >> 4, e = min(q >> 1, HG - 1), r = lane & 15;
+      P.lds[t] = P_B + 1024 * (it - 8);
+    } else {   // scales: lanes 0-15 activation runs, 16-31 L1 runs, then repeats
+      const int q = lane >> 4, r = lane & 15;
       if ((q & 1) == 0) {
         P.base[t] = reinterpret_cast<const uint8_t *>(a.xs) +
                     (int64_t)min(m0 + 8 * r, a.ms - 8) * 2;
@@ -250,7 +237,6 @@ __device__ __forceinline__ void plan_h(const GemmArgs &a, int lane, int wave, in
         P.base[t] = a.packed + geo.off_l1s + (int64_t)min(8 * r, geo.r_pad32 - 8) * 2;
         P.stride[t] = (uint32_t)geo.r_pad32 * 2;
       }
-      P.e[t] = e;
       P.lds[t] = H_S;
     }
   }
@@ -264,31 +250,35 @@ struct PKernel {
   // the last group again, so every step waits for the same count); returns
   // when group 0 is visible to the workgroup
   template <typename Pre>
-  __device__ __forceinline__ static void prologue(const PPlan &P, uint32_t ring_lds, int KG,
-                                                  Pre pre) {
+  __device__ __forceinline__ static void prologue(const PPlan &P, bool three, uint32_t ring_lds,
+                                                  int KG, Pre pre) {
     // Every load the compiler itself issued (e.g. spill reloads) is complete
     // here, so it has no reason to wait on the vector-memory counter inside
     // the K loop -- a wait there would also drain the ring's loads.
     wait_vm<0>();
     pre();   // loads issued here complete before the ring's first group
 #pragma unroll
-    for (int s = 0; s < D; s++) p_issue(P, min(s, KG - 1), ring_lds + s * C::STAGE);
-    wait_vm<2 * (D - 1)>();
+    for (int s = 0; s < D; s++) p_issue(P, three, min(s, KG - 1), ring_lds + s * C::STAGE);
+    if (three) wait_vm<3 * (D - 1)>();
+    else wait_vm<2 * (D - 1)>();
     __syncthreads();
   }
 
   // one step's hand-over: group g + 1 has landed (own loads), this wavefront's
   // reads are done, every wavefront is past step g - 1, so group g + 1 is
   // visible and slot g % D is free for group g + D
-  __device__ __forceinline__ static void advance(const PPlan &P, uint32_t ring_lds, int g, int KG) {
-    wait_vm<2 * (D - 2)>();
+  __device__ __forceinline__ static void advance(const PPlan &P, bool three, uint32_t ring_lds,
+                                                 int g, int KG) {
+    if (three) wait_vm<3 * (D - 2)>();
+    else wait_vm<2 * (D - 2)>();
     wait_lgkm0();
     __syncthreads();
-    p_issue(P, min(g + D, KG - 1), ring_lds + (g % D) * C::STAGE);
+    p_issue(P, three, min(g + D, KG - 1), ring_lds + (g % D) * C::STAGE);
   }
 
   struct Raw {
-    u32x4 a[2], b[2];
+    v8i a[2];      // fp8 activation operands, ready for the matrix cores
+    u32x4 b[2];    // TQ4 weight operands
     uint32_t sa[2], sb[2];
   };
 
@@ -298,7 +288,8 @@ struct PKernel {
 #pragma unroll
     for (int i = 0; i < 2; i++) {
       const int ti = 2 * wr + i;
-      R.a[i] = *reinterpret_cast<const u32x4 *>(S + P_A + ti * 1024 + lane * 16);
+      R.a[i] = join(*reinterpret_cast<const u32x4 *>(S + P_A + ti * 2048 + lane * 16),
+                    *reinterpret_cast<const u32x4 *>(S + P_A + ti * 2048 + 1024 + lane * 16));
       R.sa[i] = *reinterpret_cast<const uint16_t *>(S + P_SX + (32 * ti + l32) * 2);
     }
 #pragma unroll
@@ -320,13 +311,13 @@ struct PKernel {
   // (Each region between scheduling barriers is pinned to "one matrix-core
   // instruction, then the vector work".)
   template <typename Pre>
-  __device__ __forceinline__ static void main_loop(const PPlan &P, uint8_t *smem,
+  __device__ __forceinline__ static void main_loop(const PPlan &P, bool three, uint8_t *smem,
                                                    uint32_t ring_lds, int KG, int lane, int wr,
                                                    int wc, v16f (&acc)[2][2], Pre pre) {
-    prologue(P, ring_lds, KG, pre);
+    prologue(P, three, ring_lds, KG, pre);
     Raw R;
     read_raw(smem, lane, wr, wc, R);
-    v8i a0 = unpack32(R.a[0]);
+    v8i a0 = R.a[0];
     v8i b0 = unpack32(R.b[0]);
     // tile 11's products of the previous group (none yet: fma(0, 0, +0)
     // leaves the accumulator at +0)
@@ -343,7 +334,7 @@ struct PKernel {
       __builtin_amdgcn_sched_group_barrier(0x002, 12, 0);
       __builtin_amdgcn_sched_barrier(0);
       const v16f c01 = codes_half(a0, b1);
-      const v8i a1 = unpack32(R.a[1]);
+      const v8i a1 = R.a[1];
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x002, 12, 0);
       __builtin_amdgcn_sched_barrier(0);
@@ -352,7 +343,7 @@ struct PKernel {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);
       __builtin_amdgcn_sched_barrier(0);
-      advance(P, ring_lds, g, KG);
+      advance(P, three, ring_lds, g, KG);
       Raw Rn;
       read_raw(smem + ((g + 1) % D) * C::STAGE, lane, wr, wc, Rn);
       asm volatile("" ::: "memory");   // issue the reads here, ahead of their use
@@ -365,7 +356,7 @@ struct PKernel {
       __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);
       __builtin_amdgcn_sched_barrier(0);
       c11 = codes_half(a1, b1);
-      a0 = unpack32(Rn.a[0]);
+      a0 = Rn.a[0];
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x002, 12, 0);
       __builtin_amdgcn_sched_barrier(0);
@@ -382,54 +373,43 @@ struct PKernel {
   }
 
   // The stage-1 pass: H tiles of 32 tokens x 32 ranks, accumulated over all
-  // K-groups in ascending order (token tile ti, rank tiles hrt[]), HG groups
+  // K-groups in ascending order (token tile ti, rank tiles hrt[]), one group
   // per ring slot and step.
-  static constexpr int HG = RT > 2 ? 1 : 2;
   __device__ __forceinline__ static void h_loop(const HPlan &P, uint8_t *smem, uint32_t ring_lds,
                                                 int KG, int lane, bool hw, int ti,
                                                 const int (&hrt)[C::HT], v16f (&hacc)[C::HT]) {
-    const int NS = (KG + HG - 1) / HG;   // steps
     wait_vm<0>();
 #pragma unroll
-    for (int s = 0; s < D; s++) h_issue(P, min(s, NS - 1) * HG, KG, ring_lds + s * C::STAGE);
+    for (int s = 0; s < D; s++) h_issue(P, min(s, KG - 1), ring_lds + s * C::STAGE);
     wait_vm<2 * (D - 1)>();
     __syncthreads();
     const int l32 = lane & 31;
-    for (int s = 0; s < NS; s++) {
+    for (int s = 0; s < KG; s++) {
       const uint8_t *S = smem + (s % D) * C::STAGE;
-      u32x4 ra[HG], rl[HG][C::HT];
-      uint32_t sa[HG], sl[HG][C::HT];
+      v8i ra = v8i{0};
+      u32x4 rl[C::HT];
+      uint32_t sa = 0, sl[C::HT];
       if (hw) {
+        ra = join(*reinterpret_cast<const u32x4 *>(S + P_A + ti * 2048 + lane * 16),
+                  *reinterpret_cast<const u32x4 *>(S + P_A + ti * 2048 + 1024 + lane * 16));
+        sa = *reinterpret_cast<const uint16_t *>(S + H_S + (32 * ti + l32) * 2);
 #pragma unroll
-        for (int e = 0; e < HG; e++) {
-          ra[e] = *reinterpret_cast<const u32x4 *>(S + P_A + 4096 * e + ti * 1024 + lane * 16);
-          sa[e] = *reinterpret_cast<const uint16_t *>(S + H_S + 512 * e + (32 * ti + l32) * 2);
-#pragma unroll
-          for (int h = 0; h < C::HT; h++) {
-            rl[e][h] = *reinterpret_cast<const u32x4 *>(
-                S + (RT > 2 ? P_B : H_L1) + 1024 * (e * RT + hrt[h]) + lane * 16);
-            sl[e][h] = *reinterpret_cast<const uint16_t *>(S + H_S + 256 + 512 * e +
-                                                           (32 * hrt[h] + l32) * 2);
-          }
+        for (int h = 0; h < C::HT; h++) {
+          rl[h] = *reinterpret_cast<const u32x4 *>(S + P_B + 1024 * hrt[h] + lane * 16);
+          sl[h] = *reinterpret_cast<const uint16_t *>(S + H_S + 256 + (32 * hrt[h] + l32) * 2);
         }
       }
-      // step s + 1 has landed and every wavefront is done with slot s
+      // group s + 1 has landed and every wavefront is done with slot s
       wait_vm<2 * (D - 2)>();
       wait_lgkm0();
       __syncthreads();
-      h_issue(P, min(s + D, NS - 1) * HG, KG, ring_lds + (s % D) * C::STAGE);
+      h_issue(P, min(s + D, KG - 1), ring_lds + (s % D) * C::STAGE);
       if (hw) {
 #pragma unroll
-        for (int e = 0; e < HG; e++) {
-          if (s * HG + e < KG) {
-            const v8i av = unpack32(ra[e]);
-#pragma unroll
-            for (int h = 0; h < C::HT; h++) {
-              const v16f ch = codes_half(av, unpack32(rl[e][h]));
-              const v16f ph = outer2(sa[e], sl[e][h]);
-              fma16(hacc[h], ch, ph);
-            }
-          }
+        for (int h = 0; h < C::HT; h++) {
+          const v16f ch = codes_half(ra, unpack32(rl[h]));
+          const v16f ph = outer2(sa, sl[h]);
+          fma16(hacc[h], ch, ph);
         }
       }
     }
@@ -489,7 +469,7 @@ __global__ __launch_bounds__(64 * PNW, 1) void dual_gemm_prefill_kernel(GemmArgs
       if (cb == cb_begin) {
         // ---- stage 1: H for the block's 128 tokens, then Q_H and s_H in LDS ----
         HPlan HP;
-        plan_h(a, lane, wave, m0, RT, K::HG, HP);
+        plan_h(a, lane, wave, m0, RT, HP);
         v16f hacc[C::HT];
 #pragma unroll
         for (int h = 0; h < C::HT; h++) hacc[h] = v16f{0};
@@ -595,7 +575,7 @@ __global__ __launch_bounds__(64 * PNW, 1) void dual_gemm_prefill_kernel(GemmArgs
               l2_lds + 2 * C::RB * 1024);
       }
     };
-    K::main_loop(P, smem, ring_lds, KG, lane, wr, wc, acc, pre);
+    K::main_loop(P, wave == 0, smem, ring_lds, KG, lane, wr, wc, acc, pre);
 
     // ---- stage 2 (Q_H Q(L2)) and the single epilogue ----
     // (the index values are re-derived here, behind an opaque copy, so the
@@ -689,7 +669,7 @@ hipError_t launch_prefill_rt(const GemmArgs &a, hipStream_t s) {
     case 0: return launch_prefill<0, D>(a, s);
     case 1: return launch_prefill<1, D>(a, s);
     case 2: return launch_prefill<2, D>(a, s);
-    case 4: return launch_prefill<4, D>(a, s);
+    case 4: return launch_prefill<4, 5>(a, s);   // six slots and the stage-2 region overflow the LDS
     default: return hipErrorInvalidValue;
   }
 }

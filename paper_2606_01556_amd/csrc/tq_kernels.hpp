@@ -11,6 +11,18 @@ namespace tq {
 constexpr int kMaxRank = 128;
 constexpr size_t kWorkspaceBytes = 20480;
 
+// Token counts up to kMidMaxTokens run the decode and mid kernels, which take
+// the activation codes as TQ4 nibbles (k / 2 bytes per token).  Larger counts
+// run the large and prefill kernels, which are bound by vector-ALU work and
+// take the codes already expanded to their fp8 operand bytes (k bytes per
+// token), so none of their wavefronts unpacks an activation operand.
+constexpr int kMidMaxTokens = 512;
+inline bool act_codes_fp8(int m) { return m > kMidMaxTokens; }
+inline size_t act_codes_bytes(int m, int k) {
+  const size_t m32 = (size_t)(m + 31) / 32 * 32;
+  return act_codes_fp8(m) ? m32 * (size_t)k : m32 * (size_t)k / 2;
+}
+
 // Geometry shared by the packing, export and GEMM kernels.
 //  W_res codes: [n_pad/32][k/64] blocks of 1 KiB; block lane L (16 bytes,
 //               4 TQ4 words) holds column 32*t + L%32, k in [32*(L/32), +32)
@@ -27,7 +39,8 @@ struct Geometry {
 struct GemmArgs {
   const uint8_t *packed;
   Geometry geo;
-  const uint32_t *xc;   // [m32/32][k/64] 1 KiB activation tiles (matrix-core lane order)
+  const uint32_t *xc;   // [m32/32][k/64] activation tiles (matrix-core lane order):
+                        // 1 KiB of TQ4 nibbles, or 2 KiB of fp8 bytes if act_codes_fp8(m)
   const uint16_t *xs;   // [k/64][ms] fp16
   int ms;               // row stride of xs: m rounded up to a multiple of 32 (= m32)
   void *y;              // [m][n]

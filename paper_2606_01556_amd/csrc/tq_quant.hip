@@ -15,12 +15,16 @@ namespace tq {
 // 8 j + 4 h + l quantizes codes 32 h + 8 l .. + 7 of the group for token
 // 8 w + j (16 bytes of the row) into one TQ4 word, and the 8 lanes of a token
 // share the group max through three DPP lane swizzles.  All QG loads of a
-// lane are issued before any is used.  Token 32 t + i, codes 32 h .. 32 h + 31
-// of group g land at byte ((t * KG + g) * 64 + 32 h + i) * 16 (the lane order
-// of one matrix-core operand), so each wavefront stores two contiguous
-// 128-byte runs per block.  The padding tokens [m, m32) of the last tile get
-// zero codes.  Scales are stored group-major with the token count padded to
-// m32 (padding entries are zero).
+// lane are issued before any is used.  TQ4 output (m <= kMidMaxTokens): token
+// 32 t + i, codes 32 h .. 32 h + 31 of group g land at byte
+// ((t * KG + g) * 64 + 32 h + i) * 16 (the lane order of one matrix-core
+// operand), so each wavefront stores two contiguous 128-byte runs per block.
+// fp8 output (larger m): the same operand as 32 fp8 bytes per lane, split into
+// two 1 KiB halves -- bytes 16 p .. 16 p + 15 of lane slot 32 h + i at byte
+// ((t * KG + g) * 2 + p) * 1024 + (32 h + i) * 16 -- so each half is one
+// 16-byte-per-lane wave load and one conflict-free LDS read.  The padding
+// tokens [m, m32) of the last tile get zero codes.  Scales are stored
+// group-major with the token count padded to m32 (padding entries are zero).
 // ---------------------------------------------------------------------------
 constexpr int QG = 1;
 
@@ -33,6 +37,7 @@ __device__ __forceinline__ float max8_dpp(float a) {
   return a;
 }
 
+template <bool FP8>
 __global__ __launch_bounds__(256) void quant_act_kernel(const uint16_t *__restrict__ x, int m,
                                                         int k, uint32_t *__restrict__ codes,
                                                         uint16_t *__restrict__ scales) {
@@ -70,7 +75,18 @@ __global__ __launch_bounds__(256) void quant_act_kernel(const uint16_t *__restri
 #pragma unroll
     for (int e = 0; e < 8; e++) c[e] = q4_code_fp16(v[e], s, y);
     if (g < KG) {
-      codes[(((int64_t)t * KG + g) * 64 + 32 * h + i) * 4 + l] = tq4_pack8(c);
+      if constexpr (FP8) {
+        uint32_t b0 = 0, b1 = 0;
+#pragma unroll
+        for (int e = 0; e < 4; e++) {
+          b0 |= code_to_fp8(c[e]) << (8 * e);
+          b1 |= code_to_fp8(c[4 + e]) << (8 * e);
+        }
+        const int64_t off = (((int64_t)t * KG + g) * 2 + (l >> 1)) * 256 + (32 * h + i) * 4 + 2 * (l & 1);
+        *reinterpret_cast<uint2 *>(codes + off) = make_uint2(b0, b1);
+      } else {
+        codes[(((int64_t)t * KG + g) * 64 + 32 * h + i) * 4 + l] = tq4_pack8(c);
+      }
       if ((lane & 7) == 0) scales[(int64_t)g * m32 + row] = row < m ? s16 : (uint16_t)0;
     }
   }
@@ -80,8 +96,11 @@ hipError_t launch_quant_act(const uint16_t *x, int m, int k, uint32_t *codes, ui
                             hipStream_t s) {
   const int m32 = (m + 31) / 32 * 32;
   const int KG = k / kGroup;
-  hipLaunchKernelGGL(quant_act_kernel, dim3((unsigned)((KG + QG - 1) / QG), (unsigned)(m32 / 32)),
-                     dim3(256), 0, s, x, m, k, codes, scales);
+  const dim3 grid((unsigned)((KG + QG - 1) / QG), (unsigned)(m32 / 32));
+  if (act_codes_fp8(m))
+    hipLaunchKernelGGL(quant_act_kernel<true>, grid, dim3(256), 0, s, x, m, k, codes, scales);
+  else
+    hipLaunchKernelGGL(quant_act_kernel<false>, grid, dim3(256), 0, s, x, m, k, codes, scales);
   return hipGetLastError();
 }
 

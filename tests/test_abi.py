@@ -146,3 +146,36 @@ def test_act_codes_tile_layout_roundtrip():
     back = tq.act_codes_rows(blocks.reshape(m32 // 32, kg, 256), m)
     np.testing.assert_array_equal(back, codes[:m])
     assert tq.padded_tokens(1) == 32 and tq.padded_tokens(32) == 32 and tq.padded_tokens(33) == 64
+
+
+def test_act_codes_fp8_layout_roundtrip():
+    """act_codes_rows inverts the fp8 activation layout used above 512 tokens:
+    token 32 t + i, codes 32 h + 16 p .. + 15 of group g are the bytes
+    sign << 7 | |q| of lane slot 32 h + i in half p of the 2 KiB block (t, g)."""
+    rng = np.random.default_rng(6)
+    m, k = 520, 128
+    m32 = tq.padded_tokens(m)
+    codes = np.zeros((m32, k), np.int8)
+    codes[:m] = rng.integers(-7, 8, size=(m, k))
+    kg = k // 64
+    blocks = np.zeros((m32 // 32, kg, 2, 64, 16), np.uint8)   # tile, group, half p, slot, byte
+    for t in range(m32 // 32):
+        for g in range(kg):
+            for p in range(2):
+                for h in range(2):
+                    for i in range(32):
+                        q = codes[32 * t + i, 64 * g + 32 * h + 16 * p: 64 * g + 32 * h + 16 * p + 16]
+                        blocks[t, g, p, 32 * h + i] = np.where(q < 0, 0x80 | -q.astype(np.int16), q)
+    back = tq.act_codes_rows(blocks.view(np.uint32).reshape(m32 // 32, kg, 512), m)
+    np.testing.assert_array_equal(back, codes[:m])
+    assert tq.fp8_code_decode(np.array([0x87, 0x07, 0x00, 0x81], np.uint8)).tolist() == [-7, 7, 0, -1]
+
+
+def test_act_codes_bytes(L):
+    """x_codes sizes: 4 bits per code up to 512 tokens, 8 bits beyond; 0 for bad shapes."""
+    assert L.tq_act_codes_bytes(1, 4096) == 32 * 4096 // 2
+    assert L.tq_act_codes_bytes(512, 4096) == 512 * 4096 // 2
+    assert L.tq_act_codes_bytes(513, 4096) == 544 * 4096
+    assert L.tq_act_codes_bytes(2048, 64) == 2048 * 64
+    assert L.tq_act_codes_bytes(0, 4096) == 0
+    assert L.tq_act_codes_bytes(16, 100) == 0 and L.tq_act_codes_bytes(-1, 64) == 0
