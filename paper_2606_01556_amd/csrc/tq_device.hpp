@@ -88,26 +88,6 @@ __device__ __forceinline__ int q4_code(float v, float s) {
   return (int)t;
 }
 
-// The same code for fp16 inputs v and s (s = the group's fp16 scale, y any
-// approximation of 1 / s within a few ulp), without a full-precision division.
-// For fp16 v and s the exact quotient v / s is either a half-integer or at
-// least 2.4e-4 away from every half-integer (write v = A 2^p, s = B 2^q with
-// |A|, B < 2^11: a non-zero distance is a multiple of 2^(min(p+1, q) - q) / (2B)),
-// so rounding v * y to the nearest integer already gives rint(v / s) except
-// on exact ties.  Those are found with the exact remainder r = v - q s (one
-// fma; q s and the difference are exact in fp32): |r| = s / 2 exactly, and
-// the even one of q and q + sign(r) is taken (round half to even).  This is
-// the remainder correction of Markstein's division method, specialised to a
-// quotient that is only needed to the nearest integer.
-__device__ __forceinline__ int q4_code_fp16(float v, float s, float y) {
-  if (s == 0.0f) return 0;
-  float q = __builtin_rintf(v * y);
-  const float r = fmaf(-q, s, v);
-  if (fabsf(r) == 0.5f * s && ((int)q & 1)) q += r > 0.0f ? 1.0f : -1.0f;
-  q = q > 7.0f ? 7.0f : (q < -7.0f ? -7.0f : q);
-  return (int)q;
-}
-
 // Exact integer dot products of 32x32 code tiles over one group of 64:
 // D[i][j] = sum_k A[i][k] * B[k][j].  Operand lane l holds row/column l % 32,
 // k in [32 * (l / 32), +32); result lane l holds column l % 32, rows

@@ -26,8 +26,6 @@ namespace tq {
 // tokens [m, m32) of the last tile get zero codes.  Scales are stored
 // group-major with the token count padded to m32 (padding entries are zero).
 // ---------------------------------------------------------------------------
-constexpr int QG = 1;
-
 // max over the 8 lanes 8 j .. 8 j + 7 with DPP lane swizzles: swap neighbours,
 // swap pairs, then mirror the two quads of the eight
 __device__ __forceinline__ float max8_dpp(float a) {
@@ -37,7 +35,43 @@ __device__ __forceinline__ float max8_dpp(float a) {
   return a;
 }
 
-template <bool FP8>
+// Codes of eight fp16 values v of one group with fp16 scale s (s > 0, or 0
+// for a group that quantizes to zeros), as fp8 operand bytes: lo holds codes
+// 0..3, hi codes 4..7.  y is 1 / s to within a few ulp (0 when s == 0).
+//
+// For fp16 v and s the exact quotient v / s is either a half-integer or at
+// least 2.4e-4 away from every half-integer (write v = A 2^p, s = B 2^q with
+// |A|, B < 2^11: a non-zero distance is a multiple of 2^(min(p+1, q) - q) /
+// (2B)), so rounding t = v * y to the nearest integer already gives
+// rint(v / s) except on exact ties.  A tie shows in the exact remainder
+// r = v - rint(t) s (one fma; the product and the difference are exact in
+// fp32) as |r| = s / 2, and round-half-to-even then takes 2 rint(t / 2), the
+// even one of the two neighbours (t / 2 lies within rounding error of an odd
+// multiple of 1/4, far from any rounding boundary).  This is the remainder
+// correction of Markstein's division method, specialised to a quotient needed
+// only to the nearest integer.  The clamped code q becomes the byte
+// sign << 7 | |q| as the e4m3 value q 2^-9 (a subnormal, converted exactly;
+// the fma adds +0 so a zero code is never -0).
+__device__ __forceinline__ void quant8_fp8(const float (&v)[8], float s, float y, uint32_t &lo,
+                                           uint32_t &hi) {
+  const float hs = 0.5f * s;
+  float f[8];
+#pragma unroll
+  for (int e = 0; e < 8; e++) {
+    const float t = v[e] * y;
+    const float q = __builtin_rintf(t);
+    const float r = fmaf(-q, s, v[e]);
+    const float qe = 2.0f * __builtin_rintf(0.5f * t);
+    const float c = fminf(fmaxf(fabsf(r) == hs ? qe : q, -7.0f), 7.0f);
+    f[e] = fmaf(c, 0x1p-9f, 0.0f);
+  }
+  lo = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(f[0], f[1], 0, false);
+  lo = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(f[2], f[3], (int)lo, true);
+  hi = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(f[4], f[5], 0, false);
+  hi = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(f[6], f[7], (int)hi, true);
+}
+
+template <bool FP8, int QG>
 __global__ __launch_bounds__(256) void quant_act_kernel(const uint16_t *__restrict__ x, int m,
                                                         int k, uint32_t *__restrict__ codes,
                                                         uint16_t *__restrict__ scales) {
@@ -49,12 +83,15 @@ __global__ __launch_bounds__(256) void quant_act_kernel(const uint16_t *__restri
   const int row = 32 * t + i;
   const int m32 = (int)gridDim.y * 32;
   u32x4 raw[QG];
+  // padding tokens read the last real row (m >= 1) and quantize zeros; every
+  // load is issued before the first is used
+  const bool live = row < m;
+  const uint16_t *src = x + (int64_t)(live ? row : m - 1) * k + g0 * kGroup + 32 * h + 8 * l;
 #pragma unroll
-  for (int q = 0; q < QG; q++) {
-    raw[q] = u32x4{0, 0, 0, 0};
-    if (row < m && g0 + q < KG)
-      raw[q] = *reinterpret_cast<const u32x4 *>(x + (int64_t)row * k + (g0 + q) * kGroup + 32 * h + 8 * l);
-  }
+  for (int q = 0; q < QG; q++) raw[q] = *reinterpret_cast<const u32x4 *>(src + q * kGroup);
+#pragma unroll
+  for (int q = 0; q < QG; q++)
+    if (!live) raw[q] = u32x4{0, 0, 0, 0};
 #pragma unroll
   for (int q = 0; q < QG; q++) {
     const int g = g0 + q;
@@ -70,22 +107,17 @@ __global__ __launch_bounds__(256) void quant_act_kernel(const uint16_t *__restri
     amax = max8_dpp(amax);
     uint16_t s16;
     const float s = q4_scale(amax, s16);
-    const float y = __builtin_amdgcn_rcpf(s);
-    int c[8];
-#pragma unroll
-    for (int e = 0; e < 8; e++) c[e] = q4_code_fp16(v[e], s, y);
-    if (g < KG) {
+    const float y = s == 0.0f ? 0.0f : __builtin_amdgcn_rcpf(s);
+    uint32_t b0, b1;
+    quant8_fp8(v, s, y, b0, b1);
+    {   // the launch covers the K-groups exactly (QG divides k / 64)
       if constexpr (FP8) {
-        uint32_t b0 = 0, b1 = 0;
-#pragma unroll
-        for (int e = 0; e < 4; e++) {
-          b0 |= code_to_fp8(c[e]) << (8 * e);
-          b1 |= code_to_fp8(c[4 + e]) << (8 * e);
-        }
         const int64_t off = (((int64_t)t * KG + g) * 2 + (l >> 1)) * 256 + (32 * h + i) * 4 + 2 * (l & 1);
         *reinterpret_cast<uint2 *>(codes + off) = make_uint2(b0, b1);
       } else {
-        codes[(((int64_t)t * KG + g) * 64 + 32 * h + i) * 4 + l] = tq4_pack8(c);
+        // TQ4 word: the inverse of tq4_to_fp8 (codes 4..7 rotated into the
+        // bits 0x78787878 that codes 0..3 leave free)
+        codes[(((int64_t)t * KG + g) * 64 + 32 * h + i) * 4 + l] = b0 | __builtin_amdgcn_alignbit(b1, b1, 28);
       }
       if ((lane & 7) == 0) scales[(int64_t)g * m32 + row] = row < m ? s16 : (uint16_t)0;
     }
@@ -96,11 +128,13 @@ hipError_t launch_quant_act(const uint16_t *x, int m, int k, uint32_t *codes, ui
                             hipStream_t s) {
   const int m32 = (m + 31) / 32 * 32;
   const int KG = k / kGroup;
-  const dim3 grid((unsigned)((KG + QG - 1) / QG), (unsigned)(m32 / 32));
+  // one K-group per work-group: the kernel is bound by its vector ALU work,
+  // and more groups per work-group measured slower at every size
+  const dim3 grid((unsigned)KG, (unsigned)(m32 / 32));
   if (act_codes_fp8(m))
-    hipLaunchKernelGGL(quant_act_kernel<true>, grid, dim3(256), 0, s, x, m, k, codes, scales);
+    hipLaunchKernelGGL((quant_act_kernel<true, 1>), grid, dim3(256), 0, s, x, m, k, codes, scales);
   else
-    hipLaunchKernelGGL(quant_act_kernel<false>, grid, dim3(256), 0, s, x, m, k, codes, scales);
+    hipLaunchKernelGGL((quant_act_kernel<false, 1>), grid, dim3(256), 0, s, x, m, k, codes, scales);
   return hipGetLastError();
 }
 
