@@ -98,16 +98,23 @@ def run_gpu(X, W, L1, L2, bf16=False, debug=True):
     return out
 
 
-def check_tolerance(Y, ref64, bf16=False):
+def check_tolerance(Y, ref64, bf16=False, wide_range=False):
+    """Relative Frobenius error <= 1e-3 and max-abs error <= 1e-2 rms(Y).  For
+    outputs far above their rms (wide_range) the fp16 output rounding alone,
+    up to 2^-11 |y|, exceeds 1e-2 rms; the max-abs bound then adds that
+    rounding elementwise."""
     f = BF16_FACTOR if bf16 else 1.0
     err = Y.astype(np.float64) - ref64
     rel = np.linalg.norm(err) / max(np.linalg.norm(ref64), 1e-300)
     rms = np.sqrt(np.mean(ref64 ** 2))
     assert rel <= f * REL_FRO, f"relative Frobenius error {rel:.3e}"
-    assert np.max(np.abs(err)) <= f * MAX_ABS_RMS * rms + 1e-30, "max-abs error"
+    bound = f * MAX_ABS_RMS * rms + 1e-30
+    if wide_range:
+        bound = bound + f * 2.0 ** -11 * np.abs(ref64)
+    assert np.all(np.abs(err) <= bound), "max-abs error"
 
 
-def full_parity(oracle_mod, X, W, L1, L2, bf16=False):
+def full_parity(oracle_mod, X, W, L1, L2, bf16=False, wide_range=False):
     g = run_gpu(X, W, L1, L2, bf16)
     o = oracle_mod.layer(X, W, L1, L2, GROUP)
     qx, sx = oracle_mod.quantize(X, GROUP)
@@ -132,7 +139,7 @@ def full_parity(oracle_mod, X, W, L1, L2, bf16=False):
             np.testing.assert_array_equal(g["Ybits"], o["Ybf"])
         else:
             np.testing.assert_array_equal(g["Ybits"], o["Y16"].view(np.uint16))
-    check_tolerance(g["Y"], o["Y64"], bf16)
+    check_tolerance(g["Y"], o["Y64"], bf16, wide_range)
     return g, o
 
 
@@ -369,3 +376,27 @@ def test_qwen3_8b(oracle_mod, li, M):
 def test_llama3_70b(oracle_mod, li, M):
     say(f"llama3-70b layer={li} M={M}")
     sampled_parity(oracle_mod, "llama3-70b", li, M)
+
+
+@pytest.mark.parametrize("M", [7, 600])
+def test_prepared_layer(oracle_mod, M):
+    """A layer through the offline preparation (smoothing, SVD split, Hadamard
+    Q, polar-form G) and then the library: parity with the oracle on the same
+    fp16 operands, and the migration-strength search runs on the GPU path."""
+    from paper_2606_01556_amd import prep
+    say(f"prepared layer M={M}")
+    rng = np.random.default_rng(M)
+    K, N, r = 256, 192, 32
+    weight = (rng.standard_t(4, size=(N, K)) * 0.02 / np.sqrt(2)).astype(np.float16)
+    X = rng.standard_normal((M, K))
+    X[:, [3, 77, 200]] *= 40
+    L = np.eye(r) + np.tril(rng.standard_normal((r, r)) * 0.1, -1)
+    P, _ = np.linalg.qr(rng.standard_normal((r, r)))
+    p = prep.prepare_layer(weight, r, np.abs(X).max(0), 0.5, prep.hadamard(K), prep.g_from_polar(P, L, 0.0))
+    xt = prep.transform_activations(X, p.lam, p.Q)
+    # the x40 outlier channels give outputs ~20x their rms
+    full_parity(oracle_mod, xt, p.w_res, p.l1, p.l2, wide_range=True)
+    if M == 7:
+        best, errs = prep.search_alpha(X, weight, r, alphas=(0.3, 0.5, 0.7))
+        assert best in errs and all(np.isfinite(v) for v in errs.values())
+        assert errs[best] == min(errs.values())
