@@ -11,7 +11,8 @@ calls read their weights from HBM rather than from the 256 MB last-level cache.
 
 Prints one JSON line: effective TFLOPS (2*M*N*K summed over the step / step
 time), per-M microseconds per layer next to an fp16 GEMM of the same shape
-(torch.matmul -> hipBLASLt), the roofline position of the dominant kernel
+(torch.matmul -> hipBLASLt) and next to the same layer without kernel fusion
+(tq_dual_gemm_unfused), the roofline position of the dominant kernel
 (tq_dual_gemm at M = 2048, timed with HIP events on its own stream) and the
 CPU oracle timed on the host as a reported baseline.
 """
@@ -205,6 +206,16 @@ def main():
             torch.matmul(X[m], wt)
         with torch.cuda.stream(stream):
             us_fp16 = timed(f16)
+        # the same layer without kernel fusion (quantizer, residual GEMM,
+        # stage 1 to global H, re-quantization, stage 2 added to Y)
+        scratch = tq.empty_unfused_scratch(desc, m, dev)
+
+        def unf():
+            p = copies[call[0] % ncopy]
+            call[0] += 1
+            tq.quant_act(X[m], xc, xs, stream=s)
+            tq.dual_gemm_unfused(desc, p, xc, xs, m, Y[m], scratch, stream=s)
+        us_unfused = timed(unf)
         per_m.append({
             "M": m, "us_layer": round(us_layer, 3), "us_dual_gemm": round(us_gemm, 3),
             "us_quant_act": round(us_quant, 3),
@@ -214,6 +225,8 @@ def main():
             "hbm_frac_gemm": round(alg_bytes(m) / us_gemm / 1e3 / HBM_PEAK_GBS, 3),
             "fp16_gemm_us": round(us_fp16, 3),
             "speedup_vs_fp16": round(us_fp16 / us_layer, 3),
+            "us_layer_unfused": round(us_unfused, 3),
+            "fusion_speedup": round(us_unfused / us_layer, 3),
         })
 
     flops_step = sum(2.0 * m * N * K for m in MS)

@@ -165,6 +165,27 @@ tq_status tq_dual_gemm_debug(const tq_weight_desc *d, const void *packed, const 
                              const void *x_scales, int m, void *y, tq_dtype y_dtype,
                              void *h, void *sh, void *qh, void *workspace, void *stream);
 
+/* The same layer without kernel fusion, the comparison baseline of the
+ * paper's kernel profile (Appendix, Kernel Profile; Sec. 4.3 names the
+ * intermediate traffic and launches that fusion removes): the residual 4-bit
+ * GEMM writes Y, a second kernel writes H to global memory, a third
+ * re-quantizes it to Q_H and s_H in global memory, and a fourth adds
+ * Q_H Q(L2) to Y -- four launches.  H, s_H and Q_H are bit-identical to the
+ * fused layer's; Y differs by the fp16 (bf16) rounding of the residual
+ * before the low-rank part is added.
+ *   scratch  device buffer of tq_unfused_scratch_bytes(d, m) bytes, owned by
+ *            the caller, 16-byte aligned, no initial contents needed; after
+ *            the call (r > 0) it holds, at 256-byte-aligned offsets in this
+ *            order: H fp32 [m32][r_pad32], Q_H fp8 code bytes (sign << 7 |
+ *            |q|) [m32][r_pad64], s_H fp32 [r/group_r][m32], with
+ *            r_pad32 / r_pad64 the rank rounded up to 32 / 64
+ *   other arguments as tq_dual_gemm
+ * Errors as tq_dual_gemm (TQ_ERR_NULL for a NULL scratch). */
+size_t tq_unfused_scratch_bytes(const tq_weight_desc *d, int m);
+tq_status tq_dual_gemm_unfused(const tq_weight_desc *d, const void *packed, const void *x_codes,
+                               const void *x_scales, int m, void *y, tq_dtype y_dtype,
+                               void *scratch, void *stream);
+
 /* Copy the packed weights out in the canonical layout (for tests/debug):
  *   w_codes  [n, k/8] TQ4 words      w_scales  [n, k/group] fp16
  *   l1_codes [r, k/8] TQ4 words (row j = column j of L1, along k)

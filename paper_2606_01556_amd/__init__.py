@@ -39,7 +39,7 @@ class WeightDesc(ctypes.Structure):
 
 EXPORTS = ("tq_weight_desc_init", "tq_pack_weights", "tq_quant_act", "tq_dual_gemm",
            "tq_dual_gemm_debug", "tq_export_weights", "tq_workspace_bytes", "tq_act_codes_bytes",
-           "tq_status_string")
+           "tq_unfused_scratch_bytes", "tq_dual_gemm_unfused", "tq_status_string")
 
 _lib = None
 
@@ -63,11 +63,15 @@ def lib() -> ctypes.CDLL:
         L.tq_workspace_bytes.restype = ctypes.c_size_t
         L.tq_act_codes_bytes.argtypes = [I, I]
         L.tq_act_codes_bytes.restype = ctypes.c_size_t
+        L.tq_unfused_scratch_bytes.argtypes = [D, I]
+        L.tq_unfused_scratch_bytes.restype = ctypes.c_size_t
+        L.tq_dual_gemm_unfused.argtypes = [D, P, P, P, I, P, I, P, P]
         L.tq_export_weights.argtypes = [D, P, P, P, P, P, P, P, P]
         L.tq_status_string.argtypes = [I]
         L.tq_status_string.restype = ctypes.c_char_p
         for name in EXPORTS:
-            if name not in ("tq_workspace_bytes", "tq_act_codes_bytes", "tq_status_string"):
+            if name not in ("tq_workspace_bytes", "tq_act_codes_bytes", "tq_unfused_scratch_bytes",
+                            "tq_status_string"):
                 getattr(L, name).restype = I
         _lib = L
     return _lib
@@ -123,6 +127,37 @@ def dual_gemm(desc: WeightDesc, packed, x_codes, x_scales, m: int, y, workspace,
     _check(lib().tq_dual_gemm(ctypes.byref(desc), _ptr(packed), _ptr(x_codes), _ptr(x_scales), m,
                               _ptr(y), TQ_BF16 if bf16 else TQ_F16, _ptr(workspace), _stream(stream)),
            "tq_dual_gemm")
+
+
+def unfused_scratch_bytes(desc: WeightDesc, m: int) -> int:
+    return int(lib().tq_unfused_scratch_bytes(ctypes.byref(desc), m))
+
+
+def empty_unfused_scratch(desc: WeightDesc, m: int, device="cuda"):
+    import torch
+    return torch.empty(unfused_scratch_bytes(desc, m), dtype=torch.uint8, device=device)
+
+
+def unfused_parts(desc: WeightDesc, m: int, scratch):
+    """Views of (H [m32, r_pad32] fp32, Q_H codes [m32, r_pad64] uint8, s_H
+    [r/group_r, m32] fp32) inside a tq_dual_gemm_unfused scratch buffer."""
+    import torch
+    m32 = padded_tokens(m)
+    up = lambda v: (v + 255) // 256 * 256
+    r, r32, r64, gr = desc.rank, desc.r_pad32, desc.r_pad64, desc.group_r
+    o1 = up(m32 * r32 * 4)
+    o2 = o1 + up(m32 * r64)
+    h = scratch[:m32 * r32 * 4].view(torch.float32).view(m32, r32)
+    qh = scratch[o1:o1 + m32 * r64].view(m32, r64)
+    sh = scratch[o2:o2 + (r // gr) * m32 * 4].view(torch.float32).view(r // gr, m32)
+    return h, qh, sh
+
+
+def dual_gemm_unfused(desc: WeightDesc, packed, x_codes, x_scales, m: int, y, scratch,
+                      bf16: bool = False, stream=None):
+    _check(lib().tq_dual_gemm_unfused(ctypes.byref(desc), _ptr(packed), _ptr(x_codes), _ptr(x_scales),
+                                      m, _ptr(y), TQ_BF16 if bf16 else TQ_F16, _ptr(scratch),
+                                      _stream(stream)), "tq_dual_gemm_unfused")
 
 
 def dual_gemm_debug(desc: WeightDesc, packed, x_codes, x_scales, m: int, y, h, sh, qh, workspace,

@@ -95,7 +95,8 @@ tq_status tq_quant_act(const void *x, int m, int k, int group, void *x_codes, vo
 
 static tq_status dual_gemm_impl(const tq_weight_desc *d, const void *packed, const void *x_codes,
                                 const void *x_scales, int m, void *y, tq_dtype y_dtype, void *h,
-                                void *sh, void *qh, void *workspace, void *stream) {
+                                void *sh, void *qh, void *workspace, void *stream,
+                                bool unfused = false) {
   if (d == nullptr || packed == nullptr || x_codes == nullptr || x_scales == nullptr ||
       y == nullptr || workspace == nullptr)
     return TQ_ERR_NULL;
@@ -120,6 +121,8 @@ static tq_status dual_gemm_impl(const tq_weight_desc *d, const void *packed, con
   a.dbg_sh = static_cast<float *>(sh);
   a.dbg_qh = static_cast<int8_t *>(qh);
   a.ws = static_cast<uint32_t *>(workspace);
+  if (unfused)
+    return hip_status(tq::launch_dual_gemm_unfused(a, workspace, static_cast<hipStream_t>(stream)));
   return hip_status(tq::launch_dual_gemm(a, static_cast<hipStream_t>(stream)));
 }
 
@@ -143,6 +146,18 @@ tq_status tq_dual_gemm_debug(const tq_weight_desc *d, const void *packed, const 
   if (h == nullptr || sh == nullptr || qh == nullptr) return TQ_ERR_NULL;
   if (d != nullptr && d->rank == 0) return TQ_ERR_RANK;
   return dual_gemm_impl(d, packed, x_codes, x_scales, m, y, y_dtype, h, sh, qh, workspace, stream);
+}
+
+size_t tq_unfused_scratch_bytes(const tq_weight_desc *d, int m) {
+  if (!desc_ok(d) || m < 0 || m > (1 << 24)) return 0;
+  return tq::unfused_scratch_bytes(m, geometry(d));
+}
+
+tq_status tq_dual_gemm_unfused(const tq_weight_desc *d, const void *packed, const void *x_codes,
+                               const void *x_scales, int m, void *y, tq_dtype y_dtype,
+                               void *scratch, void *stream) {
+  return dual_gemm_impl(d, packed, x_codes, x_scales, m, y, y_dtype, nullptr, nullptr, nullptr,
+                        scratch, stream, true);
 }
 
 tq_status tq_export_weights(const tq_weight_desc *d, const void *packed, void *w_codes,

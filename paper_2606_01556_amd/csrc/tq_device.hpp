@@ -68,6 +68,10 @@ __device__ __forceinline__ uint16_t float_to_half_bits(float f) {
   return __builtin_bit_cast(uint16_t, (_Float16)f);  // v_cvt_f16_f32, round to nearest even
 }
 
+__device__ __forceinline__ float bf16_bits_to_float(uint16_t b) {
+  return __builtin_bit_cast(float, (uint32_t)b << 16);
+}
+
 __device__ __forceinline__ uint16_t float_to_bf16_bits(float f) {
   uint32_t b = __builtin_bit_cast(uint32_t, f);
   b += 0x7fffu + ((b >> 16) & 1u);  // round to nearest even (finite inputs)

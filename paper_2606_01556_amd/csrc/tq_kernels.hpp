@@ -64,5 +64,9 @@ hipError_t launch_dual_gemm_decode(const GemmArgs &a, hipStream_t s);  // m <= 1
 hipError_t launch_dual_gemm_mid(const GemmArgs &a, hipStream_t s);      // mid sizes
 hipError_t launch_dual_gemm_prefill(const GemmArgs &a, hipStream_t s);  // prefill sizes
 hipError_t launch_dual_gemm_large(const GemmArgs &a, hipStream_t s);    // large token counts
+// the layer without fusion (comparison baseline): residual GEMM, stage 1 to
+// global H, re-quantization, stage 2 added to the residual output
+size_t unfused_scratch_bytes(int m, const Geometry &g);
+hipError_t launch_dual_gemm_unfused(const GemmArgs &a, void *scratch, hipStream_t s);
 
 }  // namespace tq

@@ -179,3 +179,20 @@ def test_act_codes_bytes(L):
     assert L.tq_act_codes_bytes(2048, 64) == 2048 * 64
     assert L.tq_act_codes_bytes(0, 4096) == 0
     assert L.tq_act_codes_bytes(16, 100) == 0 and L.tq_act_codes_bytes(-1, 64) == 0
+
+
+def test_unfused_sizes_and_validation(L):
+    """Scratch of the unfused layer: H fp32 [m32][r_pad32], Q_H [m32][r_pad64],
+    s_H [r/group_r][m32], each at a 256-byte-aligned offset; 0 for a bad
+    descriptor; argument errors as tq_dual_gemm."""
+    D = tq.WeightDesc
+    d = tq.weight_desc_init(4096, 4096, 64, 64)
+    up = lambda v: (v + 255) // 256 * 256
+    assert L.tq_unfused_scratch_bytes(ctypes.byref(d), 1) == up(32 * 64 * 4) + up(32 * 64) + up(32 * 4)
+    d8 = tq.weight_desc_init(512, 256, 8, 64)
+    assert L.tq_unfused_scratch_bytes(ctypes.byref(d8), 40) == up(64 * 32 * 4) + up(64 * 64) + up(64 * 4)
+    bad = D()
+    assert L.tq_unfused_scratch_bytes(ctypes.byref(bad), 16) == 0
+    assert L.tq_dual_gemm_unfused(ctypes.byref(d), FAKE, FAKE, FAKE, 1, FAKE, 0, None, None) == 1
+    assert L.tq_dual_gemm_unfused(ctypes.byref(d), FAKE, FAKE, FAKE, 1, FAKE, 0, FAKE + 4, None) == 6
+    assert L.tq_dual_gemm_unfused(ctypes.byref(d), FAKE, FAKE, FAKE, 0, FAKE, 0, FAKE, None) == 0

@@ -400,3 +400,36 @@ def test_prepared_layer(oracle_mod, M):
         best, errs = prep.search_alpha(X, weight, r, alphas=(0.3, 0.5, 0.7))
         assert best in errs and all(np.isfinite(v) for v in errs.values())
         assert errs[best] == min(errs.values())
+
+
+@pytest.mark.parametrize("M,K,N,r", [(1, 256, 96, 64), (16, 320, 4096, 128), (100, 192, 520, 16),
+                                     (600, 576, 1000, 64), (40, 128, 64, 0), (530, 256, 300, 8)])
+def test_unfused_baseline(oracle_mod, M, K, N, r):
+    """The layer without fusion: H, s_H and Q_H read back from its scratch
+    are bit-identical to the oracle's, and Y is within the tolerance (its
+    residual is rounded to fp16 once more than the fused layer's)."""
+    say(f"unfused M={M} K={K} N={N} r={r}")
+    d = random_codes_layer(M, K, N, r, seed=M + K + N + r + 11)
+    X, W, L1, L2 = d["X"], d["W_res"], d["L1"], d["L2"]
+    lay = tq.Layer(dev(W), None if L1 is None else dev(L1), None if L2 is None else dev(L2))
+    xc, xs = tq.empty_act(M, K)
+    tq.quant_act(dev(X), xc, xs)
+    y = torch.empty((M, N), dtype=torch.float16, device="cuda")
+    scratch = tq.empty_unfused_scratch(lay.desc, M)
+    tq.dual_gemm_unfused(lay.desc, lay.packed, xc, xs, M, y, scratch)
+    yf = torch.empty_like(y)
+    tq.dual_gemm(lay.desc, lay.packed, xc, xs, M, yf, lay.workspace)
+    torch.cuda.synchronize()
+    o = oracle_mod.layer(X, W, L1, L2, GROUP)
+    if r:
+        h, qh, sh = (t.cpu().numpy() for t in tq.unfused_parts(lay.desc, M, scratch))
+        np.testing.assert_array_equal(h[:M, :r].view(np.uint32), o["H"].view(np.uint32))
+        np.testing.assert_array_equal(sh[:, :M].T.view(np.uint32), o["sH"].view(np.uint32))
+        np.testing.assert_array_equal(tq.fp8_code_decode(qh[:M, :r]), o["qH"])
+        assert np.all(qh[:M, r:] == 0)
+    Y = y.cpu().numpy()
+    check_tolerance(Y, o["Y64"])
+    # close to the fused layer (the extra rounding is of Y_res, not of Y, so
+    # elementwise it is not relative to Y where the two branches cancel)
+    Yf = yf.cpu().numpy().astype(np.float64)
+    assert np.linalg.norm(Y.astype(np.float64) - Yf) <= 1e-3 * np.linalg.norm(Yf)
