@@ -94,6 +94,91 @@ def cpu_baseline(data):
                       f"{dt:.1f} s on the host, weight quantization included in each call"}
 
 
+def config_sweep():
+    """Every layer and token count of the four GPU-sized workload configs
+    (LLaMA3-8B q/o and MLP, Qwen3-8B with its rank sweep, LLaMA3-70B on one
+    GPU): per call, the layer (tq_quant_act + tq_dual_gemm), the fused kernel
+    alone and an fp16 hipBLASLt GEMM of the same shape, each with HIP events
+    on the launch stream over rotated weight copies (>= 1 GiB), and the
+    kernel's roofline fraction (HBM bytes for M <= 16, fp8 matrix-core ops
+    otherwise).  Random-init weights of the layer shapes.  Prints a markdown
+    table."""
+    import torch
+    import paper_2606_01556_amd as tq
+    from tq_synth import WORKLOADS
+
+    dev = torch.device("cuda")
+    stream = torch.cuda.Stream()
+    s = stream.cuda_stream
+    torch.manual_seed(0)
+    print("| config | layer K→N | r | M | layer µs | tq_dual_gemm µs | roofline | fp16 GEMM µs | "
+          "speedup vs fp16 |")
+    print("|---|---|---|---|---|---|---|---|---|")
+    for name in ("llama3-8b-qo", "llama3-8b-mlp", "qwen3-8b", "llama3-70b"):
+        wl = WORKLOADS[name]
+        for layer in wl.layers:
+            Kl, Nl, rl = layer.K, layer.N, layer.r
+            with torch.cuda.stream(stream):
+                W = (torch.randn(Nl, Kl, device=dev) * 0.02).half()
+                L1 = (torch.randn(Kl, rl, device=dev) * 0.05).half()
+                L2 = (torch.randn(rl, Nl, device=dev) * 0.05).half()
+                lay = tq.Layer(W, L1, L2, stream=stream)
+                del L1, L2
+                ncopy = max(2, int(np.ceil(ROTATE_BYTES / lay.desc.packed_bytes)))
+                copies = [lay.packed] + [lay.packed.clone() for _ in range(ncopy - 1)]
+                WT = W.t().contiguous()
+                del W
+                nwt = max(2, int(np.ceil(ROTATE_BYTES / (WT.numel() * 2))))
+                WTs = [WT] + [WT.clone() for _ in range(nwt - 1)]
+            torch.cuda.synchronize()
+            call = [0]
+            for m in wl.Ms:
+                with torch.cuda.stream(stream):
+                    X = torch.randn(m, Kl, device=dev).half()
+                    xc, xs = tq.empty_act(m, Kl, dev)
+                    Y = torch.empty((m, Nl), dtype=torch.float16, device=dev)
+                reps = 20 if m <= 256 else 5
+
+                def timed(fn):
+                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    for _ in range(2):
+                        fn()
+                    e0.record(stream)
+                    for _ in range(reps):
+                        fn()
+                    e1.record(stream)
+                    torch.cuda.synchronize()
+                    return 1e3 * e0.elapsed_time(e1) / reps
+
+                def gemm():
+                    p = copies[call[0] % ncopy]
+                    call[0] += 1
+                    tq.dual_gemm(lay.desc, p, xc, xs, m, Y, lay.workspace, stream=s)
+
+                def layer_call():
+                    tq.quant_act(X, xc, xs, stream=s)
+                    gemm()
+
+                def f16():
+                    wt = WTs[call[0] % nwt]
+                    call[0] += 1
+                    torch.matmul(X, wt)
+
+                us_layer = timed(layer_call)
+                us_gemm = timed(gemm)
+                with torch.cuda.stream(stream):
+                    us_fp16 = timed(f16)
+                if m <= 16:
+                    roof = f"{alg_bytes(m, Nl, Kl, rl) / us_gemm / 1e3 / HBM_PEAK_GBS * 100:.1f} % HBM"
+                else:
+                    roof = f"{alg_ops(m, Nl, Kl, rl) / us_gemm / 1e6 / FP8_MFMA_PEAK_TFLOPS * 100:.1f} % fp8"
+                print(f"| {name} | {layer.name} {Kl}→{Nl} | {rl} | {m} | {us_layer:.1f} | {us_gemm:.1f} | "
+                      f"{roof} | {us_fp16:.1f} | {us_fp16 / us_layer:.2f} |", flush=True)
+                del X, xc, xs, Y
+            del lay, copies, WT, WTs
+            torch.cuda.empty_cache()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -101,6 +186,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-detail", action="store_true", help="skip the per-M detail")
+    ap.add_argument("--configs", action="store_true",
+                    help="time every layer and token count of the workload configs and print a "
+                         "markdown table instead of the benchmark line")
     ap.add_argument("--calib-copy", action="store_true",
                     help="run one plain 256 MiB device copy first (calibrates the HBM "
                          "byte counters of a profiler run)")
@@ -109,6 +197,9 @@ def main():
         print("bench.py measures one GPU only: the layer runs on a single MI355X "
               "(multi-GPU sharding is a design note, not built)", file=sys.stderr)
         sys.exit(2)
+    if args.configs:
+        config_sweep()
+        return
 
     import torch
     import paper_2606_01556_amd as tq
