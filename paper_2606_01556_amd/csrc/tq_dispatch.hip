@@ -21,6 +21,7 @@ hipError_t launch_dual_gemm(const GemmArgs &a, hipStream_t s) {
   // run of column blocks
   const int blocks = (a.m + 127) / 128 * ((a.geo.n_pad + 255) / 256);
   int large = blocks <= 256 || a.geo.r_pad32 <= 64;
+  // TQ_LARGE=0|1 forces either kernel (the tests run both on the same shapes)
   if (const char *lenv = getenv("TQ_LARGE")) large = atoi(lenv);
   if (large) return launch_dual_gemm_large(a, s);
   return launch_dual_gemm_prefill(a, s);

@@ -555,8 +555,7 @@ hipError_t launch_dual_gemm_decode(const GemmArgs &a, hipStream_t s) {
   // two 16-column tiles per work-group once one tile per work-group would
   // take more than about two rounds of the 256 CUs
   const int tiles16 = a.geo.n_pad / 16;
-  int ct = tiles16 > 2 * 256 ? 2 : 1;
-  if (const char *env = getenv("TQ_DECODE_CT")) ct = atoi(env) == 2 ? 2 : 1;
+  const int ct = tiles16 > 2 * 256 ? 2 : 1;
   return ct == 2 ? launch_decode<2>(a, s) : launch_decode<1>(a, s);
 }
 

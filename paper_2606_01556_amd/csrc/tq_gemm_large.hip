@@ -432,10 +432,7 @@ hipError_t launch_large(const GemmArgs &a, hipStream_t s) {
   using C = LCfg<RT>;
   const int m_tiles = (a.m + LBM - 1) / LBM;
   const int n_tiles = (a.geo.n_pad + LBN - 1) / LBN;
-  int band = 8;
-  if (const char *env = getenv("TQ_LARGE_BAND")) band = atoi(env);
-  if (band < 1) band = 1;
-  if (band > m_tiles) band = m_tiles;
+  const int band = m_tiles < 8 ? m_tiles : 8;   // token blocks per band of the XCD order
   auto kern = dual_gemm_large_kernel<RT>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);

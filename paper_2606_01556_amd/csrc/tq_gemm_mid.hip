@@ -564,6 +564,7 @@ hipError_t launch_dual_gemm_mid(const GemmArgs &a, hipStream_t s) {
   int ct = 1;
   for (int c : {2, 4})
     if (mid_cost(rt, c, n_rb, ct32) < mid_cost(rt, ct, n_rb, ct32)) ct = c;
+  // TQ_MID_CT=1|2|4 forces the tile count (the tests run all three)
   if (const char *env = getenv("TQ_MID_CT")) ct = atoi(env);
   if (ct == 1) return launch_mid_rt<1>(a, s);
   return ct == 4 ? launch_mid_rt<4>(a, s) : launch_mid_rt<2>(a, s);

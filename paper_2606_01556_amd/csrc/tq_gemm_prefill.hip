@@ -34,7 +34,6 @@
 // product -- exactly I * s_x * s_w -- to the fp32 accumulator in ascending
 // group order, the oracle's order for H and for the residual, so Y is
 // bit-identical to the oracle's rounded result.
-#include <stdio.h>
 #include <stdlib.h>
 
 #include <type_traits>
@@ -644,16 +643,11 @@ hipError_t launch_prefill(const GemmArgs &a, hipStream_t s) {
   using C = PCfg<RT, D>;
   const int m_tiles = (a.m + PBM - 1) / PBM;
   const int n_tiles = (a.geo.n_pad + PBN - 1) / PBN;
-  int cpw = 0, band = 0;
-  if (const char *env = getenv("TQ_PREFILL")) sscanf(env, "%d:%d", &cpw, &band);
-  if (cpw <= 0) {
-    cpw = (m_tiles * n_tiles) / 256;
-    if (cpw < 1) cpw = 1;
-  }
+  int cpw = (m_tiles * n_tiles) / 256;   // column blocks per work-group: about one round
+  if (cpw < 1) cpw = 1;
   if (cpw > n_tiles) cpw = n_tiles;
   const int n_chunks = (n_tiles + cpw - 1) / cpw;
-  if (band <= 0) band = 8;
-  if (band > m_tiles) band = m_tiles;
+  const int band = m_tiles < 8 ? m_tiles : 8;   // token blocks per band of the XCD order
   auto kern = dual_gemm_prefill_kernel<RT, D>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
@@ -677,10 +671,6 @@ hipError_t launch_prefill_rt(const GemmArgs &a, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_dual_gemm_prefill(const GemmArgs &a, hipStream_t s) {
-  // ring depth override for tuning sweeps: TQ_PREFILL_D=5|6
-  const char *env = getenv("TQ_PREFILL_D");
-  const int d = env ? atoi(env) : 6;
-  if (d == 5) return launch_prefill_rt<5>(a, s);
   return launch_prefill_rt<6>(a, s);
 }
 
