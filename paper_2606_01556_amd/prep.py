@@ -11,16 +11,16 @@ operands that tq_pack_weights quantizes:
    lam_i = max|X[:, i]|^alpha / max|W[i, :]|^(1 - alpha);
 2. the low-rank / residual split of W^ (Sec. 2, "Low-Rank Decomposition"):
    W^ = U V + R, U [K, r] and V [r, N] from a rank-r truncated SVD;
-3. the transforms of the re-parameterization (Sec. 3.1): a global orthogonal
+3. the transforms of the re-parameterization (Sec. 4.1): a global orthogonal
    Q [K, K] applied to the activation (X^ Q) and a layer-specific invertible
    G [r, r], folded into the weights as U' = Q^-1 U G, V' = G^-1 V and
    R' = Q^-1 R.  In full precision (X^ Q)(U' V' + R') = X W exactly.
 
 The kernel then computes Q(X^ Q) [Q(U') Q(V') + Q(R')]: L1 = U', L2 = V' and
-W_res = R'^T.  Learning Q and G (Sec. 3.2) is outside this module; it takes
+W_res = R'^T.  Learning Q and G (Sec. 4.2) is outside this module; it takes
 them as given, e.g. from ``hadamard`` (the fixed-rotation variant of the
-ablation study, Sec. 5) or ``g_from_polar`` (the polar form G = P S,
-S = e^gamma L L^T, of Sec. 3.2).
+ablation study, Sec. 5.5) or ``g_from_polar`` (the polar form G = P S,
+S = e^gamma L L^T, of Sec. 4.2).
 
 Everything here runs on the host in float64 except ``search_alpha``, which
 measures each candidate through the library's fused layer on the GPU.
@@ -66,7 +66,7 @@ def hadamard(n: int) -> np.ndarray:
 
 
 def g_from_polar(P, L, gamma: float) -> np.ndarray:
-    """G = P S with S = e^gamma L L^T (Sec. 3.2, Eq. polar): P orthogonal, L
+    """G = P S with S = e^gamma L L^T (Sec. 4.2, Eq. polar): P orthogonal, L
     lower triangular with a non-zero diagonal, so G is invertible."""
     P = np.asarray(P, np.float64)
     L = np.tril(np.asarray(L, np.float64))
@@ -94,7 +94,7 @@ def svd_split(w_hat, rank: int):
 
 
 def fold_transforms(U, V, R, Q=None, G=None, tol: float = 1e-8):
-    """Fold the transforms into the weights (Sec. 3.1): U' = Q^-1 U G,
+    """Fold the transforms into the weights (Sec. 4.1): U' = Q^-1 U G,
     V' = G^-1 V, R' = Q^-1 R, with Q^-1 = Q^T for the orthogonal Q.  None
     stands for the identity.  Raises ValueError for a Q that is not
     orthogonal to within tol (relative) or a G that is singular or

@@ -1,6 +1,6 @@
 """Offline weight preparation (smoothing, SVD split, transform folding),
 pinned in float64 against closed forms and the exact equivalence the
-re-parameterization preserves (Sec. 2 and Sec. 3.1)."""
+re-parameterization preserves (Sec. 2 and Sec. 4.1)."""
 import numpy as np
 import pytest
 
