@@ -433,3 +433,32 @@ def test_unfused_baseline(oracle_mod, M, K, N, r):
     # elementwise it is not relative to Y where the two branches cancel)
     Yf = yf.cpu().numpy().astype(np.float64)
     assert np.linalg.norm(Y.astype(np.float64) - Yf) <= 1e-3 * np.linalg.norm(Yf)
+
+
+@pytest.mark.parametrize("M", [512, 513])
+def test_activation_format_boundary(oracle_mod, M):
+    """The activation codes switch from TQ4 nibbles (m <= 512, mid kernel) to
+    fp8 bytes (m > 512, large and prefill kernels) between these two sizes:
+    buffer size, codes and the layer agree with the oracle on both sides."""
+    say(f"format boundary M={M}")
+    K = 192
+    assert tq.act_codes_bytes(M, K) == (tq.padded_tokens(M) * K // (2 if M <= 512 else 1))
+    d = random_codes_layer(M, K, 160, 32, seed=M)
+    full_parity(oracle_mod, d["X"], d["W_res"], d["L1"], d["L2"])
+
+
+def test_unfused_bf16(oracle_mod):
+    """The layer without fusion with a bf16 output: the residual is rounded
+    to bf16 before the low-rank part is added."""
+    say("unfused bf16")
+    M, K, N, r = 24, 256, 200, 64
+    d = random_codes_layer(M, K, N, r, seed=99)
+    lay = tq.Layer(dev(d["W_res"]), dev(d["L1"]), dev(d["L2"]))
+    xc, xs = tq.empty_act(M, K)
+    tq.quant_act(dev(d["X"]), xc, xs)
+    y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    scratch = tq.empty_unfused_scratch(lay.desc, M)
+    tq.dual_gemm_unfused(lay.desc, lay.packed, xc, xs, M, y, scratch, bf16=True)
+    torch.cuda.synchronize()
+    o = oracle_mod.layer(d["X"], d["W_res"], d["L1"], d["L2"], GROUP)
+    check_tolerance(y.float().cpu().numpy(), o["Y64"], bf16=True)
