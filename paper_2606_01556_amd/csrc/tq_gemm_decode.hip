@@ -552,10 +552,14 @@ hipError_t launch_decode(const GemmArgs &a, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_dual_gemm_decode(const GemmArgs &a, hipStream_t s) {
-  // two 16-column tiles per work-group once one tile per work-group would
-  // take more than about two rounds of the 256 CUs
+  // two 16-column tiles per work-group once one tile per work-group would not
+  // fit one round of resident work-groups (two per CU, 512 on the 256 CUs),
+  // the H producers included: a second round for a few work-groups costs a
+  // whole work-group's time (measured at N = 8192, r = 128, K = 28672: 68 us
+  // with 520 work-groups, 47 us with 264)
   const int tiles16 = a.geo.n_pad / 16;
-  const int ct = tiles16 > 2 * 256 ? 2 : 1;
+  const int nprod = (a.geo.r + 15) / 16;
+  const int ct = tiles16 + nprod > 2 * 256 ? 2 : 1;
   return ct == 2 ? launch_decode<2>(a, s) : launch_decode<1>(a, s);
 }
 
