@@ -462,3 +462,36 @@ def test_unfused_bf16(oracle_mod):
     torch.cuda.synchronize()
     o = oracle_mod.layer(d["X"], d["W_res"], d["L1"], d["L2"], GROUP)
     check_tolerance(y.float().cpu().numpy(), o["Y64"], bf16=True)
+
+
+def test_unfused_graph_replay(oracle_mod):
+    """The layer without fusion captured in a HIP graph (its four launches and
+    the quantizer) and replayed three times, with eager work between the
+    replays: every replay equals the eager result bit for bit."""
+    say("unfused graph replay")
+    M, K, N, r = 12, 320, 640, 64
+    d = random_codes_layer(M, K, N, r, seed=5)
+    lay = tq.Layer(dev(d["W_res"]), dev(d["L1"]), dev(d["L2"]))
+    x = dev(d["X"])
+    xc, xs = tq.empty_act(M, K)
+    scratch = tq.empty_unfused_scratch(lay.desc, M)
+    y_eager = torch.empty((M, N), dtype=torch.float16, device="cuda")
+    tq.quant_act(x, xc, xs)
+    tq.dual_gemm_unfused(lay.desc, lay.packed, xc, xs, M, y_eager, scratch)
+    torch.cuda.synchronize()
+    y = torch.empty_like(y_eager)
+    st = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(st):
+        g.capture_begin()
+        tq.quant_act(x, xc, xs, stream=st)
+        tq.dual_gemm_unfused(lay.desc, lay.packed, xc, xs, M, y, scratch, stream=st)
+        g.capture_end()
+    torch.cuda.synchronize()
+    for _ in range(3):
+        y.zero_()
+        scratch.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y.view(torch.int16), y_eager.view(torch.int16))
