@@ -179,6 +179,62 @@ def config_sweep():
             torch.cuda.empty_cache()
 
 
+def rank_overhead():
+    """tq_dual_gemm at ranks 0, 32, 64 and 128 on the LLaMA3-8B q_proj and
+    gate_up shapes: the latency the low-rank branch adds to the plain 4-bit
+    layer (r = 0) at the same shape.  HIP events, rotated weight copies,
+    random-init weights.  Prints a markdown table."""
+    import torch
+    import paper_2606_01556_amd as tq
+
+    dev = torch.device("cuda")
+    stream = torch.cuda.Stream()
+    s = stream.cuda_stream
+    torch.manual_seed(0)
+    print("| layer K→N | M | r = 0 µs | r = 32 | r = 64 | r = 128 |")
+    print("|---|---|---|---|---|---|")
+    for name, Kl, Nl in (("q_proj", 4096, 4096), ("gate_up", 4096, 14336)):
+        with torch.cuda.stream(stream):
+            W = (torch.randn(Nl, Kl, device=dev) * 0.02).half()
+        res = {}
+        for rl in (0, 32, 64, 128):
+            with torch.cuda.stream(stream):
+                L1 = (torch.randn(Kl, rl, device=dev) * 0.05).half() if rl else None
+                L2 = (torch.randn(rl, Nl, device=dev) * 0.05).half() if rl else None
+                lay = tq.Layer(W, L1, L2, stream=stream)
+                ncopy = max(2, int(np.ceil(ROTATE_BYTES / lay.desc.packed_bytes)))
+                copies = [lay.packed] + [lay.packed.clone() for _ in range(ncopy - 1)]
+            torch.cuda.synchronize()
+            call = [0]
+            for m in (1, 16, 128, 2048):
+                with torch.cuda.stream(stream):
+                    X = torch.randn(m, Kl, device=dev).half()
+                    xc, xs = tq.empty_act(m, Kl, dev)
+                    Y = torch.empty((m, Nl), dtype=torch.float16, device=dev)
+                    tq.quant_act(X, xc, xs, stream=s)
+
+                def gemm():
+                    p = copies[call[0] % ncopy]
+                    call[0] += 1
+                    tq.dual_gemm(lay.desc, p, xc, xs, m, Y, lay.workspace, stream=s)
+                for _ in range(3):
+                    gemm()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                for _ in range(30):
+                    gemm()
+                e1.record(stream)
+                torch.cuda.synchronize()
+                res[(rl, m)] = 1e3 * e0.elapsed_time(e1) / 30
+            del lay, copies
+            torch.cuda.empty_cache()
+        for m in (1, 16, 128, 2048):
+            base = res[(0, m)]
+            cells = " | ".join(f"{res[(r, m)]:.1f} (+{(res[(r, m)] / base - 1) * 100:.0f} %)"
+                               for r in (32, 64, 128))
+            print(f"| {name} {Kl}→{Nl} | {m} | {base:.1f} | {cells} |", flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -189,6 +245,9 @@ def main():
     ap.add_argument("--configs", action="store_true",
                     help="time every layer and token count of the workload configs and print a "
                          "markdown table instead of the benchmark line")
+    ap.add_argument("--ranks", action="store_true",
+                    help="time the fused layer at ranks 0/32/64/128 and print the low-rank "
+                         "branch's overhead as a markdown table")
     ap.add_argument("--calib-copy", action="store_true",
                     help="run one plain 256 MiB device copy first (calibrates the HBM "
                          "byte counters of a profiler run)")
@@ -199,6 +258,9 @@ def main():
         sys.exit(2)
     if args.configs:
         config_sweep()
+        return
+    if args.ranks:
+        rank_overhead()
         return
 
     import torch

@@ -643,8 +643,11 @@ hipError_t launch_prefill(const GemmArgs &a, hipStream_t s) {
   using C = PCfg<RT, D>;
   const int m_tiles = (a.m + PBM - 1) / PBM;
   const int n_tiles = (a.geo.n_pad + PBN - 1) / PBN;
-  int cpw = (m_tiles * n_tiles) / 256;   // column blocks per work-group: about one round
-  if (cpw < 1) cpw = 1;
+  // column blocks per work-group: the fewest that fit the grid in one round
+  // over the 256 CUs (one work-group per CU), so no second round runs a few
+  // leftover work-groups alone (m_tiles > 256: one run of all column blocks)
+  const int runs = m_tiles >= 256 ? 1 : 256 / m_tiles;
+  int cpw = (n_tiles + runs - 1) / runs;
   if (cpw > n_tiles) cpw = n_tiles;
   const int n_chunks = (n_tiles + cpw - 1) / cpw;
   const int band = m_tiles < 8 ? m_tiles : 8;   // token blocks per band of the XCD order
