@@ -235,6 +235,74 @@ def rank_overhead():
             print(f"| {name} {Kl}→{Nl} | {m} | {base:.1f} | {cells} |", flush=True)
 
 
+def kernel_choice():
+    """Past 512 tokens tq_dual_gemm picks the large kernel (128 x 256 blocks),
+    the prefill kernel (r > 64 beyond one round of blocks) or the mid kernel
+    (32-token blocks, where the large blocks would leave most CUs idle).  Times
+    each of them, forced through the library's TQ_LARGE / TQ_MID hooks, beside
+    the one it picks, on LLaMA3 layer shapes (HIP events, rotated weight
+    copies, random-init weights).  Prints a markdown table."""
+    import torch
+    import paper_2606_01556_amd as tq
+
+    dev = torch.device("cuda")
+    stream = torch.cuda.Stream()
+    s = stream.cuda_stream
+    torch.manual_seed(0)
+    forced = (("large", {"TQ_LARGE": "1"}), ("prefill", {"TQ_LARGE": "0"}), ("mid", {"TQ_MID": "1"}))
+    print("| layer K→N | r | M | picked | large µs | prefill µs | mid µs | picked / fastest |")
+    print("|---|---|---|---|---|---|---|---|")
+    shapes = (("k/v_proj 8B", 4096, 1024), ("q/o_proj 8B", 4096, 4096), ("gate_up 8B", 4096, 14336),
+              ("down 8B", 14336, 4096), ("k/v_proj 70B", 8192, 1024))
+    for name, Kl, Nl in shapes:
+        with torch.cuda.stream(stream):
+            W = (torch.randn(Nl, Kl, device=dev) * 0.02).half()
+        for rl in (64, 128):
+            with torch.cuda.stream(stream):
+                L1 = (torch.randn(Kl, rl, device=dev) * 0.05).half()
+                L2 = (torch.randn(rl, Nl, device=dev) * 0.05).half()
+                lay = tq.Layer(W, L1, L2, stream=stream)
+                ncopy = max(2, int(np.ceil(ROTATE_BYTES / lay.desc.packed_bytes)))
+                copies = [lay.packed] + [lay.packed.clone() for _ in range(ncopy - 1)]
+            torch.cuda.synchronize()
+            call = [0]
+            for m in (576, 1024, 2048, 4096):
+                with torch.cuda.stream(stream):
+                    X = torch.randn(m, Kl, device=dev).half()
+                    xc, xs = tq.empty_act(m, Kl, dev)
+                    Y = torch.empty((m, Nl), dtype=torch.float16, device=dev)
+                    tq.quant_act(X, xc, xs, stream=s)
+
+                def gemm():
+                    p = copies[call[0] % ncopy]
+                    call[0] += 1
+                    tq.dual_gemm(lay.desc, p, xc, xs, m, Y, lay.workspace, stream=s)
+                picked = tq.dual_gemm_kernel(lay.desc, m)
+                res = {}
+                for kname, env in forced:
+                    if kname == "prefill" and rl <= 64:
+                        continue              # the prefill kernel serves r > 64 only
+                    os.environ.update(env)
+                    try:
+                        for _ in range(3):
+                            gemm()
+                        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                        e0.record(stream)
+                        for _ in range(20):
+                            gemm()
+                        e1.record(stream)
+                        torch.cuda.synchronize()
+                    finally:
+                        for k in env:
+                            del os.environ[k]
+                    res[kname] = 1e3 * e0.elapsed_time(e1) / 20
+                cell = lambda k: f"{res[k]:.1f}" if k in res else "–"
+                print(f"| {name} {Kl}→{Nl} | {rl} | {m} | {picked} | {cell('large')} | {cell('prefill')} | "
+                      f"{cell('mid')} | {res[picked] / min(res.values()):.2f} |", flush=True)
+            del lay, copies
+            torch.cuda.empty_cache()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -248,6 +316,9 @@ def main():
     ap.add_argument("--ranks", action="store_true",
                     help="time the fused layer at ranks 0/32/64/128 and print the low-rank "
                          "branch's overhead as a markdown table")
+    ap.add_argument("--kernel-choice", action="store_true",
+                    help="time the large, prefill and mid kernels past 512 tokens beside the "
+                         "one the library picks, as a markdown table")
     ap.add_argument("--calib-copy", action="store_true",
                     help="run one plain 256 MiB device copy first (calibrates the HBM "
                          "byte counters of a profiler run)")
@@ -261,6 +332,11 @@ def main():
         return
     if args.ranks:
         rank_overhead()
+        return
+    if args.kernel_choice:
+        for k in ("TQ_LARGE", "TQ_MID", "TQ_MID_CT"):
+            os.environ.pop(k, None)
+        kernel_choice()
         return
 
     import torch

@@ -155,6 +155,24 @@ tq_status tq_dual_gemm(const tq_weight_desc *d, const void *packed, const void *
                        const void *x_scales, int m, void *y, tq_dtype y_dtype, void *workspace,
                        void *stream);
 
+/* Kernels of tq_dual_gemm. */
+typedef enum {
+  TQ_KERNEL_DECODE = 0,   /* m <= 16: weight-streaming, H handed over in the workspace */
+  TQ_KERNEL_MID = 1,      /* 32-token blocks, K split over wavefronts */
+  TQ_KERNEL_LARGE = 2,    /* 128 x 256 blocks, H in the main loop */
+  TQ_KERNEL_PREFILL = 3   /* 128 x 256 blocks, H in a separate pass */
+} tq_kernel;
+
+/* The kernel tq_dual_gemm launches for descriptor d and m tokens (a tq_kernel
+ * value), or -1 for a NULL or invalid descriptor or m outside [1, 2^24].
+ * Host-only; launches nothing.  Every kernel returns the same codes, H, s_H
+ * and Q_H; the large and prefill kernels also sum each output in the order of
+ * the fp64 definition's fp32 evaluation (ascending K-groups, then the
+ * low-rank term), while the decode and mid kernels add partial sums over
+ * parts of K, so their Y can differ from it in the last bits (within the
+ * tolerance the fp32 accumulation allows). */
+int tq_dual_gemm_kernel(const tq_weight_desc *d, int m);
+
 /* Same computation and kernel as tq_dual_gemm, for tests: additionally
  * copies the low-rank intermediate of every token out of the kernel.
  *   h   [m,r] fp32     H before re-quantization

@@ -39,7 +39,8 @@ class WeightDesc(ctypes.Structure):
 
 EXPORTS = ("tq_weight_desc_init", "tq_pack_weights", "tq_quant_act", "tq_dual_gemm",
            "tq_dual_gemm_debug", "tq_export_weights", "tq_workspace_bytes", "tq_act_codes_bytes",
-           "tq_unfused_scratch_bytes", "tq_dual_gemm_unfused", "tq_status_string")
+           "tq_unfused_scratch_bytes", "tq_dual_gemm_unfused", "tq_dual_gemm_kernel",
+           "tq_status_string")
 
 _lib = None
 
@@ -63,6 +64,8 @@ def lib() -> ctypes.CDLL:
         L.tq_workspace_bytes.restype = ctypes.c_size_t
         L.tq_act_codes_bytes.argtypes = [I, I]
         L.tq_act_codes_bytes.restype = ctypes.c_size_t
+        L.tq_dual_gemm_kernel.argtypes = [D, I]
+        L.tq_dual_gemm_kernel.restype = I
         L.tq_unfused_scratch_bytes.argtypes = [D, I]
         L.tq_unfused_scratch_bytes.restype = ctypes.c_size_t
         L.tq_dual_gemm_unfused.argtypes = [D, P, P, P, I, P, I, P, P]
@@ -71,7 +74,7 @@ def lib() -> ctypes.CDLL:
         L.tq_status_string.restype = ctypes.c_char_p
         for name in EXPORTS:
             if name not in ("tq_workspace_bytes", "tq_act_codes_bytes", "tq_unfused_scratch_bytes",
-                            "tq_status_string"):
+                            "tq_dual_gemm_kernel", "tq_status_string"):
                 getattr(L, name).restype = I
         _lib = L
     return _lib
@@ -189,6 +192,18 @@ def empty_workspace(device="cuda"):
 def padded_tokens(m: int) -> int:
     """m32: the token count rounded up to the 32-token activation tile (at least 32)."""
     return max((m + 31) // 32 * 32, 32)
+
+
+KERNEL_NAMES = ("decode", "mid", "large", "prefill")
+
+
+def dual_gemm_kernel(desc: WeightDesc, m: int) -> str:
+    """Name of the kernel tq_dual_gemm launches for this layer and m tokens
+    (tq_dual_gemm_kernel); raises ValueError for an invalid descriptor or m."""
+    k = int(lib().tq_dual_gemm_kernel(ctypes.byref(desc), m))
+    if k < 0:
+        raise ValueError(f"tq_dual_gemm_kernel: invalid descriptor or m = {m}")
+    return KERNEL_NAMES[k]
 
 
 def act_codes_bytes(m: int, k: int) -> int:

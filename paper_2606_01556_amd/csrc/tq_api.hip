@@ -128,6 +128,15 @@ static tq_status dual_gemm_impl(const tq_weight_desc *d, const void *packed, con
 
 size_t tq_workspace_bytes(void) { return tq::kWorkspaceBytes; }
 
+int tq_dual_gemm_kernel(const tq_weight_desc *d, int m) {
+  if (d == nullptr || !desc_ok(d) || m < 1 || m > (1 << 24)) return -1;
+  tq::GemmArgs a{};
+  a.geo = geometry(d);
+  a.m = m;
+  a.ms = (m + 31) / 32 * 32;
+  return tq::choose_kernel(a);
+}
+
 size_t tq_act_codes_bytes(int m, int k) {
   if (m < 0 || m > 65535 * 32 || k < 1 || k > (1 << 24) || k % 64 != 0) return 0;
   return tq::act_codes_bytes(m, k);

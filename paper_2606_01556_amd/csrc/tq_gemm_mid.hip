@@ -27,6 +27,11 @@
 // wait is one constant s_waitcnt.  One chunk ahead, the two least-loaded wavefronts expand the
 // activation codes to fp8 operand bytes, shared by all eight wavefronts.  One
 // workgroup barrier per chunk.
+//
+// Above 512 tokens the activation codes arrive as fp8 operand bytes (two
+// 1 KiB halves per group): each wavefront then issues two shared loads per
+// chunk, and the operands are read from the chunk slot as loaded, with no
+// expansion.
 #include <stdlib.h>
 
 #include <type_traits>
@@ -44,28 +49,37 @@ constexpr int MW = 8;                  // wavefronts per workgroup
 constexpr int MCG = 4;                 // K-groups per chunk
 constexpr int M_LDS = 160 * 1024;      // LDS of a CU
 
-template <int RT, int CT>
+template <int RT, int CT, bool FP8>
 struct MCfg {
   static constexpr int NRW = MW - RT;                  // residual wavefronts
   static constexpr int NITEM = MCG * CT;               // residual tile-groups per chunk
   static constexpr int NF_MAX = (NITEM + NRW - 1) / NRW;
+  // activation bytes of a group as loaded: 1 KiB of TQ4 nibbles, or two
+  // 1 KiB halves of fp8 bytes (the operand's split layout)
+  static constexpr int XB = FP8 ? 2048 : 1024;
+  static constexpr int SHL = FP8 ? 2 : 1;              // shared wave loads per wavefront and chunk
   // scale pieces (16 bytes = 8 fp16) of a chunk: activation, weight, L1
   static constexpr int NPX = MCG * 4, NPW = MCG * 4 * CT, NPL = MCG * 4 * RT;
   static constexpr int NP = NPX + NPW + NPL;
   static constexpr int NSI = (NP + 63) / 64;           // scale wave loads
-  static constexpr int NSH = MCG + NSI;                // shared wave loads per chunk
+  static constexpr int NSH = MCG * SHL + NSI;          // shared wave loads per chunk
   // chunk slot
   static constexpr int S_X = 0;                        // MCG raw activation blocks
-  static constexpr int S_SC = MCG * 1024;              // scale pieces
+  static constexpr int S_SC = MCG * XB;                // scale pieces
   static constexpr int S_FR = S_SC + NSI * 1024;       // blocks: H (RT x MCG), residual items
   static constexpr int SLOT = S_FR + (RT * MCG + NITEM) * 1024;
-  // expanded activation operands: 2 buffers x MCG groups x 2 KiB of fp8 bytes
-  static constexpr int XEB = MCG * 2048;
+  // expanded activation operands (TQ4 only): 2 buffers x MCG groups x 2 KiB
+  // of fp8 bytes; fp8 activations are read from the slot as loaded
+  static constexpr int XEB = FP8 ? 0 : MCG * 2048;
   // stage-2 operands: CT x RB L2 blocks and one scale region
   static constexpr int RB = (RT + 1) / 2;              // 64-rank blocks (= rank groups)
   static constexpr int L2B = RT > 0 ? CT * RB * 1024 + 1024 : 0;
   static constexpr int DFIT = (M_LDS - 2 * XEB - L2B) / SLOT;
-  static constexpr int D = DFIT > 16 ? 16 : DFIT;      // chunk slots
+  // the wait for a chunk leaves (D - 2) chunks of loads outstanding, and
+  // vmcnt counts to 63
+  static constexpr int PER_MAX = SHL + (RT > 0 && MCG > NF_MAX ? MCG : NF_MAX);
+  static constexpr int DVM = 63 / PER_MAX + 2;
+  static constexpr int D = DFIT < DVM ? (DFIT > 16 ? 16 : DFIT) : (DVM > 16 ? 16 : DVM);   // chunk slots
   static constexpr int OFF_XE = D * SLOT;
   static constexpr int OFF_L2 = OFF_XE + 2 * XEB;
   static constexpr int LDS = OFF_L2 + L2B;
@@ -77,7 +91,7 @@ struct MCfg {
   static constexpr int E_SH = E_QS + 32 * QSTR;                   // [RB][32] fp32
   static constexpr int E_RES = (E_SH + (RB > 0 ? RB : 1) * 128 + 255) / 256 * 256;
   static constexpr int E_END = E_RES + NITEM * 4096;              // [NITEM][64 lanes][16] fp32
-  static_assert(NSH <= MW, "one shared load per wavefront and chunk");
+  static_assert(NSH <= MW * SHL, "SHL shared loads per wavefront and chunk");
   static_assert(NF_MAX <= 4, "at most four residual items per wavefront and chunk");
   static_assert(D >= 3, "at least two chunks in flight");
   static_assert(MCG % 2 == 0 && NRW >= 2, "two expansion wavefronts, MCG / 2 groups each");
@@ -147,9 +161,9 @@ __device__ __forceinline__ v16f m_codes_half(v8i a, v8i b) {
                                                          kScale2p9);
 }
 
-template <int RT, int CT>
+template <int RT, int CT, bool FP8>
 __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, int n_rb) {
-  using C = MCfg<RT, CT>;
+  using C = MCfg<RT, CT, FP8>;
   constexpr int D = C::D;
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
   const Geometry &geo = a.geo;
@@ -171,7 +185,7 @@ __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, i
   const int cb = logical / n_rb, tb = logical % n_rb;   // column block, token block
   const uint32_t lds0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)smem);
 
-  const uint8_t *xc = reinterpret_cast<const uint8_t *>(a.xc) + (int64_t)tb * KG * 1024;
+  const uint8_t *xc = reinterpret_cast<const uint8_t *>(a.xc) + (int64_t)tb * KG * C::XB;
   const uint8_t *xs = reinterpret_cast<const uint8_t *>(a.xs);
   const uint8_t *wcodes = a.packed + geo.off_w;
   const uint8_t *wscales = a.packed + geo.off_ws;
@@ -180,37 +194,49 @@ __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, i
   const uint8_t *l2codes = a.packed + geo.off_l2;
   const uint8_t *l2scales = a.packed + geo.off_l2s;
 
-  // ---- this wavefront's shared load: lane reads base + g * stride ----
-  const int sh = wave % C::NSH;   // wavefronts past NSH repeat a load (same bytes, same place)
-  const uint8_t *sbase;
-  uint32_t sstride, sdst;
-  int sgi;
-  if (sh < MCG) {                 // activation block of group sh of the chunk
-    sbase = xc + lane * 16;
-    sstride = 1024;
-    sgi = sh;
-    sdst = C::S_X + sh * 1024;
-  } else {                        // scale pieces 64 s + lane
-    const int s = sh - MCG;
-    const int p0 = 64 * s + lane;
-    const int p = p0 < C::NP ? p0 : 0;
-    sdst = C::S_SC + s * 1024;
-    if (p < C::NPX) {
-      sgi = p / 4;
-      sbase = xs + (int64_t)(32 * tb + 8 * (p % 4)) * 2;
-      sstride = (uint32_t)ms * 2;
-    } else if (p < C::NPX + C::NPW) {
-      const int q = p - C::NPX;
-      sgi = q / (4 * CT);
-      sbase = wscales + (int64_t)min(32 * CT * cb + 8 * (q % (4 * CT)), geo.n_pad - 8) * 2;
-      sstride = (uint32_t)geo.n_pad * 2;
+  // ---- this wavefront's shared loads: lane reads base + g * stride ----
+  // Shared load sh < MCG * SHL is half sh % SHL of the activation block of
+  // group sh / SHL of the chunk, the rest are scale pieces 64 s + lane.
+  // Wavefront w issues loads w and (fp8) w + MW, modulo NSH: loads past NSH
+  // repeat one (same bytes, same place).
+  struct Shared {
+    const uint8_t *base;
+    uint32_t stride, dst;
+    int gi;
+  };
+  auto shared_load = [&](int sh) {
+    Shared L;
+    if (sh < MCG * C::SHL) {
+      const int gi = sh / C::SHL, half = sh % C::SHL;
+      L.base = xc + half * 1024 + lane * 16;
+      L.stride = C::XB;
+      L.gi = gi;
+      L.dst = C::S_X + gi * C::XB + half * 1024;
     } else {
-      const int q = p - C::NPX - C::NPW;
-      sgi = q / (4 * (RT > 0 ? RT : 1));
-      sbase = l1scales + (int64_t)(8 * (q % (4 * (RT > 0 ? RT : 1)))) * 2;
-      sstride = (uint32_t)geo.r_pad32 * 2;
+      const int s = sh - MCG * C::SHL;
+      const int p0 = 64 * s + lane;
+      const int p = p0 < C::NP ? p0 : 0;
+      L.dst = C::S_SC + s * 1024;
+      if (p < C::NPX) {
+        L.gi = p / 4;
+        L.base = xs + (int64_t)(32 * tb + 8 * (p % 4)) * 2;
+        L.stride = (uint32_t)ms * 2;
+      } else if (p < C::NPX + C::NPW) {
+        const int q = p - C::NPX;
+        L.gi = q / (4 * CT);
+        L.base = wscales + (int64_t)min(32 * CT * cb + 8 * (q % (4 * CT)), geo.n_pad - 8) * 2;
+        L.stride = (uint32_t)geo.n_pad * 2;
+      } else {
+        const int q = p - C::NPX - C::NPW;
+        L.gi = q / (4 * (RT > 0 ? RT : 1));
+        L.base = l1scales + (int64_t)(8 * (q % (4 * (RT > 0 ? RT : 1)))) * 2;
+        L.stride = (uint32_t)geo.r_pad32 * 2;
+      }
     }
-  }
+    return L;
+  };
+  const Shared sl0 = shared_load(wave % C::NSH);
+  const Shared sl1 = shared_load((wave + MW) % C::NSH);   // issued in fp8 mode only
 
   // ---- roles ----
   const bool hw = wave < RT;
@@ -242,7 +268,7 @@ __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, i
   // per 16-byte lane slot
   const int ex = ri >= C::NRW - 2 ? ri - (C::NRW - 2) : -1;   // expansion wavefront (or none)
   auto expand = [&](int c, uint32_t slot_off) {
-    if (ex >= 0) {
+    if (!FP8 && ex >= 0) {
 #pragma unroll
       for (int q = 0; q < MCG / 2; q++) {
         const int gi = ex * (MCG / 2) + q;
@@ -262,7 +288,7 @@ __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, i
   auto k_loop = [&](auto HC, auto NFC, auto &acc) {
     constexpr bool H = decltype(HC)::value;
     constexpr int NF = decltype(NFC)::value;
-    constexpr int PER = 1 + NF;   // loads per chunk
+    constexpr int PER = C::SHL + NF;   // loads per chunk
     auto item_gi = [&](int k) { return H ? k : (ri + C::NRW * k) / CT; };
     auto item_tile = [&](int k) { return (ri + C::NRW * k) % CT; };
     auto item_frag = [&](int k) { return H ? wave * MCG + k : RT * MCG + ri + C::NRW * k; };
@@ -271,8 +297,10 @@ __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, i
     // block loads (wave-uniform bases in scalar registers, lane offset
     // 16 * lane, MCG KiB per chunk).  A chunk that runs past the last K-group
     // clamps its groups to the last one.
-    const uint8_t *sh_addr = sbase + (uint64_t)sgi * sstride;
-    const uint64_t sh_inc = (uint64_t)MCG * sstride;
+    const uint8_t *sh_addr = sl0.base + (uint64_t)sl0.gi * sl0.stride;
+    const uint64_t sh_inc = (uint64_t)MCG * sl0.stride;
+    const uint8_t *sh_addr1 = sl1.base + (uint64_t)sl1.gi * sl1.stride;
+    const uint64_t sh_inc1 = (uint64_t)MCG * sl1.stride;
     const uint32_t lane16 = lane * 16;
     const uint8_t *fb[NF > 0 ? NF : 1];
 #pragma unroll
@@ -283,14 +311,17 @@ __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, i
     auto issue = [&](int c) {
       const uint32_t slot = lds0 + islot;
       if (MCG * (c + 1) <= KG) {
-        mdma(sh_addr, slot + sdst);
+        mdma(sh_addr, slot + sl0.dst);
+        if constexpr (FP8) mdma(sh_addr1, slot + sl1.dst);
 #pragma unroll
         for (int k = 0; k < NF; k++) {
           mdma_s(lane16, fb[k], slot + C::S_FR + item_frag(k) * 1024);
           fb[k] += MCG * 1024;
         }
       } else {
-        mdma(sbase + (uint64_t)min(MCG * c + sgi, KG - 1) * sstride, slot + sdst);
+        mdma(sl0.base + (uint64_t)min(MCG * c + sl0.gi, KG - 1) * sl0.stride, slot + sl0.dst);
+        if constexpr (FP8)
+          mdma(sl1.base + (uint64_t)min(MCG * c + sl1.gi, KG - 1) * sl1.stride, slot + sl1.dst);
 #pragma unroll
         for (int k = 0; k < NF; k++) {
           const int g = min(MCG * c + item_gi(k), KG - 1);
@@ -300,6 +331,7 @@ __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, i
         }
       }
       sh_addr += sh_inc;
+      sh_addr1 += sh_inc1;
       islot = islot + C::SLOT == D * C::SLOT ? 0 : islot + C::SLOT;
     };
 
@@ -313,9 +345,10 @@ __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, i
     expand(0, 0);
     uint32_t rslot = 0;   // ring offset of chunk c
     for (int c = 0; c < NCH; c++) {
-      // chunk c + 1 has landed (near the end of K nothing is issued past the
-      // last chunk, so everything issued is waited for)
-      if (c + D - 1 <= NCH) mwait_vm<(D - 3) * PER>();
+      // chunk c + 1 has landed for its expansion (fp8: chunk c, read as
+      // loaded); near the end of K nothing is issued past the last chunk, so
+      // everything issued is waited for
+      if (c + D - 1 <= NCH) mwait_vm<(FP8 ? D - 2 : D - 3) * PER>();
       else mwait_vm<0>();
       __syncthreads();             // chunk c's operands are visible; chunk c - 1 is consumed
       if (c + D - 1 < NCH) issue(c + D - 1);   // into chunk c - 1's slot
@@ -329,7 +362,13 @@ __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, i
 #pragma unroll
         for (int k = 0; k < NF; k++) {
           const int gi = item_gi(k);
-          av[k] = lds_v8i(XE + gi * 2048 + lane * 32);
+          if constexpr (FP8) {
+            const u32x4 lo = *reinterpret_cast<const u32x4 *>(S + C::S_X + gi * 2048 + lane * 16);
+            const u32x4 hi = *reinterpret_cast<const u32x4 *>(S + C::S_X + gi * 2048 + 1024 + lane * 16);
+            av[k] = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+          } else {
+            av[k] = lds_v8i(XE + gi * 2048 + lane * 32);
+          }
           bv[k] = *reinterpret_cast<const u32x4 *>(S + C::S_FR + item_frag(k) * 1024 + lane * 16);
           const uint32_t s_a = *reinterpret_cast<const uint16_t *>(S + C::S_SC + (gi * 32 + l32) * 2);
           sa[k] = MCG * c + gi < KG ? s_a : 0u;   // a group past K adds exactly zero
@@ -519,12 +558,12 @@ __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, i
   }
 }
 
-template <int RT, int CT>
+template <int RT, int CT, bool FP8>
 hipError_t launch_mid(const GemmArgs &a, hipStream_t s) {
-  using C = MCfg<RT, CT>;
+  using C = MCfg<RT, CT, FP8>;
   const int n_rb = a.ms / 32;
   const int n_cb = (a.geo.n_pad / 32 + CT - 1) / CT;
-  auto kern = dual_gemm_mid_kernel<RT, CT>;
+  auto kern = dual_gemm_mid_kernel<RT, CT, FP8>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
   if (e != hipSuccess) return e;
@@ -532,15 +571,21 @@ hipError_t launch_mid(const GemmArgs &a, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int CT>
+template <int CT, bool FP8>
 hipError_t launch_mid_rt(const GemmArgs &a, hipStream_t s) {
   switch (a.geo.r_pad32 / 32) {
-    case 0: return launch_mid<0, CT>(a, s);
-    case 1: return launch_mid<1, CT>(a, s);
-    case 2: return launch_mid<2, CT>(a, s);
-    case 4: return launch_mid<4, CT>(a, s);
+    case 0: return launch_mid<0, CT, FP8>(a, s);
+    case 1: return launch_mid<1, CT, FP8>(a, s);
+    case 2: return launch_mid<2, CT, FP8>(a, s);
+    case 4: return launch_mid<4, CT, FP8>(a, s);
     default: return hipErrorInvalidValue;
   }
+}
+
+template <bool FP8>
+hipError_t launch_mid_ct(int ct, const GemmArgs &a, hipStream_t s) {
+  if (ct == 1) return launch_mid_rt<1, FP8>(a, s);
+  return ct == 4 ? launch_mid_rt<4, FP8>(a, s) : launch_mid_rt<2, FP8>(a, s);
 }
 
 // Each work-group runs one serial K loop whose length grows with the
@@ -557,17 +602,29 @@ int mid_cost(int rt, int ct, int n_rb, int ct32) {
   return (n_wg + 255) / 256 * (3 + rt + ct);
 }
 
-}  // namespace
-
-hipError_t launch_dual_gemm_mid(const GemmArgs &a, hipStream_t s) {
+// the tile count of least cost (and that cost)
+int mid_tiles(const GemmArgs &a, int *cost) {
   const int rt = a.geo.r_pad32 / 32, ct32 = a.geo.n_pad / 32, n_rb = a.ms / 32;
   int ct = 1;
   for (int c : {2, 4})
     if (mid_cost(rt, c, n_rb, ct32) < mid_cost(rt, ct, n_rb, ct32)) ct = c;
   // TQ_MID_CT=1|2|4 forces the tile count (the tests run all three)
   if (const char *env = getenv("TQ_MID_CT")) ct = atoi(env);
-  if (ct == 1) return launch_mid_rt<1>(a, s);
-  return ct == 4 ? launch_mid_rt<4>(a, s) : launch_mid_rt<2>(a, s);
+  if (cost) *cost = mid_cost(rt, ct, n_rb, ct32);
+  return ct;
+}
+
+}  // namespace
+
+int dual_gemm_mid_cost(const GemmArgs &a) {
+  int cost = 0;
+  mid_tiles(a, &cost);
+  return cost;
+}
+
+hipError_t launch_dual_gemm_mid(const GemmArgs &a, hipStream_t s) {
+  const int ct = mid_tiles(a, nullptr);
+  return act_codes_fp8(a.m) ? launch_mid_ct<true>(ct, a, s) : launch_mid_ct<false>(ct, a, s);
 }
 
 }  // namespace tq

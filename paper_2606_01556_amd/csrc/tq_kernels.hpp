@@ -61,7 +61,13 @@ hipError_t launch_export(const Geometry &g, const uint8_t *packed, uint32_t *wc,
                          hipStream_t s);
 hipError_t launch_dual_gemm(const GemmArgs &a, hipStream_t s);
 hipError_t launch_dual_gemm_decode(const GemmArgs &a, hipStream_t s);  // m <= 16
+// the kernel launch_dual_gemm runs (values of tq_kernel in the C header)
+constexpr int kKernelDecode = 0, kKernelMid = 1, kKernelLarge = 2, kKernelPrefill = 3;
+int choose_kernel(const GemmArgs &a);
 hipError_t launch_dual_gemm_mid(const GemmArgs &a, hipStream_t s);      // mid sizes
+// relative time of the mid kernel's launch: rounds of work-groups over the
+// CUs x tile-groups per work-group and chunk (+3 for its fixed latency)
+int dual_gemm_mid_cost(const GemmArgs &a);
 hipError_t launch_dual_gemm_prefill(const GemmArgs &a, hipStream_t s);  // prefill sizes
 hipError_t launch_dual_gemm_large(const GemmArgs &a, hipStream_t s);    // large token counts
 // the layer without fusion (comparison baseline): residual GEMM, stage 1 to

@@ -196,3 +196,28 @@ def test_unfused_sizes_and_validation(L):
     assert L.tq_dual_gemm_unfused(ctypes.byref(d), FAKE, FAKE, FAKE, 1, FAKE, 0, None, None) == 1
     assert L.tq_dual_gemm_unfused(ctypes.byref(d), FAKE, FAKE, FAKE, 1, FAKE, 0, FAKE + 4, None) == 6
     assert L.tq_dual_gemm_unfused(ctypes.byref(d), FAKE, FAKE, FAKE, 0, FAKE, 0, FAKE, None) == 0
+
+
+def test_kernel_choice(L, monkeypatch):
+    """tq_dual_gemm_kernel: the decode kernel up to 16 tokens, the mid kernel
+    up to 512, past that the large kernel where its 128 x 256 blocks fill the
+    CUs, the mid kernel where they would leave most CUs idle, the prefill
+    kernel for r > 64 beyond one round of blocks; the test hooks force each;
+    -1 for a bad descriptor or m."""
+    for k in ("TQ_LARGE", "TQ_MID", "TQ_MID_CT"):
+        monkeypatch.delenv(k, raising=False)
+    d = tq.weight_desc_init(4096, 4096, 64)           # n, k, r
+    assert [tq.dual_gemm_kernel(d, m) for m in (1, 16, 17, 512, 2048)] == \
+        ["decode", "decode", "mid", "mid", "large"]
+    assert tq.dual_gemm_kernel(tq.weight_desc_init(96, 4096, 64), 600) == "mid"
+    assert tq.dual_gemm_kernel(tq.weight_desc_init(14336, 4096, 128), 4096) == "prefill"
+    monkeypatch.setenv("TQ_MID", "1")
+    assert tq.dual_gemm_kernel(d, 2048) == "mid" and tq.dual_gemm_kernel(d, 8) == "decode"
+    monkeypatch.delenv("TQ_MID")
+    monkeypatch.setenv("TQ_LARGE", "0")
+    assert tq.dual_gemm_kernel(d, 2048) == "prefill" and tq.dual_gemm_kernel(d, 300) == "mid"
+    assert L.tq_dual_gemm_kernel(ctypes.byref(d), 0) == -1
+    assert L.tq_dual_gemm_kernel(ctypes.byref(tq.WeightDesc()), 100) == -1
+    assert L.tq_dual_gemm_kernel(None, 100) == -1
+    with pytest.raises(ValueError):
+        tq.dual_gemm_kernel(d, 0)

@@ -25,8 +25,8 @@ MAX_ABS_RMS = 1e-2
 # rounding of the output alone reaches ~1.1e-3 relative Frobenius error, so the
 # fp16 bounds are scaled by 8 for bf16 results.
 BF16_FACTOR = 8.0
-# smallest token count served by the large / prefill kernels (bit-exact Y)
-PREFILL_FROM = 513
+# kernels that sum each output in the oracle's fp32 order (bit-exact Y)
+Y_EXACT_KERNELS = ("large", "prefill")
 
 
 def say(*a):
@@ -56,7 +56,7 @@ def run_gpu(X, W, L1, L2, bf16=False, debug=True):
     xc, xs = tq.empty_act(M, K)
     tq.quant_act(xd, xc, xs)
     y = torch.empty((M, N), dtype=torch.bfloat16 if bf16 else torch.float16, device="cuda")
-    out = {}
+    out = {"kernel": tq.dual_gemm_kernel(d, M)}
     if r and debug:
         h = torch.empty((M, r), dtype=torch.float32, device="cuda")
         sh = torch.empty((M, r // d.group_r), dtype=torch.float32, device="cuda")
@@ -134,7 +134,7 @@ def full_parity(oracle_mod, X, W, L1, L2, bf16=False, wide_range=False):
         np.testing.assert_array_equal(g["H"].view(np.uint32), o["H"].view(np.uint32))
         np.testing.assert_array_equal(g["sH"].view(np.uint32), o["sH"].view(np.uint32))
         np.testing.assert_array_equal(g["qH"], o["qH"])
-    if X.shape[0] >= PREFILL_FROM:
+    if g["kernel"] in Y_EXACT_KERNELS:
         if bf16:
             np.testing.assert_array_equal(g["Ybits"], o["Ybf"])
         else:
@@ -185,16 +185,34 @@ def test_mid_kernel_variants(oracle_mod, monkeypatch, ct, M, K, N, r):
     full_parity(oracle_mod, d["X"], d["W_res"], d["L1"], d["L2"])
 
 
-@pytest.mark.parametrize("large", ["0", "1"])
+@pytest.mark.parametrize("large", ["0", "1", "mid"])
 @pytest.mark.parametrize("M,K,N,r", [(600, 576, 1000, 64), (1100, 256, 520, 128), (700, 320, 300, 16),
                                      (900, 128, 2000, 0), (530, 192, 4096, 32)])
 def test_large_m_kernels(oracle_mod, monkeypatch, large, M, K, N, r):
-    """m > 512 on both large-m kernels (16-wavefront blocks with H in the main
-    loop, and the prefill kernel with its separate H pass): ragged token and
-    column counts, odd K-group counts, every rank-tile count; Y bit-exact."""
-    monkeypatch.setenv("TQ_LARGE", large)
+    """m > 512 (fp8 activation codes) on the three kernels that take it: the
+    16-wavefront blocks with H in the main loop, the prefill kernel with its
+    separate H pass, and the mid kernel's 32-token blocks; ragged token and
+    column counts, odd K-group counts, every rank-tile count."""
+    if large == "mid":
+        monkeypatch.setenv("TQ_MID", "1")
+    else:
+        monkeypatch.setenv("TQ_LARGE", large)
     say(f"large={large} M={M} K={K} N={N} r={r}")
     d = random_codes_layer(M, K, N, r, seed=M + 3 * N + r)
+    full_parity(oracle_mod, d["X"], d["W_res"], d["L1"], d["L2"])
+
+
+@pytest.mark.parametrize("ct", ["1", "2", "4"])
+@pytest.mark.parametrize("M,K,N,r", [(513, 192, 100, 32), (800, 320, 1024, 64), (640, 64, 96, 128),
+                                     (1000, 448, 520, 16), (576, 128, 300, 0)])
+def test_mid_kernel_fp8_activations(oracle_mod, monkeypatch, ct, M, K, N, r):
+    """The mid kernel on fp8 activation codes (m > 512), with 1, 2 and 4 column
+    tiles per work-group, odd K-group counts (a half chunk at the end of K)
+    and every rank-tile count."""
+    monkeypatch.setenv("TQ_MID", "1")
+    monkeypatch.setenv("TQ_MID_CT", ct)
+    say(f"mid fp8 ct={ct} M={M} K={K} N={N} r={r}")
+    d = random_codes_layer(M, K, N, r, seed=M * 5 + N + r)
     full_parity(oracle_mod, d["X"], d["W_res"], d["L1"], d["L2"])
 
 
@@ -341,7 +359,7 @@ def sampled_parity(oracle_mod, wl_name, layer_idx, M, rank=None, n_rows=6, n_col
     rows = np.unique(np.concatenate([[0, M - 1], rng.integers(0, M, n_rows)]))
     cols = np.unique(np.concatenate([[0, N - 1], rng.integers(0, N, n_cols)]))
     o = oracle_mod.layer(X, W, L1, L2, GROUP, rows=rows, cols=cols)
-    if M >= PREFILL_FROM:
+    if g["kernel"] in Y_EXACT_KERNELS:
         np.testing.assert_array_equal(g["Ybits"][np.ix_(rows, cols)], o["Y16"].view(np.uint16))
     check_tolerance(g["Y"][np.ix_(rows, cols)], o["Y64"])
     if L1 is not None:
