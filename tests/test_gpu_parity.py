@@ -10,6 +10,8 @@ output Y is bit-exact too; the decode and mid kernels split the residual K
 loop over wavefronts, which changes only the fp32 summation order of Y.  The benchmark spec's tolerance (relative Frobenius 1e-3, max-abs
 1e-2 * rms(Y)) is checked everywhere, against the oracle's fp64 result.
 """
+import os
+
 import numpy as np
 import pytest
 
@@ -339,6 +341,53 @@ def test_decode_workspace_reuse():
         torch.cuda.synchronize()
         for y, r in zip(outs, ref):
             assert torch.equal(y.view(torch.int16), r.view(torch.int16))
+
+
+def test_every_kernel_graph_replay():
+    """One call on each of the four kernels, as the dispatch picks them (decode
+    m = 4; mid m = 100; mid on fp8 activations for a narrow layer at m = 600;
+    large m = 600 on a wide one; prefill r = 128 beyond one round of 128 x 256
+    blocks), captured in one HIP graph on a shared workspace and replayed three
+    times: every replay is bit-equal to the eager calls."""
+    say("every kernel graph replay")
+    for k in ("TQ_LARGE", "TQ_MID", "TQ_MID_CT"):
+        assert k not in os.environ
+    cases = ((4, 256, 512, 64, "decode"), (100, 192, 300, 32, "mid"), (600, 256, 96, 64, "mid"),
+             (600, 128, 8192, 16, "large"), (2048, 128, 4352, 128, "prefill"))
+    calls = []
+    for (M, K, N, r, kern) in cases:
+        d = random_codes_layer(M, K, N, r, seed=M + N)
+        lay = tq.Layer(dev(d["W_res"]), dev(d["L1"]), dev(d["L2"]))
+        assert tq.dual_gemm_kernel(lay.desc, M) == kern, (M, K, N, r)
+        xc, xsc = tq.empty_act(M, K)
+        tq.quant_act(dev(d["X"]), xc, xsc)
+        calls.append((lay, M, xc, xsc, torch.empty((M, N), dtype=torch.float16, device="cuda")))
+    ws = tq.empty_workspace()
+
+    def run(stream=None):
+        for lay, M, xc, xsc, y in calls:
+            tq.dual_gemm(lay.desc, lay.packed, xc, xsc, M, y, ws, stream=stream)
+
+    run()
+    torch.cuda.synchronize()
+    ref = [y.clone() for *_, y in calls]
+    st = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(st):
+        g.capture_begin()
+        run(stream=st)
+        g.capture_end()
+    for _ in range(3):
+        for *_, y in calls:
+            y.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for (*_, y), r in zip(calls, ref):
+            assert torch.equal(y.view(torch.int16), r.view(torch.int16))
+        run()                       # eager work between the replays
+        torch.cuda.synchronize()
 
 
 def test_repeatable_bitwise(oracle_mod):
