@@ -20,15 +20,20 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "tq_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
-# -ffp-contract=off: no implicit fma; every float op is IEEE single precision.
-BUILD_CMD = ["gcc", "-O2", "-std=c99", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
-             "-fPIC", "-shared", "-Wall", "-Wno-unknown-pragmas", _SRC, "-o", _LIB, "-lm"]
+
+def build_cmd(src: str = _SRC, out: str = _LIB) -> list:
+    # -ffp-contract=off: no implicit fma; every float op is IEEE single precision.
+    return ["gcc", "-O2", "-std=c99", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
+            "-fPIC", "-shared", "-Wall", "-Wno-unknown-pragmas", src, "-o", out, "-lm"]
 
 
-def build() -> str:
-    """Compile the oracle library in place and return its path."""
-    subprocess.run(BUILD_CMD, check=True)
-    return _LIB
+BUILD_CMD = build_cmd()
+
+
+def build(src: str = _SRC, out: str = _LIB) -> str:
+    """Compile the oracle library (in place by default) and return its path."""
+    subprocess.run(build_cmd(src, out), check=True)
+    return out
 
 
 _lib = None
@@ -39,21 +44,26 @@ def lib():
     if _lib is None:
         if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
             build()
-        L = ctypes.CDLL(_LIB)
-        P = ctypes.c_void_p
-        L.tqo_f16_to_f64.argtypes = [ctypes.c_uint16]
-        L.tqo_f16_to_f64.restype = ctypes.c_double
-        L.tqo_f64_to_f16.argtypes = [ctypes.c_double]
-        L.tqo_f64_to_f16.restype = ctypes.c_uint16
-        L.tqo_f32_to_bf16.argtypes = [ctypes.c_float]
-        L.tqo_f32_to_bf16.restype = ctypes.c_uint16
-        L.tqo_quantize.argtypes = [P, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
-                                   ctypes.c_int64, ctypes.c_int, P, P]
-        L.tqo_quantize.restype = ctypes.c_int
-        L.tqo_layer.argtypes = [ctypes.c_int] * 5 + [P] * 4 + [P, ctypes.c_int, P, ctypes.c_int] + [P] * 7
-        L.tqo_layer.restype = ctypes.c_int
-        _lib = L
+        _lib = load(_LIB)
     return _lib
+
+
+def load(path: str):
+    """Load an oracle library file and declare its entry points."""
+    L = ctypes.CDLL(path)
+    P = ctypes.c_void_p
+    L.tqo_f16_to_f64.argtypes = [ctypes.c_uint16]
+    L.tqo_f16_to_f64.restype = ctypes.c_double
+    L.tqo_f64_to_f16.argtypes = [ctypes.c_double]
+    L.tqo_f64_to_f16.restype = ctypes.c_uint16
+    L.tqo_f32_to_bf16.argtypes = [ctypes.c_float]
+    L.tqo_f32_to_bf16.restype = ctypes.c_uint16
+    L.tqo_quantize.argtypes = [P, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
+                               ctypes.c_int64, ctypes.c_int, P, P]
+    L.tqo_quantize.restype = ctypes.c_int
+    L.tqo_layer.argtypes = [ctypes.c_int] * 5 + [P] * 4 + [P, ctypes.c_int, P, ctypes.c_int] + [P] * 7
+    L.tqo_layer.restype = ctypes.c_int
+    return L
 
 
 def _ptr(a):

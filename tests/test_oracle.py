@@ -380,3 +380,111 @@ def test_row_col_selection_matches_full(oracle_mod):
     np.testing.assert_array_equal(sub["Y32"], full["Y32"][np.ix_(rows, cols)])
     np.testing.assert_array_equal(sub["qH"], full["qH"][rows])
     np.testing.assert_array_equal(sub["Y16"], full["Y16"][np.ix_(rows, cols)])
+
+
+# ---------------------------------------------------------------- H order and Q_H ties
+def f32_rne_exact(x: Fr) -> Fr:
+    """Nearest binary32 value of an exact rational, ties to even (normal range)."""
+    if x == 0:
+        return Fr(0)
+    sgn = -1 if x < 0 else 1
+    x = abs(x)
+    e = 0
+    while x >= 2:
+        x /= 2
+        e += 1
+    while x < 1:
+        x *= 2
+        e -= 1
+    ulp = Fr(2) ** (e - 23)
+    return sgn * rne_int(x * Fr(2) ** e / ulp) * ulp
+
+
+def check_h_chain_order(oracle_mod):
+    """O4 (Sec. 4.3, stage 1; reading R11): H is summed over K-groups in
+    ascending order, one fused multiply-add (a single rounding) per group, with
+    the exact fp32 scale product s_x s_L1.  The designed layer fixes the codes
+    and scales, so the integer group sums A_g and the scale products c_g are
+    known exactly; the expected H is the ascending chain
+    h <- rn32(A_g c_g + h) evaluated in exact rationals.  The design also
+    checks that it tells this chain apart from a descending chain, from an
+    unfused chain (the product rounded before the add) and from the correctly
+    rounded sum."""
+    from designed import chain_order_layer
+    d = chain_order_layer(M=8, r=32, seed=1)
+    out = oracle_mod.layer(d["X"], d["W_res"], d["L1"], d["L2"], GROUP)
+    M, r = out["H"].shape
+    KG = d["sx"].shape[1]
+    qx = d["qx"].reshape(M, KG, GROUP)
+    ql1 = d["ql1"].reshape(KG, GROUP, r)
+    A = np.einsum("mgk,gkj->mjg", qx, ql1)                      # exact int64 sums
+    diffs = {"descending": 0, "unfused": 0, "exact_sum": 0}
+    for m in range(M):
+        for j in range(r):
+            terms = [int(A[m, j, g]) * Fr(float(d["sx"][m, g])) * Fr(float(d["sl1"][g, j]))
+                     for g in range(KG)]
+            asc = Fr(0)
+            for t in terms:
+                asc = f32_rne_exact(t + asc)
+            desc = Fr(0)
+            for t in reversed(terms):
+                desc = f32_rne_exact(t + desc)
+            unf = Fr(0)
+            for t in terms:
+                unf = f32_rne_exact(f32_rne_exact(t) + unf)
+            exact = f32_rne_exact(sum(terms))
+            assert Fr(float(out["H"][m, j])) == asc, (m, j)
+            diffs["descending"] += desc != asc
+            diffs["unfused"] += unf != asc
+            diffs["exact_sum"] += exact != asc
+    assert all(v > 0 for v in diffs.values()), diffs
+
+
+def check_qh_ties(oracle_mod):
+    """O5 (Sec. 4.3, on-the-fly scaling; readings R1, R10): on the designed
+    layer of tests/golden/qh_ties.txt, H / s_H lands exactly on k + 1/2 and
+    the codes are the fixture's hand-derived round-half-to-even values."""
+    from designed import qh_tie_layer
+    fx_u = [1.0, 3.0, 0.125]
+    d = qh_tie_layer(M=3, N=16)
+    out = oracle_mod.layer(d["X"], d["W_res"], d["L1"], d["L2"], GROUP)
+    np.testing.assert_array_equal(out["sH"][:, 0], np.array(fx_u, np.float32))
+    np.testing.assert_array_equal(out["H"], (d["t"] * np.array(fx_u)[:, None]).astype(np.float32))
+    np.testing.assert_array_equal(out["qH"], d["qh"])
+
+
+def test_h_chain_order_exact(oracle_mod):
+    check_h_chain_order(oracle_mod)
+
+
+def test_qh_ties_golden(oracle_mod):
+    check_qh_ties(oracle_mod)
+
+
+# Each pin above must fail on an oracle with the corresponding plausible
+# mistake; the mutants are built from the oracle's source on the CPU.
+MUTANTS = {
+    "h_descending": ("for (int g = 0; g < KG; g++) {\n                    int32_t a = 0;",
+                     "for (int g = KG - 1; g >= 0; g--) {\n                    int32_t a = 0;",
+                     check_h_chain_order),
+    "h_unfused": ("acc = fmaf((float)a, sxf * slf, acc);",
+                  "acc = (float)a * (sxf * slf) + acc;", check_h_chain_order),
+    "qh_half_away": ("double rr = nearbyint((double)t);", "double rr = round((double)t);",
+                     check_qh_ties),
+    "qh_truncate": ("double rr = nearbyint((double)t);", "double rr = trunc((double)t);",
+                    check_qh_ties),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_reject_mutant_oracle(oracle_mod, tmp_path, monkeypatch, name):
+    old, new, check = MUTANTS[name]
+    with open(oracle_mod._SRC) as f:
+        src = f.read()
+    assert src.count(old) == 1, "mutation site not found once in the oracle source"
+    mut = tmp_path / "mutant.c"
+    mut.write_text(src.replace(old, new))
+    lib = oracle_mod.load(oracle_mod.build(str(mut), str(tmp_path / "libmutant.so")))
+    monkeypatch.setattr(oracle_mod, "_lib", lib)
+    with pytest.raises(AssertionError):
+        check(oracle_mod)
