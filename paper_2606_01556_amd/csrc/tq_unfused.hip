@@ -19,24 +19,6 @@
 namespace tq {
 namespace {
 
-typedef _Float16 v4h __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-
-// 2 * s_row * s_col of a 32x32 tile (both scales in k = 0 and k = 4)
-__device__ __forceinline__ v16f u_outer2(uint32_t sa, uint32_t sb) {
-  const v16f z = {0};
-  const u32x2 a2 = {sa, 0u}, b2 = {sb, 0u};
-  return __builtin_amdgcn_mfma_f32_32x32x8f16(__builtin_bit_cast(v4h, a2),
-                                              __builtin_bit_cast(v4h, b2), z, 0, 0, 0);
-}
-
-// half of the exact integer group sum of a 32x32 tile of code products
-__device__ __forceinline__ v16f u_codes_half(v8i a, v8i b) {
-  const v16f z = {0};
-  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, z, 0, 0, 0, kScale2p9 - 1, 0,
-                                                         kScale2p9);
-}
-
 // activation operand of token tile t, group g (both activation formats)
 template <bool FP8>
 __device__ __forceinline__ v8i act_operand(const uint8_t *xc, int KG, int t, int g, int lane) {
@@ -50,46 +32,70 @@ __device__ __forceinline__ v8i act_operand(const uint8_t *xc, int KG, int t, int
   }
 }
 
-// Stage 1: one wavefront per 32-token x 32-rank tile of H, all K-groups in
-// ascending order, with the operands of the next PF groups in flight (each
-// slot is refilled with group g + PF as soon as group g is consumed).
+// Stage 1: one work-group of eight wavefronts per 32-token x 32-rank tile of
+// H.  K runs in chunks of up to 32 groups: wavefront w forms the exact
+// integer sums of groups w, w + 8, w + 16 and w + 24 of the chunk (one
+// matrix-core product each, with the next chunk's operands already in
+// flight) and stores them and the group scales in LDS; then each wavefront
+// takes two of the tile's sixteen accumulator registers and runs the
+// ascending-group chain over the chunk, one fma per group with the exact
+// fp32 scale product s_x s_L1.
+constexpr int kS1Waves = 8, kS1Gpw = 4, kS1Chunk = kS1Waves * kS1Gpw;
+constexpr int kS1Lds = kS1Chunk * 16 * 64 * 4 + 2 * kS1Chunk * 32 * 4;
+
 template <bool FP8>
-__global__ __launch_bounds__(64) void unfused_stage1_kernel(GemmArgs a, float *__restrict__ h) {
-  constexpr int PF = 16;
+__global__ __launch_bounds__(64 * kS1Waves) void unfused_stage1_kernel(GemmArgs a,
+                                                                        float *__restrict__ h) {
+  extern __shared__ __attribute__((aligned(16))) float s1_lds[];
+  float *CS = s1_lds;                              // [chunk group][v][lane]
+  float *SX = s1_lds + kS1Chunk * 16 * 64;         // [chunk group][32 tokens]
+  float *SL = SX + kS1Chunk * 32;                  // [chunk group][32 ranks]
   const Geometry &geo = a.geo;
-  const int t = blockIdx.x, rt = blockIdx.y, lane = threadIdx.x, l32 = lane & 31;
+  const int t = blockIdx.x, rt = blockIdx.y, tid = threadIdx.x, lane = tid & 63, l32 = lane & 31;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int KG = geo.k / kGroup;
   const uint8_t *xc = reinterpret_cast<const uint8_t *>(a.xc);
   const uint8_t *l1 = a.packed + geo.off_l1 + (int64_t)rt * KG * 1024 + lane * 16;
   const uint16_t *l1s = reinterpret_cast<const uint16_t *>(a.packed + geo.off_l1s);
-  v8i av[PF];
-  u32x4 lraw[PF];
-  uint32_t sx[PF], sl[PF];
-  auto load = [&](int j, int g) {
-    g = min(g, KG - 1);
-    av[j] = act_operand<FP8>(xc, KG, t, g, lane);
-    lraw[j] = *reinterpret_cast<const u32x4 *>(l1 + (int64_t)g * 1024);
-    sx[j] = a.xs[(int64_t)g * a.ms + 32 * t + l32];
-    sl[j] = l1s[(int64_t)g * geo.r_pad32 + 32 * rt + l32];
+  v8i av[kS1Gpw];
+  u32x4 lraw[kS1Gpw];
+  uint32_t sc[kS1Gpw];   // lanes 0-31: token scale, lanes 32-63: rank scale
+  auto load = [&](int i, int g) {
+    av[i] = act_operand<FP8>(xc, KG, t, g, lane);
+    lraw[i] = *reinterpret_cast<const u32x4 *>(l1 + (int64_t)g * 1024);
+    sc[i] = lane < 32 ? a.xs[(int64_t)g * a.ms + 32 * t + l32]
+                      : l1s[(int64_t)g * geo.r_pad32 + 32 * rt + l32];
   };
 #pragma unroll
-  for (int j = 0; j < PF; j++) load(j, j);
-  v16f acc = v16f{0};
-  for (int g0 = 0; g0 < KG; g0 += PF) {
+  for (int i = 0; i < kS1Gpw; i++)
+    if (i * kS1Waves + w < KG) load(i, i * kS1Waves + w);
+  float acc0 = 0.0f, acc1 = 0.0f;
+  const int v0 = 2 * w, row0 = row_of_32x32(lane, v0), row1 = row_of_32x32(lane, v0 + 1);
+  for (int c0 = 0; c0 < KG; c0 += kS1Chunk) {
 #pragma unroll
-    for (int j = 0; j < PF; j++) {
-      if (g0 + j < KG) {
-        const v16f c = u_codes_half(av[j], unpack32(lraw[j]));
-        const v16f p = u_outer2(sx[j], sl[j]);
+    for (int i = 0; i < kS1Gpw; i++) {
+      const int gl = i * kS1Waves + w;
+      if (c0 + gl < KG) {
+        const v16f c = mfma_codes_32x32x64(av[i], unpack32(lraw[i]));
 #pragma unroll
-        for (int v = 0; v < 16; v++) acc[v] = fmaf(c[v], p[v], acc[v]);
+        for (int v = 0; v < 16; v++) CS[(gl * 16 + v) * 64 + lane] = c[v];
+        const float sv = half_bits_to_float((uint16_t)sc[i]);
+        if (lane < 32) SX[gl * 32 + l32] = sv;
+        else SL[gl * 32 + l32] = sv;
       }
-      load(j, g0 + j + PF);
+      if (c0 + kS1Chunk + gl < KG) load(i, c0 + kS1Chunk + gl);
     }
+    __syncthreads();
+    const int ng = min(kS1Chunk, KG - c0);
+    for (int gl = 0; gl < ng; gl++) {
+      const float sl = SL[gl * 32 + l32];
+      acc0 = fmaf(CS[(gl * 16 + v0) * 64 + lane], SX[gl * 32 + row0] * sl, acc0);
+      acc1 = fmaf(CS[(gl * 16 + v0 + 1) * 64 + lane], SX[gl * 32 + row1] * sl, acc1);
+    }
+    __syncthreads();
   }
-#pragma unroll
-  for (int v = 0; v < 16; v++)
-    h[(int64_t)(32 * t + row_of_32x32(lane, v)) * geo.r_pad32 + 32 * rt + l32] = acc[v];
+  h[(int64_t)(32 * t + row0) * geo.r_pad32 + 32 * rt + l32] = acc0;
+  h[(int64_t)(32 * t + row1) * geo.r_pad32 + 32 * rt + l32] = acc1;
 }
 
 // Re-quantization: one lane per element of H; a wavefront covers 64 ranks of
@@ -191,10 +197,11 @@ hipError_t launch_dual_gemm_unfused(const GemmArgs &a, void *scratch, hipStream_
   uint8_t *qh = base + up((size_t)m32 * g.r_pad32 * 4);
   float *sh = reinterpret_cast<float *>(qh + up((size_t)m32 * g.r_pad64));
   // 2. stage 1: H to global memory
-  if (act_codes_fp8(a.m))
-    hipLaunchKernelGGL(unfused_stage1_kernel<true>, dim3(tiles, g.r_pad32 / 32), dim3(64), 0, s, a, h);
-  else
-    hipLaunchKernelGGL(unfused_stage1_kernel<false>, dim3(tiles, g.r_pad32 / 32), dim3(64), 0, s, a, h);
+  auto s1 = act_codes_fp8(a.m) ? unfused_stage1_kernel<true> : unfused_stage1_kernel<false>;
+  e = hipFuncSetAttribute(reinterpret_cast<const void *>(s1),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, kS1Lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(s1, dim3(tiles, g.r_pad32 / 32), dim3(64 * kS1Waves), kS1Lds, s, a, h);
   // 3. re-quantization: Q_H and s_H to global memory
   const int64_t waves = (int64_t)m32 * (g.r_pad64 / 64);
   hipLaunchKernelGGL(unfused_requant_kernel, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s, h,
