@@ -62,7 +62,8 @@ typedef enum {
     TQ_ERR_DTYPE = 5,   /* unknown output dtype                              */
     TQ_ERR_ALIGN = 6,   /* a device pointer is not 16-byte aligned           */
     TQ_ERR_BUFFER = 7,  /* descriptor inconsistent / not initialised         */
-    TQ_ERR_HIP = 8      /* the HIP runtime reported an error on launch       */
+    TQ_ERR_HIP = 8,     /* the HIP runtime reported an error on launch       */
+    TQ_ERR_TOO_LARGE = 9 /* needs more scratch than the static buffer holds  */
 } tq_status;
 
 typedef enum { TQ_F16 = 0, TQ_BF16 = 1 } tq_dtype;
@@ -203,6 +204,28 @@ size_t tq_unfused_scratch_bytes(const tq_weight_desc *d, int m);
 tq_status tq_dual_gemm_unfused(const tq_weight_desc *d, const void *packed, const void *x_codes,
                                const void *x_scales, int m, void *y, tq_dtype y_dtype,
                                void *scratch, void *stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the layer
+ * without fusion exactly as tq_dual_gemm_unfused computes it (same kernels,
+ * same Y, H, s_H and Q_H), but its scratch is a static device array of
+ * TQ_NOALLOC_SCRATCH_BYTES inside the library instead of a caller buffer.
+ * Every device the library runs on holds one copy of that array until the
+ * process ends; its address is looked up on the first call for a device
+ * (the device of `stream`, or the current device for the NULL stream).  The
+ * call allocates nothing and needs no initial contents in the array.
+ *   limits  tq_unfused_scratch_bytes(d, m) <= TQ_NOALLOC_SCRATCH_BYTES (8 MiB:
+ *           e.g. r = 128 up to m = 12928 tokens, r = 64 up to m = 25888),
+ *           TQ_ERR_TOO_LARGE otherwise (checked before anything is launched)
+ *   races   every call on one device shares that device's array: calls that
+ *           may overlap in time on one device (other streams, other host
+ *           threads) race and must be serialized by the caller; calls on one
+ *           stream never overlap
+ * Other arguments and errors as tq_dual_gemm_unfused (no scratch argument). */
+#define TQ_NOALLOC_SCRATCH_BYTES (8u << 20)
+tq_status tq_dual_gemm_unfused_noalloc(const tq_weight_desc *d, const void *packed,
+                                       const void *x_codes, const void *x_scales, int m, void *y,
+                                       tq_dtype y_dtype, void *stream);
 
 /* Copy the packed weights out in the canonical layout (for tests/debug):
  *   w_codes  [n, k/8] TQ4 words      w_scales  [n, k/group] fp16

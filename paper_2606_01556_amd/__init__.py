@@ -19,7 +19,9 @@ GROUP = 64
 
 TQ_F16, TQ_BF16 = 0, 1
 STATUS = {0: "TQ_OK", 1: "TQ_ERR_NULL", 2: "TQ_ERR_SHAPE", 3: "TQ_ERR_GROUP", 4: "TQ_ERR_RANK",
-          5: "TQ_ERR_DTYPE", 6: "TQ_ERR_ALIGN", 7: "TQ_ERR_BUFFER", 8: "TQ_ERR_HIP"}
+          5: "TQ_ERR_DTYPE", 6: "TQ_ERR_ALIGN", 7: "TQ_ERR_BUFFER", 8: "TQ_ERR_HIP",
+          9: "TQ_ERR_TOO_LARGE"}
+NOALLOC_SCRATCH_BYTES = 8 << 20   # TQ_NOALLOC_SCRATCH_BYTES
 
 
 class TQError(RuntimeError):
@@ -39,8 +41,8 @@ class WeightDesc(ctypes.Structure):
 
 EXPORTS = ("tq_weight_desc_init", "tq_pack_weights", "tq_quant_act", "tq_dual_gemm",
            "tq_dual_gemm_debug", "tq_export_weights", "tq_workspace_bytes", "tq_act_codes_bytes",
-           "tq_unfused_scratch_bytes", "tq_dual_gemm_unfused", "tq_dual_gemm_kernel",
-           "tq_status_string")
+           "tq_unfused_scratch_bytes", "tq_dual_gemm_unfused", "tq_dual_gemm_unfused_noalloc",
+           "tq_dual_gemm_kernel", "tq_status_string")
 
 _lib = None
 
@@ -69,6 +71,7 @@ def lib() -> ctypes.CDLL:
         L.tq_unfused_scratch_bytes.argtypes = [D, I]
         L.tq_unfused_scratch_bytes.restype = ctypes.c_size_t
         L.tq_dual_gemm_unfused.argtypes = [D, P, P, P, I, P, I, P, P]
+        L.tq_dual_gemm_unfused_noalloc.argtypes = [D, P, P, P, I, P, I, P]
         L.tq_export_weights.argtypes = [D, P, P, P, P, P, P, P, P]
         L.tq_status_string.argtypes = [I]
         L.tq_status_string.restype = ctypes.c_char_p
@@ -161,6 +164,14 @@ def dual_gemm_unfused(desc: WeightDesc, packed, x_codes, x_scales, m: int, y, sc
     _check(lib().tq_dual_gemm_unfused(ctypes.byref(desc), _ptr(packed), _ptr(x_codes), _ptr(x_scales),
                                       m, _ptr(y), TQ_BF16 if bf16 else TQ_F16, _ptr(scratch),
                                       _stream(stream)), "tq_dual_gemm_unfused")
+
+
+def dual_gemm_unfused_noalloc(desc: WeightDesc, packed, x_codes, x_scales, m: int, y,
+                              bf16: bool = False, stream=None):
+    """tq_dual_gemm_unfused with the library's static scratch (allocates nothing)."""
+    _check(lib().tq_dual_gemm_unfused_noalloc(ctypes.byref(desc), _ptr(packed), _ptr(x_codes),
+                                              _ptr(x_scales), m, _ptr(y), TQ_BF16 if bf16 else TQ_F16,
+                                              _stream(stream)), "tq_dual_gemm_unfused_noalloc")
 
 
 def dual_gemm_debug(desc: WeightDesc, packed, x_codes, x_scales, m: int, y, h, sh, qh, workspace,

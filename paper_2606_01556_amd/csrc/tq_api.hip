@@ -1,7 +1,10 @@
 // C ABI of libtq: argument validation on the host, then one or more kernel
-// launches on the caller's stream.  No allocation, no synchronization, no
-// global state.
+// launches on the caller's stream.  No allocation and no synchronization.
+// The only global state is the static scratch array of
+// tq_dual_gemm_unfused_noalloc and its per-device address, looked up once.
 #include <stdint.h>
+
+#include <mutex>
 
 #include "tq.h"
 #include "tq_kernels.hpp"
@@ -93,12 +96,65 @@ tq_status tq_quant_act(const void *x, int m, int k, int group, void *x_codes, vo
                                          static_cast<hipStream_t>(stream)));
 }
 
+}  // extern "C"
+
+namespace tq {
+// Scratch memory of tq_dual_gemm_unfused_noalloc, for callers that cannot
+// allocate: every device the library runs on holds one copy for the life of
+// the process.  Host code uses it only through the device address that
+// hipGetSymbolAddress returns for the device (static_scratch below).
+__device__ __align__(256) uint8_t scratch[TQ_NOALLOC_SCRATCH_BYTES];
+}  // namespace tq
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices];
+
+// Device address of the static scratch array on the device of `stream` (the
+// current device for the NULL stream), looked up on the first call for that
+// device with the device current, then cached.
+hipError_t static_scratch(hipStream_t stream, void **out) {
+  int cur = 0;
+  hipError_t e = hipGetDevice(&cur);
+  if (e != hipSuccess) return e;
+  int dev = cur;
+  if (stream != nullptr) {
+    hipDevice_t sd = 0;
+    e = hipStreamGetDevice(stream, &sd);
+    if (e != hipSuccess) return e;
+    dev = sd;
+  }
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    if (dev != cur && (e = hipSetDevice(dev)) != hipSuccess) return e;
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(tq::scratch));
+    if (dev != cur) {
+      const hipError_t e2 = hipSetDevice(cur);
+      if (e == hipSuccess) e = e2;
+    }
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
+enum class Path { Fused, Unfused, UnfusedStatic };
+
+}  // namespace
+
+extern "C" {
+
 static tq_status dual_gemm_impl(const tq_weight_desc *d, const void *packed, const void *x_codes,
                                 const void *x_scales, int m, void *y, tq_dtype y_dtype, void *h,
                                 void *sh, void *qh, void *workspace, void *stream,
-                                bool unfused = false) {
+                                Path path = Path::Fused) {
   if (d == nullptr || packed == nullptr || x_codes == nullptr || x_scales == nullptr ||
-      y == nullptr || workspace == nullptr)
+      y == nullptr || (workspace == nullptr && path != Path::UnfusedStatic))
     return TQ_ERR_NULL;
   if (!desc_ok(d)) return TQ_ERR_BUFFER;
   if (m < 0 || m > (1 << 24)) return TQ_ERR_SHAPE;
@@ -107,6 +163,9 @@ static tq_status dual_gemm_impl(const tq_weight_desc *d, const void *packed, con
       !aligned16(workspace))
     return TQ_ERR_ALIGN;
   if (h != nullptr && (!aligned16(h) || !aligned16(sh) || !aligned16(qh))) return TQ_ERR_ALIGN;
+  if (path == Path::UnfusedStatic &&
+      tq::unfused_scratch_bytes(m, geometry(d)) > (size_t)TQ_NOALLOC_SCRATCH_BYTES)
+    return TQ_ERR_TOO_LARGE;
   if (m == 0) return TQ_OK;
   tq::GemmArgs a;
   a.packed = static_cast<const uint8_t *>(packed);
@@ -121,7 +180,12 @@ static tq_status dual_gemm_impl(const tq_weight_desc *d, const void *packed, con
   a.dbg_sh = static_cast<float *>(sh);
   a.dbg_qh = static_cast<int8_t *>(qh);
   a.ws = static_cast<uint32_t *>(workspace);
-  if (unfused)
+  if (path == Path::UnfusedStatic) {
+    const hipError_t e = static_scratch(static_cast<hipStream_t>(stream), &workspace);
+    if (e != hipSuccess) return TQ_ERR_HIP;
+    a.ws = nullptr;
+  }
+  if (path != Path::Fused)
     return hip_status(tq::launch_dual_gemm_unfused(a, workspace, static_cast<hipStream_t>(stream)));
   return hip_status(tq::launch_dual_gemm(a, static_cast<hipStream_t>(stream)));
 }
@@ -166,7 +230,14 @@ tq_status tq_dual_gemm_unfused(const tq_weight_desc *d, const void *packed, cons
                                const void *x_scales, int m, void *y, tq_dtype y_dtype,
                                void *scratch, void *stream) {
   return dual_gemm_impl(d, packed, x_codes, x_scales, m, y, y_dtype, nullptr, nullptr, nullptr,
-                        scratch, stream, true);
+                        scratch, stream, Path::Unfused);
+}
+
+tq_status tq_dual_gemm_unfused_noalloc(const tq_weight_desc *d, const void *packed,
+                                       const void *x_codes, const void *x_scales, int m, void *y,
+                                       tq_dtype y_dtype, void *stream) {
+  return dual_gemm_impl(d, packed, x_codes, x_scales, m, y, y_dtype, nullptr, nullptr, nullptr,
+                        nullptr, stream, Path::UnfusedStatic);
 }
 
 tq_status tq_export_weights(const tq_weight_desc *d, const void *packed, void *w_codes,
@@ -198,6 +269,7 @@ const char *tq_status_string(tq_status s) {
     case TQ_ERR_ALIGN: return "device pointer not 16-byte aligned";
     case TQ_ERR_BUFFER: return "weight descriptor not initialised or inconsistent";
     case TQ_ERR_HIP: return "HIP runtime error on launch";
+    case TQ_ERR_TOO_LARGE: return "the call needs more scratch memory than the static buffer holds";
   }
   return "unknown status";
 }

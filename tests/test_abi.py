@@ -33,8 +33,8 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_status_strings(L):
-    for code in range(0, 9):
-        assert L.tq_status_string(code)
+    for code in range(0, 10):
+        assert L.tq_status_string(code) != b"unknown status"
     assert L.tq_status_string(1234) == b"unknown status"
 
 
@@ -98,6 +98,19 @@ def test_dual_gemm_validation(L):
     d3 = tq.weight_desc_init(128, 128, 16)
     d3.n_pad = 64
     assert L.tq_dual_gemm(D(d3), FAKE, FAKE, FAKE, 4, FAKE, 0, FAKE, None) == 7
+
+
+def test_noalloc_validation(L):
+    """The allocation-free entry point validates on the host and rejects a call
+    whose scratch exceeds the static buffer before touching any device."""
+    d = tq.weight_desc_init(128, 1024, 128)
+    D = ctypes.byref
+    assert L.tq_dual_gemm_unfused_noalloc(D(d), None, FAKE, FAKE, 4, FAKE, 0, None) == 1
+    assert L.tq_dual_gemm_unfused_noalloc(D(d), FAKE, FAKE, FAKE, 4, FAKE, 9, None) == 5
+    assert tq.unfused_scratch_bytes(d, 12928) <= tq.NOALLOC_SCRATCH_BYTES
+    assert tq.unfused_scratch_bytes(d, 12929) > tq.NOALLOC_SCRATCH_BYTES
+    assert L.tq_dual_gemm_unfused_noalloc(D(d), FAKE, FAKE, FAKE, 12929, FAKE, 0, None) == 9
+    assert L.tq_dual_gemm_unfused_noalloc(D(d), FAKE, FAKE, FAKE, 0, FAKE, 0, None) == 0
 
 
 def test_pack_export_validation(L):
