@@ -153,7 +153,7 @@ def config_sweep():
                 def gemm():
                     p = copies[call[0] % ncopy]
                     call[0] += 1
-                    tq.dual_gemm(lay.desc, p, xc, xs, m, Y, lay.workspace, stream=s)
+                    tq.dual_gemm(lay.desc, p, xc, xs, m, Y, stream=s)
 
                 def layer_call():
                     tq.quant_act(X, xc, xs, stream=s)
@@ -216,7 +216,7 @@ def rank_overhead():
                 def gemm():
                     p = copies[call[0] % ncopy]
                     call[0] += 1
-                    tq.dual_gemm(lay.desc, p, xc, xs, m, Y, lay.workspace, stream=s)
+                    tq.dual_gemm(lay.desc, p, xc, xs, m, Y, stream=s)
                 for _ in range(3):
                     gemm()
                 e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -276,7 +276,7 @@ def kernel_choice():
                 def gemm():
                     p = copies[call[0] % ncopy]
                     call[0] += 1
-                    tq.dual_gemm(lay.desc, p, xc, xs, m, Y, lay.workspace, stream=s)
+                    tq.dual_gemm(lay.desc, p, xc, xs, m, Y, stream=s)
                 picked = tq.dual_gemm_kernel(lay.desc, m)
                 res = {}
                 for kname, env in forced:
@@ -380,7 +380,7 @@ def main():
         call[0] += 1
         if ev is not None:
             ev[0].record(stream)
-        tq.dual_gemm(desc, p, xc, xs, m, Y[m], lay.workspace, stream=s)
+        tq.dual_gemm(desc, p, xc, xs, m, Y[m], stream=s)
         if ev is not None:
             ev[1].record(stream)
 
@@ -427,7 +427,7 @@ def main():
         def g():
             p = copies[call[0] % ncopy]
             call[0] += 1
-            tq.dual_gemm(desc, p, xc, xs, m, Y[m], lay.workspace, stream=s)
+            tq.dual_gemm(desc, p, xc, xs, m, Y[m], stream=s)
         us_gemm = timed(g)
         def f16():
             wt = WTs[call[0] % nwt]

@@ -21,9 +21,9 @@
  *
  * Conventions for every entry point:
  *  - All array pointers are DEVICE pointers owned by the caller; the library
- *    never allocates, frees or synchronizes and keeps no global state (the
- *    few bytes of state tq_dual_gemm needs live in the caller's workspace).
- *    Device pointers must be 16-byte aligned (TQ_ERR_ALIGN otherwise).
+ *    never allocates, frees or synchronizes.  Its only global state is the
+ *    static scratch array of tq_dual_gemm_unfused_noalloc.  Device pointers
+ *    must be 16-byte aligned (TQ_ERR_ALIGN otherwise).
  *  - `stream` is a hipStream_t (NULL = the default stream).  Work is enqueued
  *    asynchronously on it; results are visible after the stream completes.
  *  - Arguments are validated on the host before anything is launched; on any
@@ -84,7 +84,8 @@ typedef struct {
 /* Validate a layer shape and fill `out` (host only, touches no GPU).
  *   n >= 1 output features, k input features with k % group == 0,
  *   group == 64 (the only group size built), rank r in {0, 8, 16, 32, 64,
- *   128}.  r == 0 is the plain 4-bit linear layer of Sec. 2 Eq. (2).
+ *   128}.  r == 0 is the plain 4-bit linear layer of Sec. 2 Eq. (2).  The
+ *   packed buffer must stay below 4 GiB (TQ_ERR_SHAPE otherwise).
  * Errors: TQ_ERR_NULL, TQ_ERR_SHAPE, TQ_ERR_GROUP, TQ_ERR_RANK. */
 tq_status tq_weight_desc_init(int n, int k, int rank, int group, tq_weight_desc *out);
 
@@ -131,34 +132,34 @@ tq_status tq_quant_act(const void *x, int m, int k, int group, void *x_codes,
  * (0 if m or k is out of range or k % 64 != 0).  Host-only. */
 size_t tq_act_codes_bytes(int m, int k);
 
-/* Size in bytes of the workspace that tq_dual_gemm takes (a constant of the
- * library build; currently 20480). */
-size_t tq_workspace_bytes(void);
-
 /* The fused dual-component layer: residual 4-bit GEMM, low-rank stage 1
  * (H = Q(X) Q(L1)), on-the-fly re-quantization of H, stage 2 (Q_H Q(L2)),
- * and one epilogue that sums both branches and stores Y once.
+ * and one epilogue that sums both branches and stores Y once (Sec. 4.3).
  *   packed            buffer written by tq_pack_weights for descriptor d
  *   x_codes/x_scales  written by tq_quant_act for the same k (m tokens)
  *   y                 [m,n] output, fp16 or bf16 per y_dtype, row-major
- *   workspace         device buffer of tq_workspace_bytes() bytes, owned by
- *                     the caller and zero-filled before its first use; every
- *                     call leaves its counters at zero, so it stays ready
- *                     for the next call of any layer.  Calls that share a
- *                     workspace must not run concurrently (calls on one
- *                     stream never do); give each stream its own.  At
- *                     m <= 16 the work-groups of the launch hand H from the
- *                     ones that form it to the others through it; larger m
- *                     keep H on chip and do not touch it.
- * One kernel launch.  m == 0 is a no-op.  Errors: TQ_ERR_NULL, TQ_ERR_SHAPE,
- * TQ_ERR_BUFFER, TQ_ERR_DTYPE, TQ_ERR_ALIGN, TQ_ERR_HIP. */
+ * One kernel launch; H, s_H and Q_H never leave the chip (registers and LDS
+ * of each work-group).  No workspace and no state: calls may run
+ * concurrently on any streams.  m == 0 is a no-op.  Errors: TQ_ERR_NULL,
+ * TQ_ERR_SHAPE, TQ_ERR_BUFFER, TQ_ERR_DTYPE, TQ_ERR_ALIGN, TQ_ERR_HIP. */
 tq_status tq_dual_gemm(const tq_weight_desc *d, const void *packed, const void *x_codes,
-                       const void *x_scales, int m, void *y, tq_dtype y_dtype, void *workspace,
-                       void *stream);
+                       const void *x_scales, int m, void *y, tq_dtype y_dtype, void *stream);
+
+/* The fused layer with the activation quantizer inside the same launch
+ * (Sec. 4.3: the kernel quantizes the activation tile once and feeds the
+ * codes to both branches): x is the fp16 activation [m,k], row-major.  Each
+ * work-group quantizes X into its own LDS with the arithmetic of
+ * tq_quant_act (bit-identical codes and scales), so nothing but Y is
+ * written.  For decode-sized calls: 1 <= m <= 16 and the codes of m tokens
+ * must fit the kernel's LDS (m = 1: k <= 114688; m = 2: k <= 57344;
+ * m <= 8: k <= 28672; m <= 16: k <= 14336); TQ_ERR_SHAPE otherwise.
+ * Errors as tq_dual_gemm. */
+tq_status tq_dual_gemm_fused_quant(const tq_weight_desc *d, const void *packed, const void *x,
+                                   int m, void *y, tq_dtype y_dtype, void *stream);
 
 /* Kernels of tq_dual_gemm. */
 typedef enum {
-  TQ_KERNEL_DECODE = 0,   /* m <= 16: weight-streaming, H handed over in the workspace */
+  TQ_KERNEL_DECODE = 0,   /* m <= 16: weight-streaming, H formed in every work-group */
   TQ_KERNEL_MID = 1,      /* 32-token blocks, K split over wavefronts */
   TQ_KERNEL_LARGE = 2,    /* 128 x 256 blocks, H in the main loop */
   TQ_KERNEL_PREFILL = 3   /* 128 x 256 blocks, H in a separate pass */
@@ -166,6 +167,8 @@ typedef enum {
 
 /* The kernel tq_dual_gemm launches for descriptor d and m tokens (a tq_kernel
  * value), or -1 for a NULL or invalid descriptor or m outside [1, 2^24].
+ * (Decode-sized m whose activation codes exceed the decode kernel's LDS --
+ * e.g. m = 16 with k > 14336 -- run the mid kernel.)
  * Host-only; launches nothing.  Every kernel returns the same codes, H, s_H
  * and Q_H; the large and prefill kernels also sum each output in the order of
  * the fp64 definition's fp32 evaluation (ascending K-groups, then the
@@ -174,15 +177,26 @@ typedef enum {
  * tolerance the fp32 accumulation allows). */
 int tq_dual_gemm_kernel(const tq_weight_desc *d, int m);
 
-/* Same computation and kernel as tq_dual_gemm, for tests: additionally
- * copies the low-rank intermediate of every token out of the kernel.
- *   h   [m,r] fp32     H before re-quantization
- *   sh  [m,r/group_r]  fp32 scales s_H
- *   qh  [m,r] int8     codes Q_H in [-7, 7]
- * Errors as tq_dual_gemm; additionally TQ_ERR_RANK when r == 0. */
+/* The same computation as tq_dual_gemm, for tests and measurements:
+ *   x          NULL: the activations are x_codes / x_scales as in
+ *              tq_dual_gemm; otherwise (x_codes and x_scales NULL) the fp16
+ *              activation [m,k] of tq_dual_gemm_fused_quant, quantized in the
+ *              kernel (kernel must then be -1 or TQ_KERNEL_DECODE)
+ *   kernel     -1: the kernel tq_dual_gemm would launch; otherwise the
+ *              tq_kernel value to run (TQ_KERNEL_DECODE needs a decode-sized
+ *              m that fits its LDS, TQ_KERNEL_LARGE / TQ_KERNEL_PREFILL need
+ *              m > 512, TQ_KERNEL_MID serves any m; TQ_ERR_SHAPE otherwise)
+ *   mid_tiles  0: the mid kernel's own choice of 32-column tiles per
+ *              work-group; 1, 2 or 4 forces it (TQ_ERR_SHAPE otherwise)
+ *   h, sh, qh  all NULL, or all set (r > 0, else TQ_ERR_RANK) to copy the
+ *              low-rank intermediate of every token out of the kernel:
+ *                h   [m,r] fp32     H before re-quantization
+ *                sh  [m,r/group_r]  fp32 scales s_H
+ *                qh  [m,r] int8     codes Q_H in [-7, 7]
+ * Errors as tq_dual_gemm. */
 tq_status tq_dual_gemm_debug(const tq_weight_desc *d, const void *packed, const void *x_codes,
-                             const void *x_scales, int m, void *y, tq_dtype y_dtype,
-                             void *h, void *sh, void *qh, void *workspace, void *stream);
+                             const void *x_scales, const void *x, int m, void *y, tq_dtype y_dtype,
+                             int kernel, int mid_tiles, void *h, void *sh, void *qh, void *stream);
 
 /* The same layer without kernel fusion, the comparison baseline of the
  * paper's kernel profile (Appendix, Kernel Profile; Sec. 4.3 names the

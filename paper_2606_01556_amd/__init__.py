@@ -40,9 +40,9 @@ class WeightDesc(ctypes.Structure):
 
 
 EXPORTS = ("tq_weight_desc_init", "tq_pack_weights", "tq_quant_act", "tq_dual_gemm",
-           "tq_dual_gemm_debug", "tq_export_weights", "tq_workspace_bytes", "tq_act_codes_bytes",
-           "tq_unfused_scratch_bytes", "tq_dual_gemm_unfused", "tq_dual_gemm_unfused_noalloc",
-           "tq_dual_gemm_kernel", "tq_status_string")
+           "tq_dual_gemm_fused_quant", "tq_dual_gemm_debug", "tq_export_weights",
+           "tq_act_codes_bytes", "tq_unfused_scratch_bytes", "tq_dual_gemm_unfused",
+           "tq_dual_gemm_unfused_noalloc", "tq_dual_gemm_kernel", "tq_status_string")
 
 _lib = None
 
@@ -60,10 +60,9 @@ def lib() -> ctypes.CDLL:
         L.tq_weight_desc_init.argtypes = [I, I, I, I, D]
         L.tq_pack_weights.argtypes = [D, P, P, P, P, P]
         L.tq_quant_act.argtypes = [P, I, I, I, P, P, P]
-        L.tq_dual_gemm.argtypes = [D, P, P, P, I, P, I, P, P]
-        L.tq_dual_gemm_debug.argtypes = [D, P, P, P, I, P, I, P, P, P, P, P]
-        L.tq_workspace_bytes.argtypes = []
-        L.tq_workspace_bytes.restype = ctypes.c_size_t
+        L.tq_dual_gemm.argtypes = [D, P, P, P, I, P, I, P]
+        L.tq_dual_gemm_fused_quant.argtypes = [D, P, P, I, P, I, P]
+        L.tq_dual_gemm_debug.argtypes = [D, P, P, P, P, I, P, I, I, I, P, P, P, P]
         L.tq_act_codes_bytes.argtypes = [I, I]
         L.tq_act_codes_bytes.restype = ctypes.c_size_t
         L.tq_dual_gemm_kernel.argtypes = [D, I]
@@ -76,7 +75,7 @@ def lib() -> ctypes.CDLL:
         L.tq_status_string.argtypes = [I]
         L.tq_status_string.restype = ctypes.c_char_p
         for name in EXPORTS:
-            if name not in ("tq_workspace_bytes", "tq_act_codes_bytes", "tq_unfused_scratch_bytes",
+            if name not in ("tq_act_codes_bytes", "tq_unfused_scratch_bytes",
                             "tq_dual_gemm_kernel", "tq_status_string"):
                 getattr(L, name).restype = I
         _lib = L
@@ -106,6 +105,40 @@ def _stream(stream):
     return stream.cuda_stream
 
 
+# ------------------------------------------------------------------ argument checks
+# Every wrapper below checks its tensors before the C call: the library sees
+# only raw pointers and would read or write out of bounds on a wrong shape.
+def _tensor(t, name, dtype=None, shape=None, min_bytes=None):
+    if t is None:
+        raise ValueError(f"{name}: missing")
+    if isinstance(t, int):
+        return                          # a raw device address: the caller vouches for it
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name}: expected a torch tensor, got {type(t).__name__}")
+    if not t.is_cuda:
+        raise ValueError(f"{name}: must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name}: dtype {t.dtype}, expected {dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if min_bytes is not None and t.numel() * t.element_size() < min_bytes:
+        raise ValueError(f"{name}: {t.numel() * t.element_size()} bytes, needs {min_bytes}")
+
+
+def _act_checks(desc, x_codes, x_scales, m):
+    k = desc.k
+    _tensor(x_codes, "x_codes", min_bytes=act_codes_bytes(m, k))
+    _tensor(x_scales, "x_scales", min_bytes=(k // GROUP) * padded_tokens(m) * 2)
+
+
+def _y_check(desc, y, m, bf16):
+    import torch
+    _tensor(y, "y", torch.bfloat16 if bf16 else torch.float16, (m, desc.n))
+
+
 # ------------------------------------------------------------------ C ABI
 def weight_desc_init(n: int, k: int, rank: int, group: int = GROUP) -> WeightDesc:
     d = WeightDesc()
@@ -114,25 +147,52 @@ def weight_desc_init(n: int, k: int, rank: int, group: int = GROUP) -> WeightDes
 
 
 def pack_weights(desc: WeightDesc, w_res, l1, l2, packed, stream=None):
+    import torch
+    f16 = torch.float16
+    _tensor(w_res, "w_res", f16, (desc.n, desc.k))
+    if desc.rank:
+        _tensor(l1, "l1", f16, (desc.k, desc.rank))
+        _tensor(l2, "l2", f16, (desc.rank, desc.n))
+    _tensor(packed, "packed", min_bytes=int(desc.packed_bytes))
     _check(lib().tq_pack_weights(ctypes.byref(desc), _ptr(w_res), _ptr(l1), _ptr(l2), _ptr(packed),
                                  _stream(stream)), "tq_pack_weights")
 
 
 def quant_act(x, x_codes, x_scales, group: int = GROUP, stream=None):
+    import torch
+    _tensor(x, "x", torch.float16)
+    if x.dim() != 2:
+        raise ValueError(f"x: expected [m, k], got shape {tuple(x.shape)}")
     m, k = x.shape
+    _tensor(x_codes, "x_codes", min_bytes=act_codes_bytes(m, k))
+    _tensor(x_scales, "x_scales", min_bytes=(k // GROUP) * padded_tokens(m) * 2)
     _check(lib().tq_quant_act(_ptr(x), m, k, group, _ptr(x_codes), _ptr(x_scales), _stream(stream)),
            "tq_quant_act")
 
 
-def workspace_bytes() -> int:
-    return int(lib().tq_workspace_bytes())
-
-
-def dual_gemm(desc: WeightDesc, packed, x_codes, x_scales, m: int, y, workspace, bf16: bool = False,
+def dual_gemm(desc: WeightDesc, packed, x_codes, x_scales, m: int, y, bf16: bool = False,
               stream=None):
+    _tensor(packed, "packed", min_bytes=int(desc.packed_bytes))
+    _act_checks(desc, x_codes, x_scales, m)
+    _y_check(desc, y, m, bf16)
     _check(lib().tq_dual_gemm(ctypes.byref(desc), _ptr(packed), _ptr(x_codes), _ptr(x_scales), m,
-                              _ptr(y), TQ_BF16 if bf16 else TQ_F16, _ptr(workspace), _stream(stream)),
+                              _ptr(y), TQ_BF16 if bf16 else TQ_F16, _stream(stream)),
            "tq_dual_gemm")
+
+
+def dual_gemm_fused_quant(desc: WeightDesc, packed, x, y, bf16: bool = False, stream=None):
+    """The fused layer from fp16 activations x [m, k], quantized inside the
+    kernel (decode-sized m; tq_dual_gemm_fused_quant)."""
+    import torch
+    _tensor(packed, "packed", min_bytes=int(desc.packed_bytes))
+    _tensor(x, "x", torch.float16)
+    if x.dim() != 2 or x.shape[1] != desc.k:
+        raise ValueError(f"x: expected [m, {desc.k}], got shape {tuple(x.shape)}")
+    m = x.shape[0]
+    _y_check(desc, y, m, bf16)
+    _check(lib().tq_dual_gemm_fused_quant(ctypes.byref(desc), _ptr(packed), _ptr(x), m, _ptr(y),
+                                          TQ_BF16 if bf16 else TQ_F16, _stream(stream)),
+           "tq_dual_gemm_fused_quant")
 
 
 def unfused_scratch_bytes(desc: WeightDesc, m: int) -> int:
@@ -161,6 +221,10 @@ def unfused_parts(desc: WeightDesc, m: int, scratch):
 
 def dual_gemm_unfused(desc: WeightDesc, packed, x_codes, x_scales, m: int, y, scratch,
                       bf16: bool = False, stream=None):
+    _tensor(packed, "packed", min_bytes=int(desc.packed_bytes))
+    _act_checks(desc, x_codes, x_scales, m)
+    _y_check(desc, y, m, bf16)
+    _tensor(scratch, "scratch", min_bytes=unfused_scratch_bytes(desc, m))
     _check(lib().tq_dual_gemm_unfused(ctypes.byref(desc), _ptr(packed), _ptr(x_codes), _ptr(x_scales),
                                       m, _ptr(y), TQ_BF16 if bf16 else TQ_F16, _ptr(scratch),
                                       _stream(stream)), "tq_dual_gemm_unfused")
@@ -169,16 +233,41 @@ def dual_gemm_unfused(desc: WeightDesc, packed, x_codes, x_scales, m: int, y, sc
 def dual_gemm_unfused_noalloc(desc: WeightDesc, packed, x_codes, x_scales, m: int, y,
                               bf16: bool = False, stream=None):
     """tq_dual_gemm_unfused with the library's static scratch (allocates nothing)."""
+    _tensor(packed, "packed", min_bytes=int(desc.packed_bytes))
+    _act_checks(desc, x_codes, x_scales, m)
+    _y_check(desc, y, m, bf16)
     _check(lib().tq_dual_gemm_unfused_noalloc(ctypes.byref(desc), _ptr(packed), _ptr(x_codes),
                                               _ptr(x_scales), m, _ptr(y), TQ_BF16 if bf16 else TQ_F16,
                                               _stream(stream)), "tq_dual_gemm_unfused_noalloc")
 
 
-def dual_gemm_debug(desc: WeightDesc, packed, x_codes, x_scales, m: int, y, h, sh, qh, workspace,
-                    bf16: bool = False, stream=None):
-    _check(lib().tq_dual_gemm_debug(ctypes.byref(desc), _ptr(packed), _ptr(x_codes), _ptr(x_scales), m,
-                                    _ptr(y), TQ_BF16 if bf16 else TQ_F16, _ptr(h), _ptr(sh), _ptr(qh),
-                                    _ptr(workspace), _stream(stream)), "tq_dual_gemm_debug")
+KERNEL_NAMES = ("decode", "mid", "large", "prefill")
+
+
+def dual_gemm_debug(desc: WeightDesc, packed, x_codes, x_scales, m: int, y, h=None, sh=None, qh=None,
+                    bf16: bool = False, kernel: str | None = None, mid_tiles: int = 0, x=None,
+                    stream=None):
+    """tq_dual_gemm_debug: the fused layer with an optional forced kernel
+    (one of KERNEL_NAMES) and mid-kernel tile count, and optional copies of
+    H [m, r] fp32, s_H [m, r/group_r] fp32 and Q_H [m, r] int8.  With x (fp16
+    [m, k]) instead of x_codes / x_scales it runs the fused-quantization
+    path of tq_dual_gemm_fused_quant."""
+    import torch
+    _tensor(packed, "packed", min_bytes=int(desc.packed_bytes))
+    if x is None:
+        _act_checks(desc, x_codes, x_scales, m)
+    else:
+        _tensor(x, "x", torch.float16, (m, desc.k))
+    _y_check(desc, y, m, bf16)
+    if h is not None or sh is not None or qh is not None:
+        r = desc.rank
+        _tensor(h, "h", torch.float32, (m, r))
+        _tensor(sh, "sh", torch.float32, (m, r // max(desc.group_r, 1)))
+        _tensor(qh, "qh", torch.int8, (m, r))
+    kid = -1 if kernel is None else KERNEL_NAMES.index(kernel)
+    _check(lib().tq_dual_gemm_debug(ctypes.byref(desc), _ptr(packed), _ptr(x_codes), _ptr(x_scales),
+                                    _ptr(x), m, _ptr(y), TQ_BF16 if bf16 else TQ_F16, kid, mid_tiles,
+                                    _ptr(h), _ptr(sh), _ptr(qh), _stream(stream)), "tq_dual_gemm_debug")
 
 
 def export_weights(desc: WeightDesc, packed, w_codes, w_scales, l1_codes=None, l1_scales=None,
@@ -194,18 +283,9 @@ def empty_packed(desc: WeightDesc, device="cuda"):
     return torch.empty(int(desc.packed_bytes), dtype=torch.uint8, device=device)
 
 
-def empty_workspace(device="cuda"):
-    """A zero-filled workspace for tq_dual_gemm (one per stream that runs layers)."""
-    import torch
-    return torch.zeros(workspace_bytes(), dtype=torch.uint8, device=device)
-
-
 def padded_tokens(m: int) -> int:
     """m32: the token count rounded up to the 32-token activation tile (at least 32)."""
     return max((m + 31) // 32 * 32, 32)
-
-
-KERNEL_NAMES = ("decode", "mid", "large", "prefill")
 
 
 def dual_gemm_kernel(desc: WeightDesc, m: int) -> str:
@@ -238,9 +318,9 @@ def empty_act(m: int, k: int, device="cuda"):
 
 
 class Layer:
-    """One packed layer: descriptor, packed device buffer and a workspace (device
-    memory from torch).  Calls of one Layer must not overlap in time: run them
-    on one stream, or pass each stream's own workspace to dual_gemm."""
+    """One packed layer: descriptor and packed device buffer (device memory from
+    torch).  Calls may run concurrently on any streams: the layer keeps no
+    per-call state."""
 
     def __init__(self, w_res, l1=None, l2=None, group: int = GROUP, stream=None):
         n, k = w_res.shape
@@ -249,16 +329,19 @@ class Layer:
         self.packed = empty_packed(self.desc, w_res.device)
         pack_weights(self.desc, w_res.contiguous(), None if l1 is None else l1.contiguous(),
                      None if l2 is None else l2.contiguous(), self.packed, stream)
-        self.workspace = empty_workspace(w_res.device)
         self.n, self.k, self.rank = n, k, r
 
     def __call__(self, x, bf16: bool = False, stream=None):
+        """Y = layer(x) for fp16 x [m, k]: tq_quant_act, then tq_dual_gemm."""
         import torch
+        _tensor(x, "x", torch.float16)
+        if x.dim() != 2 or x.shape[1] != self.k:
+            raise ValueError(f"x: expected [m, {self.k}], got shape {tuple(x.shape)}")
         m = x.shape[0]
         xc, xs = empty_act(m, self.k, x.device)
         y = torch.empty((m, self.n), dtype=torch.bfloat16 if bf16 else torch.float16, device=x.device)
-        quant_act(x.contiguous(), xc, xs, stream=stream)
-        dual_gemm(self.desc, self.packed, xc, xs, m, y, self.workspace, bf16, stream)
+        quant_act(x, xc, xs, stream=stream)
+        dual_gemm(self.desc, self.packed, xc, xs, m, y, bf16, stream)
         return y
 
 

@@ -63,6 +63,8 @@ tq_status tq_weight_desc_init(int n, int k, int rank, int group, tq_weight_desc 
   const uint64_t rgroups = rank == 0 ? 0 : (uint64_t)rank / (uint64_t)d.group_r;
   off = round_up(off + rgroups * (uint64_t)d.n_pad * 2, 256);
   d.packed_bytes = off;
+  // the kernels form offsets inside one packed buffer in 32 bits
+  if (off >= ((uint64_t)1 << 32)) return TQ_ERR_SHAPE;
   *out = d;
   return TQ_OK;
 }
@@ -145,29 +147,51 @@ hipError_t static_scratch(hipStream_t stream, void **out) {
 
 enum class Path { Fused, Unfused, UnfusedStatic };
 
+// What one layer call runs, beyond the common arguments.
+struct Call {
+  Path path = Path::Fused;
+  void *scratch = nullptr;                     // Path::Unfused: the caller's scratch
+  void *h = nullptr, *sh = nullptr, *qh = nullptr;   // optional copies of H, s_H, Q_H
+  int kernel = -1, mid_ct = 0;                 // forced kernel / mid tile count (tests)
+  const void *x16 = nullptr;                   // fp16 activations quantized in the kernel
+};
+
 }  // namespace
 
 extern "C" {
 
 static tq_status dual_gemm_impl(const tq_weight_desc *d, const void *packed, const void *x_codes,
-                                const void *x_scales, int m, void *y, tq_dtype y_dtype, void *h,
-                                void *sh, void *qh, void *workspace, void *stream,
-                                Path path = Path::Fused) {
-  if (d == nullptr || packed == nullptr || x_codes == nullptr || x_scales == nullptr ||
-      y == nullptr || (workspace == nullptr && path != Path::UnfusedStatic))
-    return TQ_ERR_NULL;
+                                const void *x_scales, int m, void *y, tq_dtype y_dtype,
+                                void *stream, const Call &c) {
+  const bool fq = c.x16 != nullptr;
+  if (d == nullptr || packed == nullptr || y == nullptr) return TQ_ERR_NULL;
+  if (!fq && (x_codes == nullptr || x_scales == nullptr)) return TQ_ERR_NULL;
+  if (c.path == Path::Unfused && c.scratch == nullptr) return TQ_ERR_NULL;
+  const int ndbg = (c.h != nullptr) + (c.sh != nullptr) + (c.qh != nullptr);
+  if (ndbg != 0 && ndbg != 3) return TQ_ERR_NULL;
   if (!desc_ok(d)) return TQ_ERR_BUFFER;
   if (m < 0 || m > (1 << 24)) return TQ_ERR_SHAPE;
   if (y_dtype != TQ_F16 && y_dtype != TQ_BF16) return TQ_ERR_DTYPE;
+  if (ndbg == 3 && d->rank == 0) return TQ_ERR_RANK;
   if (!aligned16(packed) || !aligned16(x_codes) || !aligned16(x_scales) || !aligned16(y) ||
-      !aligned16(workspace))
+      !aligned16(c.scratch) || !aligned16(c.x16))
     return TQ_ERR_ALIGN;
-  if (h != nullptr && (!aligned16(h) || !aligned16(sh) || !aligned16(qh))) return TQ_ERR_ALIGN;
-  if (path == Path::UnfusedStatic &&
+  if (ndbg == 3 && (!aligned16(c.h) || !aligned16(c.sh) || !aligned16(c.qh))) return TQ_ERR_ALIGN;
+  if (fq && m > 0 && (m > tq::kDecodeMaxTokens || !tq::decode_fits(m, d->k))) return TQ_ERR_SHAPE;
+  if (c.kernel < -1 || c.kernel > tq::kKernelPrefill) return TQ_ERR_SHAPE;
+  if (c.mid_ct != 0 && c.mid_ct != 1 && c.mid_ct != 2 && c.mid_ct != 4) return TQ_ERR_SHAPE;
+  if (m > 0) {
+    // a forced kernel must be one that serves m tokens
+    if (c.kernel == tq::kKernelDecode && (m > tq::kDecodeMaxTokens || !tq::decode_fits(m, d->k)))
+      return TQ_ERR_SHAPE;
+    if ((c.kernel == tq::kKernelLarge || c.kernel == tq::kKernelPrefill) && !tq::act_codes_fp8(m))
+      return TQ_ERR_SHAPE;
+  }
+  if (c.path == Path::UnfusedStatic &&
       tq::unfused_scratch_bytes(m, geometry(d)) > (size_t)TQ_NOALLOC_SCRATCH_BYTES)
     return TQ_ERR_TOO_LARGE;
   if (m == 0) return TQ_OK;
-  tq::GemmArgs a;
+  tq::GemmArgs a{};
   a.packed = static_cast<const uint8_t *>(packed);
   a.geo = geometry(d);
   a.xc = static_cast<const uint32_t *>(x_codes);
@@ -176,21 +200,21 @@ static tq_status dual_gemm_impl(const tq_weight_desc *d, const void *packed, con
   a.m = m;
   a.ms = (m + 31) / 32 * 32;
   a.bf16_out = y_dtype == TQ_BF16;
-  a.dbg_h = static_cast<float *>(h);
-  a.dbg_sh = static_cast<float *>(sh);
-  a.dbg_qh = static_cast<int8_t *>(qh);
-  a.ws = static_cast<uint32_t *>(workspace);
-  if (path == Path::UnfusedStatic) {
-    const hipError_t e = static_scratch(static_cast<hipStream_t>(stream), &workspace);
-    if (e != hipSuccess) return TQ_ERR_HIP;
-    a.ws = nullptr;
+  a.dbg_h = static_cast<float *>(c.h);
+  a.dbg_sh = static_cast<float *>(c.sh);
+  a.dbg_qh = static_cast<int8_t *>(c.qh);
+  a.force_kernel = c.kernel;
+  a.mid_ct = c.mid_ct;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (fq) return hip_status(tq::launch_dual_gemm_decode(a, static_cast<const uint16_t *>(c.x16), s));
+  if (c.path == Path::Unfused) return hip_status(tq::launch_dual_gemm_unfused(a, c.scratch, s));
+  if (c.path == Path::UnfusedStatic) {
+    void *scr = nullptr;
+    if (static_scratch(s, &scr) != hipSuccess) return TQ_ERR_HIP;
+    return hip_status(tq::launch_dual_gemm_unfused(a, scr, s));
   }
-  if (path != Path::Fused)
-    return hip_status(tq::launch_dual_gemm_unfused(a, workspace, static_cast<hipStream_t>(stream)));
-  return hip_status(tq::launch_dual_gemm(a, static_cast<hipStream_t>(stream)));
+  return hip_status(tq::launch_dual_gemm(a, s));
 }
-
-size_t tq_workspace_bytes(void) { return tq::kWorkspaceBytes; }
 
 int tq_dual_gemm_kernel(const tq_weight_desc *d, int m) {
   if (d == nullptr || !desc_ok(d) || m < 1 || m > (1 << 24)) return -1;
@@ -198,6 +222,7 @@ int tq_dual_gemm_kernel(const tq_weight_desc *d, int m) {
   a.geo = geometry(d);
   a.m = m;
   a.ms = (m + 31) / 32 * 32;
+  a.force_kernel = -1;
   return tq::choose_kernel(a);
 }
 
@@ -207,18 +232,34 @@ size_t tq_act_codes_bytes(int m, int k) {
 }
 
 tq_status tq_dual_gemm(const tq_weight_desc *d, const void *packed, const void *x_codes,
-                       const void *x_scales, int m, void *y, tq_dtype y_dtype, void *workspace,
-                       void *stream) {
-  return dual_gemm_impl(d, packed, x_codes, x_scales, m, y, y_dtype, nullptr, nullptr, nullptr,
-                        workspace, stream);
+                       const void *x_scales, int m, void *y, tq_dtype y_dtype, void *stream) {
+  return dual_gemm_impl(d, packed, x_codes, x_scales, m, y, y_dtype, stream, Call{});
+}
+
+tq_status tq_dual_gemm_fused_quant(const tq_weight_desc *d, const void *packed, const void *x,
+                                   int m, void *y, tq_dtype y_dtype, void *stream) {
+  if (x == nullptr) return TQ_ERR_NULL;
+  Call c;
+  c.x16 = x;
+  return dual_gemm_impl(d, packed, nullptr, nullptr, m, y, y_dtype, stream, c);
 }
 
 tq_status tq_dual_gemm_debug(const tq_weight_desc *d, const void *packed, const void *x_codes,
-                             const void *x_scales, int m, void *y, tq_dtype y_dtype, void *h,
-                             void *sh, void *qh, void *workspace, void *stream) {
-  if (h == nullptr || sh == nullptr || qh == nullptr) return TQ_ERR_NULL;
-  if (d != nullptr && d->rank == 0) return TQ_ERR_RANK;
-  return dual_gemm_impl(d, packed, x_codes, x_scales, m, y, y_dtype, h, sh, qh, workspace, stream);
+                             const void *x_scales, const void *x, int m, void *y, tq_dtype y_dtype,
+                             int kernel, int mid_tiles, void *h, void *sh, void *qh, void *stream) {
+  Call c;
+  if (x != nullptr) {
+    // the fused-quantization path: no codes, and only the decode kernel
+    if (x_codes != nullptr || x_scales != nullptr) return TQ_ERR_SHAPE;
+    if (kernel != -1 && kernel != tq::kKernelDecode) return TQ_ERR_SHAPE;
+    c.x16 = x;
+  }
+  c.kernel = kernel;
+  c.mid_ct = mid_tiles;
+  c.h = h;
+  c.sh = sh;
+  c.qh = qh;
+  return dual_gemm_impl(d, packed, x_codes, x_scales, m, y, y_dtype, stream, c);
 }
 
 size_t tq_unfused_scratch_bytes(const tq_weight_desc *d, int m) {
@@ -229,15 +270,18 @@ size_t tq_unfused_scratch_bytes(const tq_weight_desc *d, int m) {
 tq_status tq_dual_gemm_unfused(const tq_weight_desc *d, const void *packed, const void *x_codes,
                                const void *x_scales, int m, void *y, tq_dtype y_dtype,
                                void *scratch, void *stream) {
-  return dual_gemm_impl(d, packed, x_codes, x_scales, m, y, y_dtype, nullptr, nullptr, nullptr,
-                        scratch, stream, Path::Unfused);
+  Call c;
+  c.path = Path::Unfused;
+  c.scratch = scratch;
+  return dual_gemm_impl(d, packed, x_codes, x_scales, m, y, y_dtype, stream, c);
 }
 
 tq_status tq_dual_gemm_unfused_noalloc(const tq_weight_desc *d, const void *packed,
                                        const void *x_codes, const void *x_scales, int m, void *y,
                                        tq_dtype y_dtype, void *stream) {
-  return dual_gemm_impl(d, packed, x_codes, x_scales, m, y, y_dtype, nullptr, nullptr, nullptr,
-                        nullptr, stream, Path::UnfusedStatic);
+  Call c;
+  c.path = Path::UnfusedStatic;
+  return dual_gemm_impl(d, packed, x_codes, x_scales, m, y, y_dtype, stream, c);
 }
 
 tq_status tq_export_weights(const tq_weight_desc *d, const void *packed, void *w_codes,

@@ -108,6 +108,53 @@ __device__ __forceinline__ v4f mfma_codes_16x16x128(v8i a, v8i b) {
   return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, z, 0, 0, 0, kScale2p9, 0, kScale2p9);
 }
 
+// Activation quantizer step shared by the quantizer kernel and the decode
+// kernel's fp16 entry: eight lanes own one 64-value group, eight values each.
+// max over the 8 lanes 8 j .. 8 j + 7 with DPP lane swizzles: swap neighbours,
+// swap pairs, then mirror the two quads of the eight
+__device__ __forceinline__ float max8_dpp(float a) {
+  a = fmaxf(a, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, a), 0xB1, 0xF, 0xF, false)));
+  a = fmaxf(a, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, a), 0x4E, 0xF, 0xF, false)));
+  a = fmaxf(a, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, a), 0x141, 0xF, 0xF, false)));
+  return a;
+}
+
+// Codes of eight fp16 values v of one group with fp16 scale s (s > 0, or 0
+// for a group that quantizes to zeros), as fp8 operand bytes: lo holds codes
+// 0..3, hi codes 4..7.  y is 1 / s to within a few ulp (0 when s == 0).
+//
+// For fp16 v and s the exact quotient v / s is either a half-integer or at
+// least 2.4e-4 away from every half-integer (write v = A 2^p, s = B 2^q with
+// |A|, B < 2^11: a non-zero distance is a multiple of 2^(min(p+1, q) - q) /
+// (2B)), so rounding t = v * y to the nearest integer already gives
+// rint(v / s) except on exact ties.  A tie shows in the exact remainder
+// r = v - rint(t) s (one fma; the product and the difference are exact in
+// fp32) as |r| = s / 2, and round-half-to-even then takes 2 rint(t / 2), the
+// even one of the two neighbours (t / 2 lies within rounding error of an odd
+// multiple of 1/4, far from any rounding boundary).  This is the remainder
+// correction of Markstein's division method, specialised to a quotient needed
+// only to the nearest integer.  The clamped code q becomes the byte
+// sign << 7 | |q| as the e4m3 value q 2^-9 (a subnormal, converted exactly;
+// the fma adds +0 so a zero code is never -0).
+__device__ __forceinline__ void quant8_fp8(const float (&v)[8], float s, float y, uint32_t &lo,
+                                           uint32_t &hi) {
+  const float hs = 0.5f * s;
+  float f[8];
+#pragma unroll
+  for (int e = 0; e < 8; e++) {
+    const float t = v[e] * y;
+    const float q = __builtin_rintf(t);
+    const float r = fmaf(-q, s, v[e]);
+    const float qe = 2.0f * __builtin_rintf(0.5f * t);
+    const float c = fminf(fmaxf(fabsf(r) == hs ? qe : q, -7.0f), 7.0f);
+    f[e] = fmaf(c, 0x1p-9f, 0.0f);
+  }
+  lo = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(f[0], f[1], 0, false);
+  lo = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(f[2], f[3], (int)lo, true);
+  hi = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(f[4], f[5], 0, false);
+  hi = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(f[6], f[7], (int)hi, true);
+}
+
 __device__ __forceinline__ int row_of_32x32(int lane, int v) {
   return 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
 }

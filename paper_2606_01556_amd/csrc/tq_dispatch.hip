@@ -1,12 +1,10 @@
 // Kernel selection for the fused layer by token count: the decode kernel for
-// m <= 16 (bound by the weight bytes and by H's K-long chain), the mid kernel
+// m <= 16 (bound by the weight bytes; H formed in every work-group), the mid kernel
 // (32-token blocks, H formed per block) up to 512 tokens, then the large
 // kernel (128 x 256 blocks, 16 wavefronts), or for r > 64 once its blocks
 // take more than one round over the CUs the prefill kernel (H shared by runs
 // of column blocks); past 512 tokens the mid kernel again where the large
 // kernel's blocks would leave most CUs idle.
-#include <stdlib.h>
-
 #include "tq_kernels.hpp"
 
 namespace tq {
@@ -15,8 +13,9 @@ namespace tq {
 constexpr int kLargeRound = 28;
 
 int choose_kernel(const GemmArgs &a) {
+  if (a.force_kernel >= 0) return a.force_kernel;   // validated by the caller
   // the activation code format follows the same token-count split
-  if (a.m <= 16) return kKernelDecode;
+  if (a.m <= kDecodeMaxTokens && decode_fits(a.m, a.geo.k)) return kKernelDecode;
   if (!act_codes_fp8(a.m)) return kKernelMid;
   // 128 x 256 blocks: the large kernel (16 wavefronts, H formed in the main
   // loop of every block) is faster while its blocks fit in one round over the
@@ -24,26 +23,19 @@ int choose_kernel(const GemmArgs &a) {
   // quarter of a block's work); beyond, the prefill kernel forms H once per
   // run of column blocks
   const int blocks = (a.m + 127) / 128 * ((a.geo.n_pad + 255) / 256);
-  int large = blocks <= 256 || a.geo.r_pad32 <= 64;
+  const bool large = blocks <= 256 || a.geo.r_pad32 <= 64;
   // Few large blocks leave most CUs idle (a round of them costs about as much
   // as kLargeRound tile-group units of the mid kernel, whose 32-token blocks
   // fill the CUs at these sizes too): take the cheaper of the two.
   const int rounds = (blocks + 255) / 256;
-  bool mid = large && dual_gemm_mid_cost(a) < rounds * kLargeRound;
-  // TQ_LARGE=0|1 forces either large-m kernel, TQ_MID=1 the mid kernel (the
-  // tests run all three on the same shapes)
-  if (const char *lenv = getenv("TQ_LARGE")) {
-    large = atoi(lenv);
-    mid = false;
-  }
-  if (const char *menv = getenv("TQ_MID")) mid = atoi(menv) != 0;
+  const bool mid = large && dual_gemm_mid_cost(a) < rounds * kLargeRound;
   if (mid) return kKernelMid;
   return large ? kKernelLarge : kKernelPrefill;
 }
 
 hipError_t launch_dual_gemm(const GemmArgs &a, hipStream_t s) {
   switch (choose_kernel(a)) {
-    case kKernelDecode: return launch_dual_gemm_decode(a, s);
+    case kKernelDecode: return launch_dual_gemm_decode(a, nullptr, s);
     case kKernelMid: return launch_dual_gemm_mid(a, s);
     case kKernelLarge: return launch_dual_gemm_large(a, s);
     default: return launch_dual_gemm_prefill(a, s);

@@ -1,92 +1,104 @@
 // Fused dual-component W4A4 layer (paper Sec. 4.3) for decode-sized token
 // counts (m <= 16): the residual 4-bit GEMM, the stage-1 product
-// H = Q(X) Q(L1), its re-quantization, stage 2 Q_H Q(L2) and one epilogue,
-// in one kernel.  At these sizes the layer is bound by the bytes of the
-// packed weights and by the latency of H's K-long chain (one fp32 fma per
-// K-group, in ascending group order, so that Q_H is bit-exact).
+// H = Q(X) Q(L1), its on-chip re-quantization, stage 2 Q_H Q(L2) and one
+// epilogue, in one kernel.  Nothing of the layer leaves the chip but Y.
 //
-// Work decomposition.  Forming H in every work-group would read all of L1
-// (K x r codes) once per work-group and put the K-long chain in front of
-// every tile, so H is formed once per call:
-//  * Work-groups 0 .. ceil(r / 16) - 1 are H producers, one per 16-rank tile
-//    of H.  Work-groups are dispatched in index order, so the producers are
-//    running before any work-group that waits for them; they wait for nothing
-//    themselves.  (The wait is bounded all the same: a work-group that gives
-//    up sets an error word in the workspace instead of hanging.)
-//  * Each producer writes its fp32 H tile to the caller's workspace and then
-//    counts itself on a ready counter kept on up to 32 cache lines; column
-//    work-group c polls line c mod 32 (so that few work-groups poll any one
-//    line).
-//  * Every other work-group owns CT 16-column tiles of Y.  It forms its
-//    residual tiles, waits until every producer has counted, reads H,
-//    re-quantizes it in LDS (per token and rank group, s_H in fp32; every
-//    column work-group computes the same Q_H from the same H), runs stage 2
-//    with its L2 columns and stores Y once.
-//  * Flags and H are written with device-scope stores, which complete at the
-//    device's point of coherence; a writer waits for its stores to complete
-//    before it counts itself (no cache write-back, which would touch every
-//    other work-group's lines).  Flags are polled with device-scope loads.  H
-//    is read with ordinary loads: its lines are first touched in this launch
-//    after the count is complete and every launch starts with invalidated
-//    caches, so the column work-groups on one XCD share a fresh copy in L2.
-//  * Column work-groups also count themselves on their line once they have
-//    read H; the last one on a line clears the line's two counts, so every
-//    call leaves the workspace as it found it (zero).
+// Work decomposition.  One work-group of sixteen wavefronts per CU owns CT
+// 16-column tiles of Y and streams their packed weights once.  H is small
+// (m x r) and every work-group forms all of it in its own registers, so no
+// work-group waits for another; the price is that each CU reads all of L1
+// (from L2, where the first reader leaves it) in addition to its columns.
+//  * Wavefront w < ceil(r / 16) owns rank tile w of H and walks every K-group
+//    pair in ascending order, so its fp32 chain (one fma per K-group,
+//    ascending, with the exact scale product s_x s_L1) stays in registers
+//    and H is bit-identical to the oracle's.
+//  * The other wavefronts take the residual work: each owns one or two of
+//    the column tiles and every NPH-th K-group pair (NPH wavefronts share a
+//    tile group); their partial sums are added in a fixed order at the end
+//    (the order of Y's fp32 accumulation is free; H's is not).
+//  * Operands stream from global memory straight into registers, 16 pairs
+//    ahead for a stage-1 wavefront and 16 / (its tiles) pairs ahead for a
+//    residual one, so a CU keeps ~256 KiB of loads in flight (the L1 bytes
+//    come from L2, at its latency); there is no LDS staging and no barrier in
+//    the K loop.  The
+//    activation codes (a few KiB at these sizes) are copied to LDS once, or,
+//    for the fp16 entry point, quantized into LDS by the work-group itself
+//    (Sec. 4.3: the activation tile is quantized once and reused by both
+//    branches), with the same arithmetic as the quantizer kernel.
 //
-// Products.  16 x 16 x 128 fp8 MFMAs over a K-group pair (codes as fp8
-// subnormals, block scales 2^9: exact integer sums); a group's own sum uses
-// the other group's half of the activation operand as zeros.  The exact scale
-// products s_x s_w (and s_x s_L1) come from a 16 x 16 x 16 f16 product with
-// the scales in k = 0.  Wavefront w of a work-group takes the group pairs
-// w, w + 8, w + 16, ... and fetches their operands from global memory straight
-// into registers, four pairs ahead: there is no LDS staging and no barrier in
-// the residual loop.  A producer stages the integer products of up to 64
-// groups and their fp32 scales in LDS; four wavefronts (one for each of a
-// lane's four outputs) then run the ascending-group fma chain over them,
-// forming each scale product s_x s_L1 exactly in fp32 as they go.
-#include <stdlib.h>
-
+// Products.  v_mfma_scale_f32_16x16x128_f8f6f4 on codes as fp8 subnormals
+// (block scales 2^9: exact integer sums).  A K-group pair spans the 128 K of
+// one product, and the two groups need separate sums:
+//  * up to 8 tokens, rows 0-7 take group A's codes in k < 64 and rows 8-15
+//    group B's in k >= 64 (zeros elsewhere), so one product yields both
+//    groups' sums; lanes 32-63 hold group B's and v_permlane32_swap brings
+//    them to lanes 0-31 for the chain;
+//  * up to 16 tokens, rows are tokens and two products take the pair's
+//    groups in turn (the other group's half of the operand zero).
+// Only the accumulator rows that hold real tokens (MV of the four per lane)
+// are rescaled, so single-token decode spends one fma per group and output
+// column, not sixteen.
 #include "tq_device.hpp"
 #include "tq_kernels.hpp"
 
 namespace tq {
 namespace {
 
-typedef _Float16 v4h __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+constexpr int DW = 16;                     // wavefronts per work-group
+constexpr int kDecodeXBytes = 112 * 1024;  // LDS for the activation codes
 
-constexpr int SW = 8;      // wavefronts per work-group
-constexpr int SPD = 4;     // group pairs in flight per wavefront
-constexpr int SCG = 64;    // K-groups per producer chunk
+// Token layouts: MODE 1 / 2 / 4 put two K-groups in one product (rows are
+// (group, token) pairs, up to 8 tokens) with MV = MODE live accumulator rows
+// per lane; MODE 16 takes up to 16 tokens, one group per product.
+template <int MODE>
+struct DMode {
+  static constexpr bool TOK8 = MODE != 16;
+  static constexpr int MV = MODE == 16 ? 4 : MODE;
+  // LDS copy of the activation codes: fp8 operand bytes for one or two tokens,
+  // TQ4 words (unpacked at use) otherwise; MX token slots per K-group
+  static constexpr bool XFP8 = MODE <= 2;
+  static constexpr int MX = MODE == 16 ? 16 : (MODE <= 2 ? MODE : 8);
+  static constexpr int XB = XFP8 ? 64 : 32;   // bytes per (group, token)
+  // pairs of operands in flight per stage-1 wavefront, and the residual
+  // ring's budget in 16-byte fragments (what fits 128 registers unspilled)
+  static constexpr int D1 = MODE == 16 ? 8 : 10;
+  static constexpr int RF = MODE == 1 ? 10 : 8;
+};
 
-// Workspace layout (bytes; every counter on its own 128-byte line):
-constexpr int WS_LINE = 128;
-constexpr int WS_NL = 32;                              // flag / count copies
-constexpr int WS_ERR = 0;                              // set when a wait gave up
-constexpr int WS_READY = WS_LINE;   // line x: producers finished (word 0), column work-groups done (word 1)
-constexpr int WS_H = WS_READY + WS_NL * WS_LINE;       // [16][kMaxRank] fp32 H
-constexpr int WS_END = WS_H + 16 * kMaxRank * 4;
-static_assert(WS_END <= (int)kWorkspaceBytes, "the workspace holds the layout");
-constexpr int kSpinLimit = 1 << 20;   // polls (~1 s at most) before giving up
+// A residual wavefront owns CTW of the work-group's CT column tiles (TG
+// tile groups) and keeps D2 pairs of their operands in flight.
+template <int CT, int RF> struct DRes {
+  static constexpr int CTW = CT == 1 ? 1 : 2;
+  static constexpr int TG = CT / CTW;
+  static constexpr int D2 = RF / CTW;
+};
 
-__device__ __forceinline__ uint32_t *ws_word(uint32_t *ws, int byte) {
-  return reinterpret_cast<uint32_t *>(reinterpret_cast<uint8_t *>(ws) + byte);
-}
-__device__ __forceinline__ uint32_t ld_dev(const uint32_t *p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void st_dev(uint32_t *p, uint32_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ uint32_t add_dev(uint32_t *p) {
-  return __hip_atomic_fetch_add(p, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void add_dev_nr(uint32_t *p) {   // result unused: no return trip
-  (void)__hip_atomic_fetch_add(p, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-// max over runs of n = 8, 16 or 32 lanes (aligned), in every lane of the run:
-// quad permutes and row mirrors (DPP) within a row of 16, the two rows of a
-// 32-lane half from scalar reads
+// LDS layout (bytes): region 0 holds the activation codes during the K loop
+// and, aliased, the epilogue's residual partials, H, Q_H and s_H; the fp32
+// activation scales follow it.
+struct DLayout {
+  int xa, epi_res, epi_h, epi_q, epi_sh, xs, is, total;
+  static constexpr int HSTR = kMaxRank + 1;   // fp32 per H row
+  static constexpr int QSTR = kMaxRank + 16;  // bytes per Q_H row
+  // is_bytes: the two-pass path's int16 integer sums (after the scales)
+  __host__ __device__ DLayout(int kg, int mx, int xb, int ct, int nres, int is_bytes = 0) {
+    const int kgp = (kg + 1) / 2 * 2;
+    xa = kgp * mx * xb + 32;   // + a 32-byte zero pad
+    epi_res = 0;
+    epi_h = nres * ct * 256 * 4 / (ct == 1 ? 1 : ct / 2);   // [NPH][CT][16][16] fp32
+    epi_q = epi_h + 16 * HSTR * 4;
+    epi_sh = epi_q + 16 * QSTR;
+    const int epi_end = epi_sh + 2 * 16 * 4;
+    xs = ((xa > epi_end ? xa : epi_end) + 15) / 16 * 16;
+    is = (xs + kgp * mx * 4 + 15) / 16 * 16;
+    total = is + is_bytes;
+  }
+};
+
+__host__ __device__ inline int rank_tiles(int r) { return (r + 15) / 16; }
+__host__ __device__ inline int res_waves(int r) { return DW - rank_tiles(r); }
+
+// max over runs of n = 8, 16 or 32 aligned lanes, in every lane of the run
 __device__ __forceinline__ float dpp_max(float a, int ctrl_sel) {
   int b;
   switch (ctrl_sel) {
@@ -111,456 +123,626 @@ __device__ __forceinline__ float run_max(float a, int n, int lane) {
   }
   return a;
 }
+
+// lanes 0-31 receive lanes 32-63 of v (lanes 32-63 get their own values back)
+__device__ __forceinline__ float upper_half(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, v),
+                                                  __builtin_bit_cast(uint32_t, v), false, false);
+  return __builtin_bit_cast(float, (uint32_t)r[1]);
+}
+
 __device__ __forceinline__ v8i lds_v8i(const uint8_t *p) {
   const u32x4 lo = *reinterpret_cast<const u32x4 *>(p);
   const u32x4 hi = *reinterpret_cast<const u32x4 *>(p + 16);
   return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
 }
-// Release for device-scope stores: every store the other work-groups read is a
-// device-scope store, which completes at the device's point of coherence, so
-// waiting for this wavefront's stores to complete orders them before a later
-// flag.  (A release fence would also write back the whole L2, ~1 us.)
-__device__ __forceinline__ void wait_dev_stores() {
-  __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
-}
 
-template <int CT>
-struct SCfg {
-  // producer: integer products [4 outputs][SCG / 4][64 lanes][4 groups] fp32,
-  // then scales [16 tokens][SSTR] and [16 ranks][SSTR] fp32 (groups
-  // contiguous, so that the chain reads 4 groups per 16-byte load)
-  static constexpr int SSTR = SCG + 4;
-  static constexpr int P_C = 0;
-  static constexpr int P_SX = SCG * 1024;
-  static constexpr int P_SL = P_SX + 16 * SSTR * 4;
-  static constexpr int P_END = P_SL + 16 * SSTR * 4;
-  // column work-group (aliases the producer region)
-  static constexpr int RES = SW * CT * 1024;                   // [SW][CT][4][64] fp32
-  static constexpr int HSTR = kMaxRank + 1;
-  static constexpr int E_HS = RES;                             // [16][HSTR] fp32
-  static constexpr int QSTR = kMaxRank + 16;
-  static constexpr int E_QS = E_HS + 16 * HSTR * 4;            // [16][QSTR] fp8 codes
-  static constexpr int E_SH = E_QS + 16 * QSTR;                // [2][16] fp32
-  static constexpr int E_END = E_SH + 2 * 16 * 4;
-  static constexpr int LDS = P_END > E_END ? P_END : E_END;
-  static_assert(LDS <= 80 * 1024, "two work-groups fit in the 160 KiB LDS of a CU");
+__device__ __forceinline__ float lo_half(uint32_t w) { return half_bits_to_float((uint16_t)(w & 0xffffu)); }
+__device__ __forceinline__ float hi_half(uint32_t w) { return half_bits_to_float((uint16_t)(w >> 16)); }
+
+// Operands of one K-group pair: for a stage-1 wavefront the fragment of its
+// rank tile with the L1 scales of both groups, for a residual wavefront the
+// CT weight fragments with their scales.
+struct S1Slot {
+  u32x4 l1;
+  uint32_t sla, slb;  // fp16 L1 scales of groups A and B (the lane's rank)
+};
+template <int CTW>
+struct ResSlot {
+  u32x4 w[CTW];
+  uint32_t swa[CTW], swb[CTW];   // fp16 weight scales (TOK8: the lane's own group in swa)
 };
 
-// exact products s_a[row] * s_b[col] of a 16 x 16 tile (lanes 0-15 carry the
-// fp16 scales in k = 0, every other operand element is zero)
-__device__ __forceinline__ v4f outer16(uint32_t sa, uint32_t sb) {
-  const v4f z = {0, 0, 0, 0};
-  const u32x2 a2 = {sa, 0u}, b2 = {sb, 0u};
-  return __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(v4h, a2),
-                                               __builtin_bit_cast(v4h, b2), z, 0, 0, 0);
-}
-
-// Operands of one group pair: raw activation codes (token c16, half q % 2 of
-// group 2p + q / 2), NB raw weight (or L1) fragments of 16 columns, and the
-// fp16 scales of both groups on lanes 0-15.
-template <int NB>
-struct PairOps {
-  u32x4 x;
-  u32x4 b[NB];
-  uint32_t sx1, sx2;
-  uint32_t sb1[NB], sb2[NB];
-};
-
-template <int CT>
-__global__ __launch_bounds__(64 * SW, 4) void dual_gemm_decode_kernel(GemmArgs a, int nprod) {
-  using C = SCfg<CT>;
+// TWO (single token only): the stage-1 wavefronts share all (pair, rank
+// tile) products and park their exact integer sums as int16 in LDS; after
+// the K loop, ceil(16 R / 64) wavefronts run each rank's ascending chain over
+// them.  This spreads the products over ns wavefronts instead of one per
+// rank tile.
+template <int MODE, int CT, bool FQ, bool TWO>
+__global__ __launch_bounds__(64 * DW) void dual_gemm_decode_kernel(GemmArgs a,
+                                                                   const uint16_t *__restrict__ xh,
+                                                                   int ns) {
+  static_assert(!TWO || MODE == 1, "the two-pass path serves a single token");
+  using MD = DMode<MODE>;
+  constexpr int MX = MD::MX, MV = MD::MV, XB = MD::XB;
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
   const Geometry &geo = a.geo;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int q = lane >> 4, c16 = lane & 15;
+  const int q = lane >> 4, c16 = lane & 15, qh = q & 1;
   const int KG = geo.k / kGroup, NP = (KG + 1) / 2;
-  const int m = a.m, ms = a.ms;
+  const int m = a.m;
+  const int r = geo.r, R = rank_tiles(r);
+  const int NS = TWO ? ns : R;    // stage-1 wavefronts
+  const int NRES = DW - NS;
   const int ct16 = geo.n_pad / 16;
-  const int r = geo.r;
-  const int RB = (r + 63) / 64;   // 64-rank blocks of stage 2 (<= 2)
-  uint32_t *ws = a.ws;
-  uint8_t *wsb = reinterpret_cast<uint8_t *>(ws);
-  const uint8_t *xc = reinterpret_cast<const uint8_t *>(a.xc);
-  const uint16_t *xs = a.xs;
+  const int c0 = blockIdx.x * CT;
+  const DLayout LY(KG, MX, XB, CT, NRES, TWO ? NP * R * 64 : 0);
+  int16_t *IS = reinterpret_cast<int16_t *>(smem + LY.is);   // [pair][rank tile][group][16]
+  uint8_t *XA = smem;
+  float *XS = reinterpret_cast<float *>(smem + LY.xs);
   const uint8_t *wcodes = a.packed + geo.off_w;
   const uint16_t *wscales = reinterpret_cast<const uint16_t *>(a.packed + geo.off_ws);
   const uint8_t *l1codes = a.packed + geo.off_l1;
   const uint16_t *l1scales = reinterpret_cast<const uint16_t *>(a.packed + geo.off_l1s);
   const uint8_t *l2codes = a.packed + geo.off_l2;
   const uint16_t *l2scales = reinterpret_cast<const uint16_t *>(a.packed + geo.off_l2s);
-  const int wg = blockIdx.x;
-  const bool producer = wg < nprod;
 
-  // fetch the operands of pair p (p < NP) into o: activation fragment and NB
-  // fragments of the 16-column blocks col16 + j of `blocks`, with their scales
-  // (scale of column c, group g at scales[g * sstride + c])
-  auto fetch = [&](auto &o, int p, const uint8_t *blocks, const uint16_t *scales, int sstride,
-                   int col16, int ncol16) {
-    constexpr int NB = sizeof(o.b) / sizeof(o.b[0]);
-    const int g1 = 2 * p, g2 = min(2 * p + 1, KG - 1);
-    const int gq = (q >> 1) ? g2 : g1;
-    o.x = u32x4{0u, 0u, 0u, 0u};
-    if (c16 < m) o.x = *reinterpret_cast<const u32x4 *>(xc + ((int64_t)gq * 64 + 32 * (q & 1) + c16) * 16);
-    o.sx1 = 0u;
-    o.sx2 = 0u;
-    if (lane < 16) {
-      o.sx1 = xs[(int64_t)g1 * ms + c16];
-      o.sx2 = xs[(int64_t)g2 * ms + c16];
-    }
+  // ---- roles: wavefront w < R forms rank tile w of H over every pair; the
+  // others are residual wavefronts: rslot = w - R owns tile group rslot % TG
+  // and the pairs rslot / TG + i NPH ----
+  using DR = DRes<CT, MD::RF>;
+  constexpr int D1 = MD::D1;
+  constexpr int CTW = DR::CTW, TG = DR::TG, D2 = DR::D2;
+  const bool s1 = wave < NS;
+  const int rslot = wave - NS;
+  const int NPH = NRES / TG;
+  const int tg = s1 ? 0 : rslot % TG, ph = s1 ? 0 : rslot / TG;
+  const bool rbusy = !s1 && ph < NPH;
+  const int nres_it = rbusy && ph < NP ? (NP - ph + NPH - 1) / NPH : 0;
+  const int ctw0 = c0 + tg * CTW;   // first column tile of this residual wavefront
+
+  // Ring loads are unconditional (a pair past the end reloads the last one),
+  // so the compiler can count the outstanding loads and wait only for the
+  // slot it uses.  Lane quarters q < 2 take group A = 2p, q >= 2 group B.
+  // Addresses are a wave-uniform base (pair p) plus a fixed 32-bit lane
+  // offset, so the compiler forms them mostly with scalar adds.  On an odd
+  // tail (group 2p + 1 == KG) the group-B lanes re-read group KG - 1, whose
+  // products the zero activation codes of group KG cancel.
+  const int gq = q >> 1;
+  auto tail_adj = [&](int p) -> uint32_t {
+    return (KG & 1) && p == NP - 1 ? (uint32_t)gq * 1024u : 0u;
+  };
+  const uint32_t l1_lane = (uint32_t)(((wave >> 1) * KG * 64 + gq * 64 + qh * 32 + (wave & 1) * 16 + c16) * 16);
+  const uint32_t l1s_lane = (uint32_t)(16 * wave + c16) * 2;
+  auto load_s1 = [&](S1Slot &S, int p) {
+    S.l1 = *reinterpret_cast<const u32x4 *>(l1codes + (uint32_t)(p * 2048) + (l1_lane - tail_adj(p)));
+    // (section offsets fit 32 bits: the whole packed buffer is below 4 GiB)
+    const uint8_t *sb = reinterpret_cast<const uint8_t *>(l1scales) + (uint32_t)(2 * p * geo.r_pad32 * 2);
+    const uint8_t *sbb = reinterpret_cast<const uint8_t *>(l1scales) + (uint32_t)(min(2 * p + 1, KG - 1) * geo.r_pad32 * 2);
+    S.sla = *reinterpret_cast<const uint16_t *>(sb + l1s_lane);
+    S.slb = *reinterpret_cast<const uint16_t *>(sbb + l1s_lane);
+  };
+  uint32_t w_lane[CTW], ws_lane[CTW];
 #pragma unroll
-    for (int j = 0; j < NB; j++) {
-      const int cj = min(col16 + j, ncol16 - 1);
-      const int L = (q & 1) * 32 + (cj & 1) * 16 + c16;
-      o.b[j] = *reinterpret_cast<const u32x4 *>(blocks + (((int64_t)(cj >> 1) * KG + gq) * 64 + L) * 16);
-      o.sb1[j] = 0u;
-      o.sb2[j] = 0u;
-      if (lane < 16) {
-        o.sb1[j] = scales[(int64_t)g1 * sstride + cj * 16 + c16];
-        o.sb2[j] = scales[(int64_t)g2 * sstride + cj * 16 + c16];
+  for (int j = 0; j < CTW; j++) {
+    const int ct = min(ctw0 + j, ct16 - 1);
+    w_lane[j] = (uint32_t)((((ct >> 1) * KG + gq) * 64 + qh * 32 + (ct & 1) * 16 + c16) * 16);
+    ws_lane[j] = (uint32_t)(16 * ct + c16) * 2;
+  }
+  auto load_res = [&](ResSlot<CTW> &S, int p) {
+    const uint8_t *sa = reinterpret_cast<const uint8_t *>(wscales) + (uint32_t)(2 * p * geo.n_pad * 2);
+    const uint8_t *sbb = reinterpret_cast<const uint8_t *>(wscales) + (uint32_t)(min(2 * p + 1, KG - 1) * geo.n_pad * 2);
+#pragma unroll
+    for (int j = 0; j < CTW; j++) {
+      S.w[j] = *reinterpret_cast<const u32x4 *>(wcodes + (uint32_t)(p * 2048) + (w_lane[j] - tail_adj(p)));
+      if constexpr (MD::TOK8) {
+        // the lane's own group: A for quarters 0-1, B for 2-3
+        S.swa[j] = *reinterpret_cast<const uint16_t *>((gq ? sbb : sa) + ws_lane[j]);
+      } else {
+        S.swa[j] = *reinterpret_cast<const uint16_t *>(sa + ws_lane[j]);
+        S.swb[j] = *reinterpret_cast<const uint16_t *>(sbb + ws_lane[j]);
       }
     }
   };
-  // products of pair p: f(j, g, codes, scale products) for both groups
-  auto products = [&](const auto &o, int p, auto f) {
-    constexpr int NB = sizeof(o.b) / sizeof(o.b[0]);
-    const v8i av = unpack32(o.x);
-    const v8i z = {0, 0, 0, 0, 0, 0, 0, 0};
-    const v8i a1 = q < 2 ? av : z;
-    const v8i a2 = q < 2 ? z : av;
-#pragma unroll
-    for (int j = 0; j < NB; j++) {
-      const v8i b = unpack32(o.b[j]);
-      const v4f m1 = mfma_codes_16x16x128(a1, b);
-      const v4f o1 = outer16(o.sx1, o.sb1[j]);
-      const v4f m2 = mfma_codes_16x16x128(a2, b);
-      const v4f o2 = outer16(o.sx2, o.sb2[j]);
-      f(j, 2 * p, m1, o1);
-      if (2 * p + 1 < KG) f(j, 2 * p + 1, m2, o2);
-    }
-  };
 
-  if (producer) {
-    // ================= H producer: 16-rank tile `wg` =================
-    const int p16 = wg;
-    float *CV = reinterpret_cast<float *>(smem + C::P_C);
-    float *SXL = reinterpret_cast<float *>(smem + C::P_SX);
-    float *SLL = reinterpret_cast<float *>(smem + C::P_SL);
-    const int nchunk = (KG + SCG - 1) / SCG;
-    constexpr int PPC = SCG / 2 / SW;   // pairs per wavefront and chunk (= SPD)
-    static_assert(PPC == SPD, "one chunk of pairs in flight");
-    PairOps<1> F[SPD];
-    // wavefront pair sequence i -> pair SW i + wave; chunk c holds i in [SPD c, SPD c + SPD)
-    const int npw = SPD * nchunk;
+  // ---- the activation codes and scales into LDS (each wavefront runs this
+  // once, after issuing the first loads of its own ring) ----
+  const int KGP = 2 * NP;
+  auto prologue = [&]() {
+    if constexpr (FQ) {
+      // eight lanes per (token, group), eight values each; the steps are those
+      // of the quantizer kernel, so the codes and scales are the same bits
+      const int e = lane & 7;
+      const int nitem = m * KG;
+      for (int it0 = 0; it0 < nitem; it0 += 64 * DW / 8) {
+        const int it = it0 + tid / 8;
+        const bool live = it < nitem;
+        const int t = live ? it / KG : 0, g = live ? it % KG : 0;
+        const u32x4 raw = *reinterpret_cast<const u32x4 *>(xh + (int64_t)t * geo.k + g * kGroup + 8 * e);
+        float v[8];
 #pragma unroll
-    for (int s = 0; s < SPD; s++)
-      if (SW * s + wave < NP) fetch(F[s], SW * s + wave, l1codes, l1scales, geo.r_pad32, p16, geo.r_pad32 / 16);
-    float hacc = 0.0f;
-    for (int c = 0; c < nchunk; c++) {
-#pragma unroll
-      for (int s = 0; s < SPD; s++) {
-        const int i = SPD * c + s;
-        const int p = SW * i + wave;
-        if (p < NP) {
-          const PairOps<1> &o = F[s];
-          const v8i av = unpack32(o.x);
-          const v8i z = {0, 0, 0, 0, 0, 0, 0, 0};
-          const v8i b = unpack32(o.b[0]);
-          const v4f m1 = mfma_codes_16x16x128(q < 2 ? av : z, b);
-          const v4f m2 = mfma_codes_16x16x128(q < 2 ? z : av, b);
-          const int gl1 = 2 * p - SCG * c, gl2 = gl1 + 1;
-          auto cidx = [&](int v, int gl) { return ((v * (SCG / 4) + gl / 4) * 64 + lane) * 4 + gl % 4; };
-#pragma unroll
-          for (int v = 0; v < 4; v++) CV[cidx(v, gl1)] = m1[v];
-          if (2 * p + 1 < KG) {
-#pragma unroll
-            for (int v = 0; v < 4; v++) CV[cidx(v, gl2)] = m2[v];
-          }
-          if (lane < 16) {
-            SXL[c16 * C::SSTR + gl1] = half_bits_to_float((uint16_t)o.sx1);
-            SXL[c16 * C::SSTR + gl2] = half_bits_to_float((uint16_t)o.sx2);
-            SLL[c16 * C::SSTR + gl1] = half_bits_to_float((uint16_t)o.sb1[0]);
-            SLL[c16 * C::SSTR + gl2] = half_bits_to_float((uint16_t)o.sb2[0]);
-          }
+        for (int i = 0; i < 4; i++) {
+          v[2 * i] = half_bits_to_float((uint16_t)(raw[i] & 0xffffu));
+          v[2 * i + 1] = half_bits_to_float((uint16_t)(raw[i] >> 16));
         }
-        const int pn = SW * (i + SPD) + wave;
-        if (i + SPD < npw && pn < NP)
-          fetch(F[s], pn, l1codes, l1scales, geo.r_pad32, p16, geo.r_pad32 / 16);
-      }
-      __syncthreads();   // the chunk's products and scales are in LDS
-      if (wave < 4) {
-        // output v = wave of every lane (token 4q + v, rank 16 p16 + c16),
-        // groups in ascending order, in batches of 8 whose reads (six
-        // 16-byte loads) go before their fmas
-        const int row = 4 * q + wave;
-        const int ng = min(SCG, KG - SCG * c);
-        const float4 *CV4 = reinterpret_cast<const float4 *>(CV) + (wave * (SCG / 4)) * 64 + lane;
-        const float4 *SX4 = reinterpret_cast<const float4 *>(SXL + row * C::SSTR);
-        const float4 *SL4 = reinterpret_cast<const float4 *>(SLL + c16 * C::SSTR);
-        int g0 = 0;
-        for (; g0 + 8 <= ng; g0 += 8) {
-          float4 cv[2], sv[2], lv[2];
-#pragma unroll
-          for (int e = 0; e < 2; e++) {
-            cv[e] = CV4[(g0 / 4 + e) * 64];
-            sv[e] = SX4[g0 / 4 + e];
-            lv[e] = SL4[g0 / 4 + e];
-          }
-#pragma unroll
-          for (int e = 0; e < 8; e++)   // s_x s_L1 is exact in fp32
-            hacc = fmaf(cv[e / 4][e % 4], sv[e / 4][e % 4] * lv[e / 4][e % 4], hacc);
-        }
-        for (; g0 < ng; g0++) {
-          const int gl = g0;
-          hacc = fmaf(CV[((wave * (SCG / 4) + gl / 4) * 64 + lane) * 4 + gl % 4],
-                      SXL[row * C::SSTR + gl] * SLL[c16 * C::SSTR + gl], hacc);
-        }
-      }
-      __syncthreads();   // the chunk's products are consumed
-    }
-    // this tile of H -> workspace; each wavefront waits for its stores, the
-    // barrier orders them before the count
-    float *wsH = reinterpret_cast<float *>(wsb + WS_H);
-    if (wave < 4)
-      __hip_atomic_store(wsH + (4 * q + wave) * kMaxRank + 16 * p16 + c16, hacc, __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_AGENT);
-    wait_dev_stores();
-    __syncthreads();
-    const int ncol = (int)gridDim.x - nprod;
-    if (tid < WS_NL && tid < ncol) add_dev_nr(ws_word(ws, WS_READY + tid * WS_LINE));
-  } else {
-    // ================= column work-group =================
-    const int c0 = (wg - nprod) * CT;   // first 16-column tile
-    // stage-2 operands (wavefront j < CT, tile c0 + j), fetched before the
-    // residual loop: rank blocks in pairs, lanes q < 2 carry block 0, lanes
-    // q >= 2 block 1
-    u32x4 l2raw = u32x4{0u, 0u, 0u, 0u};
-    float s2a = 0.0f, s2b = 0.0f;
-    if (nprod > 0 && wave < CT && c0 + wave < ct16) {
-      const int ct = c0 + wave;
-      const int rbq = min(q >> 1, RB - 1);
-      const int L = (q & 1) * 32 + (ct & 1) * 16 + c16;
-      l2raw = *reinterpret_cast<const u32x4 *>(
-          l2codes + (((int64_t)(ct >> 1) * (geo.r_pad64 / 64) + rbq) * 64 + L) * 16);
-      const int col = ct * 16 + c16;
-      s2a = half_bits_to_float(l2scales[col]);
-      if (RB > 1) s2b = half_bits_to_float(l2scales[(int64_t)geo.n_pad + col]);
-    }
-    v4f acc[CT];
-#pragma unroll
-    for (int j = 0; j < CT; j++) acc[j] = v4f{0, 0, 0, 0};
-    {
-      constexpr int PD = CT == 1 ? SPD : SPD / 2;   // pairs in flight (registers)
-      PairOps<CT> F[PD];
-      const int npw = (NP + SW - 1) / SW;
-#pragma unroll
-      for (int s = 0; s < PD; s++)
-        if (s < npw && SW * s + wave < NP) fetch(F[s], SW * s + wave, wcodes, wscales, geo.n_pad, c0, ct16);
-      for (int i0 = 0; i0 < npw; i0 += PD) {
-#pragma unroll
-        for (int s = 0; s < PD; s++) {
-          const int i = i0 + s;
-          const int p = SW * i + wave;
-          if (i < npw && p < NP)
-            products(F[s], p, [&](int j, int, const v4f &cv, const v4f &pv) {
-#pragma unroll
-              for (int v = 0; v < 4; v++) acc[j][v] = fmaf(cv[v], pv[v], acc[j][v]);
-            });
-          const int pn = SW * (i + PD) + wave;
-          if (i + PD < npw && pn < NP) fetch(F[s], pn, wcodes, wscales, geo.n_pad, c0, ct16);
-        }
-      }
-    }
-    float *RES = reinterpret_cast<float *>(smem);
-#pragma unroll
-    for (int j = 0; j < CT; j++)
-#pragma unroll
-      for (int v = 0; v < 4; v++) RES[((wave * CT + j) * 4 + v) * 64 + lane] = acc[j][v];
-    __syncthreads();
-
-    float *HS = reinterpret_cast<float *>(smem + C::E_HS);
-    uint8_t *QS = smem + C::E_QS;
-    float *SHS = reinterpret_cast<float *>(smem + C::E_SH);
-    if (nprod > 0) {
-      // ---- wait for every producer's H tile ----
-      if (wave == 0) {
-        const uint32_t *cnt = ws_word(ws, WS_READY + ((wg - nprod) % WS_NL) * WS_LINE);
-        int spins = 0;
-        while (ld_dev(cnt) < (uint32_t)nprod) {
-          __builtin_amdgcn_s_sleep(2);
-          if (++spins > kSpinLimit) {
-            st_dev(ws_word(ws, WS_ERR), 1u);
-            break;
-          }
-        }
-      }
-      __syncthreads();
-      // all of a thread's loads are issued before any is used
-      const float *wsH = reinterpret_cast<const float *>(wsb + WS_H);
-      const int rp = 16 * nprod;
-      constexpr int HPT = 16 * kMaxRank / (64 * SW);   // H values per thread at most
-      float hl[HPT];
-#pragma unroll
-      for (int e = 0; e < HPT; e++) {
-        const int idx = tid + 64 * SW * e;
-        const int row = idx / rp, j = idx % rp;
-        hl[e] = idx < 16 * rp && row < m ? wsH[row * kMaxRank + j] : 0.0f;
-      }
-#pragma unroll
-      for (int e = 0; e < HPT; e++) {
-        const int idx = tid + 64 * SW * e;
-        if (idx < 16 * rp) HS[(idx / rp) * C::HSTR + idx % rp] = hl[e];
-      }
-      for (int idx = tid; idx < 16 * RB * 64; idx += 64 * SW) {
-        const int row = idx / (RB * 64), j = idx % (RB * 64);
-        if (j >= r) QS[row * C::QSTR + j] = 0;
-      }
-      __syncthreads();
-
-      // ---- re-quantize H per token and rank group (s_H stays fp32) ----
-      // Half a wavefront per token row (wavefront w: rows 2w, 2w + 1); lane j
-      // of the half takes ranks epl j .. epl j + epl - 1, so a rank group is a
-      // run of gr / epl lanes and its max is a shuffle reduction over them.
-      {
-        const int gr = geo.gr, rg = r / gr;
-        const int epl = r >= 32 ? r / 32 : 1;      // ranks per lane: 1, 2 or 4
-        const int row = 2 * wave + (lane >> 5), j = lane & 31;
-        const int lpg = gr / epl;                  // lanes per rank group (<= 32)
-        const int hg = j / lpg;
-        const bool valid = j * epl < r;
-        const bool dbg = a.dbg_h != nullptr && wg == nprod;
-        float hv[4];
         float amax = 0.0f;
 #pragma unroll
-        for (int e = 0; e < 4; e++) {
-          hv[e] = valid && e < epl ? HS[row * C::HSTR + j * epl + e] : 0.0f;
-          amax = fmaxf(amax, fabsf(hv[e]));
-        }
-        amax = run_max(amax, lpg, lane);
-        const float sh = amax / 7.0f;   // IEEE division
-        if (valid) {
-          uint32_t w = 0;
-#pragma unroll
-          for (int e = 0; e < 4; e++) {
-            if (e < epl) {
-              int qv = 0;
-              if (sh != 0.0f) {
-                float tq = __builtin_rintf(hv[e] / sh);
-                tq = tq > 7.0f ? 7.0f : (tq < -7.0f ? -7.0f : tq);
-                qv = (int)tq;
-              }
-              w |= code_to_fp8(qv) << (8 * e);
-              if (dbg && row < m) {
-                a.dbg_h[(int64_t)row * r + j * epl + e] = hv[e];
-                a.dbg_qh[(int64_t)row * r + j * epl + e] = (int8_t)qv;
-              }
-            }
-          }
-          uint8_t *qd = QS + row * C::QSTR + j * epl;
-          if (epl == 4) *reinterpret_cast<uint32_t *>(qd) = w;
-          else if (epl == 2) *reinterpret_cast<uint16_t *>(qd) = (uint16_t)w;
-          else *qd = (uint8_t)w;
-          if (j % lpg == 0) {
-            SHS[hg * 16 + row] = sh;
-            if (dbg && row < m) a.dbg_sh[(int64_t)row * rg + hg] = sh;
-          }
+        for (int i = 0; i < 8; i++) amax = fmaxf(amax, fabsf(v[i]));
+        amax = max8_dpp(amax);
+        uint16_t s16;
+        const float sc = q4_scale(amax, s16);
+        const float y = sc == 0.0f ? 0.0f : __builtin_amdgcn_rcpf(sc);
+        uint32_t b0, b1;
+        quant8_fp8(v, sc, y, b0, b1);
+        if (live) {
+          uint8_t *dst = XA + (g * MX + t) * XB;
+          if constexpr (MD::XFP8)
+            *reinterpret_cast<uint2 *>(dst + 8 * e) = make_uint2(b0, b1);
+          else
+            *reinterpret_cast<uint32_t *>(dst + 4 * e) = b0 | __builtin_amdgcn_alignbit(b1, b1, 28);
+          if (e == 0) XS[g * MX + t] = sc;
         }
       }
-      __syncthreads();
+      for (int idx = tid; idx < KGP * MX; idx += 64 * DW)
+        if (idx / MX >= KG || idx % MX >= m) XS[idx] = 0.0f;
+    } else {
+      // 16-byte fragments (group g, token t, half h) of tile 0's TQ4 blocks
+      const uint8_t *xc = reinterpret_cast<const uint8_t *>(a.xc);
+      const int nfrag = KG * m * 2;
+      for (int f = tid; f < nfrag; f += 64 * DW) {
+        const int g = f / (2 * m), t = (f / 2) % m, h = f & 1;
+        const u32x4 raw = *reinterpret_cast<const u32x4 *>(xc + ((int64_t)g * 64 + 32 * h + t) * 16);
+        uint8_t *dst = XA + (g * MX + t) * XB;
+        if constexpr (MD::XFP8) {
+          const v8i o = unpack32(raw);
+          *reinterpret_cast<u32x4 *>(dst + 32 * h) = u32x4{(uint32_t)o[0], (uint32_t)o[1], (uint32_t)o[2], (uint32_t)o[3]};
+          *reinterpret_cast<u32x4 *>(dst + 32 * h + 16) = u32x4{(uint32_t)o[4], (uint32_t)o[5], (uint32_t)o[6], (uint32_t)o[7]};
+        } else {
+          *reinterpret_cast<u32x4 *>(dst + 16 * h) = raw;
+        }
+      }
+      for (int idx = tid; idx < KGP * MX; idx += 64 * DW) {
+        const int g = idx / MX, t = idx % MX;
+        XS[idx] = g < KG && t < m ? half_bits_to_float(a.xs[(int64_t)g * a.ms + t]) : 0.0f;
+      }
     }
+    // zero codes for the token slots past m, the odd tail group and the pad
+    // that lanes outside the operand's live rows read
+    for (int idx = tid; idx < KGP * MX * XB / 16 + 2; idx += 64 * DW) {
+      const int e = idx * 16;
+      const int g = e / (MX * XB), t = (e / XB) % MX;
+      if (idx >= KGP * MX * XB / 16 || g >= KG || t >= m)
+        *reinterpret_cast<u32x4 *>(XA + e) = u32x4{0u, 0u, 0u, 0u};
+    }
+    __syncthreads();
+  };
 
-    // ---- stage 2 and the single epilogue: wavefront j < CT stores tile j ----
-    if (wave < CT) {
-      const int j = wave;
-      const int ct = c0 + j;
-      if (ct < ct16) {
-        v4f ylr = v4f{0, 0, 0, 0};
-        const int orow0 = 4 * q;   // output rows 4q .. 4q + 3 of this lane
-        if (nprod > 0) {
-          const int rbq = min(q >> 1, RB - 1);
-          const v8i qa = lds_v8i(QS + c16 * C::QSTR + rbq * 64 + (q & 1) * 32);
-          float sh0[4], sh1[4];
+  // activation operand of pair p: lanes outside the operand's live rows
+  // (TOK8: group A lives in rows 0-7 of quarters 0-1, group B in rows 8-15
+  // of quarters 2-3) or past the MX token slots read the zero pad after the
+  // codes; the others read their (group 2p + gq, token, half) slot, zero
+  // past m and past the last K-group
+  const int arow = lane & 15;
+  const int atok = MD::TOK8 ? (arow & 7) : arow;
+  const bool alive = (MD::TOK8 ? ((arow < 8) == (q < 2)) : true) && atok < MX;
+  const int xpad = KGP * MX * XB;
+  const int abase = alive ? (gq * MX + atok) * XB + qh * (XB / 2) : xpad;
+  const int astride = alive ? 2 * MX * XB : 0;
+  auto act_op = [&](int p) -> v8i {
+    const uint8_t *src = XA + abase + p * astride;
+    if constexpr (MD::XFP8) return lds_v8i(src);
+    else return unpack32(*reinterpret_cast<const u32x4 *>(src));
+  };
+  // token of accumulator row v of this lane, clamped into the LDS slots
+  auto tok_of = [&](int v) {
+    const int t = MD::TOK8 ? 4 * qh + v : 4 * q + v;
+    return t < MX ? t : 0;
+  };
+  const v8i z8 = {0, 0, 0, 0, 0, 0, 0, 0};
+
+  float hacc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  v4f acc[CTW];
 #pragma unroll
-          for (int v = 0; v < 4; v++) {
-            sh0[v] = SHS[orow0 + v];
-            sh1[v] = RB > 1 ? SHS[16 + orow0 + v] : 0.0f;
-          }
-          const v8i lb = unpack32(l2raw);
-          const v8i zero = {0, 0, 0, 0, 0, 0, 0, 0};
-          const v8i qa1 = q < 2 ? qa : zero;
-          const v8i qa2 = q < 2 ? zero : qa;
-          {
-            const v4f cb = mfma_codes_16x16x128(qa1, lb);
+  for (int j = 0; j < CTW; j++) acc[j] = v4f{0, 0, 0, 0};
+
+  // the activation scales of this lane's accumulator rows for group g (the
+  // rows are consecutive tokens, so one LDS read)
+  auto xs_row = [&](int g) -> v4f {
+    const float *p = XS + g * MX + tok_of(0);
+    if constexpr (MV == 1) return v4f{p[0], 0.0f, 0.0f, 0.0f};
+    else if constexpr (MV == 2) { const float2 t = *reinterpret_cast<const float2 *>(p); return v4f{t.x, t.y, 0.0f, 0.0f}; }
+    else return *reinterpret_cast<const v4f *>(p);
+  };
+
+  // Stage 1, software-pipelined three deep so that no step waits on the one
+  // before it: the LDS operands of pair i + 2 are read, the matrix product of
+  // pair i + 1 is issued, and the chain step of pair i runs, in that order.
+  // The chain is the ascending-group fma of rank tile `wave` (gb == KG on an
+  // odd tail: zero codes and scales, so that step adds exactly nothing).
+  struct S1Lds {
+    v8i av;          // activation operand
+    v4f sxa, sxb;    // activation scales of the lane's rows, groups A and B
+  };
+  struct S1Prod {
+    v4f I;           // integer sums (TOK8: group A in lanes 0-31, B in 32-63)
+    v4f I2;          // 16-token layout: group B's sums
+    v4f sxa, sxb;
+  };
+  auto s1_lds = [&](int p) -> S1Lds {
+    S1Lds r;
+    r.av = act_op(p);
+    r.sxa = xs_row(2 * p);
+    r.sxb = xs_row(2 * p + 1);
+    return r;
+  };
+  auto s1_mfma = [&](const S1Lds &A, const S1Slot &Sl) -> S1Prod {
+    S1Prod r;
+    const v8i b = unpack32(Sl.l1);
+    if constexpr (MD::TOK8) {
+      r.I = mfma_codes_16x16x128(A.av, b);
+      r.I2 = v4f{0, 0, 0, 0};
+    } else {
+      r.I = mfma_codes_16x16x128(q < 2 ? A.av : z8, b);
+      r.I2 = mfma_codes_16x16x128(q < 2 ? z8 : A.av, b);
+    }
+    r.sxa = A.sxa;
+    r.sxb = A.sxb;
+    return r;
+  };
+  // One chain step per group: h = fma(I s_x, s_L1, h).  I s_x is exact in
+  // fp32 (|I| < 2^12 times an 11-bit fp16 significand), so this rounds the
+  // same exact value I s_x s_L1 + h once, as fma(I, s_x s_L1, h) does; the
+  // fp16 scale enters the fma without a separate conversion.
+  auto s1_chain = [&](const S1Prod &P, const S1Slot &Sl) {
+    const _Float16 sla = __builtin_bit_cast(_Float16, (uint16_t)Sl.sla);
+    const _Float16 slb = __builtin_bit_cast(_Float16, (uint16_t)Sl.slb);
 #pragma unroll
-            for (int v = 0; v < 4; v++) ylr[v] = fmaf(cb[v], sh0[v] * s2a, ylr[v]);
-          }
-          if (RB > 1) {
-            const v4f cb = mfma_codes_16x16x128(qa2, lb);
+    for (int v = 0; v < MV; v++) {
+      const float ib = MD::TOK8 ? upper_half(P.I[v]) : P.I2[v];
+      hacc[v] = fmaf(P.I[v] * P.sxa[v], (float)sla, hacc[v]);
+      hacc[v] = fmaf(ib * P.sxb[v], (float)slb, hacc[v]);
+    }
+  };
+  auto residual = [&](const ResSlot<CTW> &Sl, int p) {
+    const int ga = 2 * p, gb = 2 * p + 1;
+    const v8i av = act_op(p);
+    const v4f sxa = xs_row(ga), sxb = xs_row(gb);
 #pragma unroll
-            for (int v = 0; v < 4; v++) ylr[v] = fmaf(cb[v], sh1[v] * s2b, ylr[v]);
-          }
+    for (int j = 0; j < CTW; j++) {
+      const v8i b = unpack32(Sl.w[j]);
+      if constexpr (MD::TOK8) {
+        const v4f I = mfma_codes_16x16x128(av, b);
+        const _Float16 sw = __builtin_bit_cast(_Float16, (uint16_t)Sl.swa[j]);
+        const v4f sx = q < 2 ? sxa : sxb;   // the lane's own group
+#pragma unroll
+        for (int v = 0; v < MV; v++) acc[j][v] = fmaf(I[v] * sx[v], (float)sw, acc[j][v]);
+      } else {
+        const v4f I1 = mfma_codes_16x16x128(q < 2 ? av : z8, b);
+        const v4f I2 = mfma_codes_16x16x128(q < 2 ? z8 : av, b);
+        const _Float16 swa = __builtin_bit_cast(_Float16, (uint16_t)Sl.swa[j]);
+        const _Float16 swb = __builtin_bit_cast(_Float16, (uint16_t)Sl.swb[j]);
+#pragma unroll
+        for (int v = 0; v < 4; v++) {
+          acc[j][v] = fmaf(I1[v] * sxa[v], (float)swa, acc[j][v]);
+          acc[j][v] = fmaf(I2[v] * sxb[v], (float)swb, acc[j][v]);
         }
-        // the matrix-core products above read operands from every lane: keep
-        // them out of the per-lane store branch below
-        asm volatile("" : "+v"(ylr));
-        const int col = ct * 16 + c16;
-        if (col < geo.n) {
+      }
+    }
+  };
+
+  // The two roles keep their rings in separate scopes, so their registers
+  // overlap.  Each issues its first loads, then joins the prologue's barrier.
+  if (TWO && s1) {
+    // pass A: items it = wave, wave + NS, ... of the NP x R (pair, rank tile)
+    // products; the exact sums of token 0 (rows 0 and 8) go to LDS as int16
+    const int nit = NP * R;
+    const int nmy = wave < nit ? (nit - wave + NS - 1) / NS : 0;
+    const int ilast = nmy > 0 ? nmy - 1 : 0;
+    const uint32_t lanepart = (uint32_t)((gq * 64 + qh * 32 + c16) * 16);
+    auto load_a = [&](u32x4 &f, int i) {
+      const int it = wave + i * NS, p = it / R, rt = it - p * R;
+      const uint32_t off = (uint32_t)(((rt >> 1) * KG * 64) * 16 + (rt & 1) * 256 + p * 2048);
+      f = *reinterpret_cast<const u32x4 *>(l1codes + off + (lanepart - tail_adj(p)));
+    };
+    u32x4 F[D1];
 #pragma unroll
-          for (int v = 0; v < 4; v++) {
-            const int row = orow0 + v;
-            if (row < m) {
-              float yres = 0.0f;
-              for (int w2 = 0; w2 < SW; w2++) yres += RES[((w2 * CT + j) * 4 + v) * 64 + lane];
-              const float yv = yres + ylr[v];
-              const uint16_t bits = a.bf16_out ? float_to_bf16_bits(yv) : float_to_half_bits(yv);
-              reinterpret_cast<uint16_t *>(a.y)[(int64_t)row * geo.n + col] = bits;
-            }
-          }
+    for (int s = 0; s < D1; s++) load_a(F[s], min(s, ilast));
+    prologue();
+    for (int i0 = 0; i0 < nmy; i0 += D1) {
+#pragma unroll
+      for (int s = 0; s < D1; s++) {
+        const int i = i0 + s;
+        if (i < nmy) {
+          const int it = wave + i * NS, p = it / R;
+          v4f I = mfma_codes_16x16x128(act_op(p), unpack32(F[s]));
+          // the product reads its operands from every lane: keep it (and the
+          // unpacking) out of the store branch below
+          asm volatile("" : "+v"(I));
+          if ((q & 1) == 0) IS[(it * 2 + gq) * 16 + c16] = (int16_t)(int)I[0];
         }
+        load_a(F[s], min(i + D1, ilast));
+      }
+    }
+  } else if (s1) {
+    S1Slot S1[D1];
+#pragma unroll
+    for (int s = 0; s < D1; s++) load_s1(S1[s], min(s, NP - 1));
+    prologue();
+    // slot s holds pair i0 + s; it is refilled after pair i's chain step
+    S1Lds lds2 = s1_lds(min(1, NP - 1));
+    S1Prod prod = s1_mfma(s1_lds(0), S1[0]);
+    for (int i0 = 0; i0 < NP; i0 += D1) {
+#pragma unroll
+      for (int s = 0; s < D1; s++) {
+        const int i = i0 + s;
+        if (i < NP) {
+          const S1Lds lds_next = s1_lds(min(i + 2, NP - 1));
+          const S1Prod prod_next = s1_mfma(lds2, S1[(s + 1) % D1]);
+          s1_chain(prod, S1[s]);
+          prod = prod_next;
+          lds2 = lds_next;
+        }
+        load_s1(S1[s], min(i + D1, NP - 1));
+      }
+    }
+  } else {
+    ResSlot<CTW> SR[D2];
+    const int plast = nres_it > 0 ? ph + (nres_it - 1) * NPH : 0;
+#pragma unroll
+    for (int s = 0; s < D2; s++) load_res(SR[s], min(ph + s * NPH, plast));
+    prologue();
+    for (int i0 = 0; i0 < nres_it; i0 += D2) {
+#pragma unroll
+      for (int s = 0; s < D2; s++) {
+        const int i = i0 + s;
+        if (i < nres_it) residual(SR[s], ph + i * NPH);
+        load_res(SR[s], min(ph + (i + D2) * NPH, plast));
       }
     }
   }
+  __syncthreads();   // every wavefront is done with the activation codes
 
-  // ---- the last column work-group of a line clears the line ----
-  if (nprod > 0 && !producer) {
-    __syncthreads();   // every read of the line and of H is done
-    if (tid == 0) {
-      const int x = (wg - nprod) % WS_NL, ncol = (int)gridDim.x - nprod;
-      const uint32_t per = (uint32_t)((ncol - x + WS_NL - 1) / WS_NL);   // column work-groups on line x
-      if (add_dev(ws_word(ws, WS_READY + x * WS_LINE + 4)) == per - 1) {
-        st_dev(ws_word(ws, WS_READY + x * WS_LINE), 0u);
-        st_dev(ws_word(ws, WS_READY + x * WS_LINE + 4), 0u);
+  // ---- epilogue: residual partials, H, re-quantization, stage 2, store ----
+  float *RES = reinterpret_cast<float *>(smem + LY.epi_res);   // [NPH][CT][16 tokens][16 columns]
+  float *HS = reinterpret_cast<float *>(smem + LY.epi_h);      // [16][HSTR]
+  uint8_t *QS = smem + LY.epi_q;                                // [16][QSTR] fp8 codes
+  float *SHS = reinterpret_cast<float *>(smem + LY.epi_sh);    // [2][16]
+  constexpr int HSTR = DLayout::HSTR, QSTR = DLayout::QSTR;
+  const bool store_lane = !MD::TOK8 || lane < 32;
+  if (rbusy) {
+#pragma unroll
+    for (int j = 0; j < CTW; j++)
+#pragma unroll
+      for (int v = 0; v < MV; v++) {
+        float val = acc[j][v];
+        if constexpr (MD::TOK8) val += upper_half(val);   // group A + group B partials
+        const int t = MD::TOK8 ? 4 * qh + v : 4 * q + v;
+        if (store_lane) RES[((ph * CT + tg * CTW + j) * 16 + t) * 16 + c16] = val;
+      }
+  }
+  if (!TWO && s1) {
+#pragma unroll
+    for (int v = 0; v < MV; v++) {
+      const int t = MD::TOK8 ? 4 * qh + v : 4 * q + v;
+      if (store_lane) HS[t * HSTR + 16 * wave + c16] = hacc[v];
+    }
+  }
+  if (TWO && wave * 64 < 16 * R) {
+    // pass B: rank j's chain over every K-group in ascending order,
+    // h = fma(I s_x, s_L1, h) (I s_x exact, as in the one-pass chain); the
+    // L1 scales are fetched 8 groups ahead
+    const int j = wave * 64 + lane;
+    const bool jok = j < 16 * R;
+    const int jj = jok ? j : 0;
+    const int rt = jj >> 4, cj = jj & 15;
+    const uint16_t *slp = l1scales + jj;
+    float h = 0.0f;
+    uint16_t sl[8];
+#pragma unroll
+    for (int e = 0; e < 8; e++) sl[e] = slp[(int64_t)min(e, KG - 1) * geo.r_pad32];
+    for (int g0 = 0; g0 < KG; g0 += 8) {
+      uint16_t sn[8];
+#pragma unroll
+      for (int e = 0; e < 8; e++) sn[e] = slp[(int64_t)min(g0 + 8 + e, KG - 1) * geo.r_pad32];
+#pragma unroll
+      for (int e = 0; e < 8; e++) {
+        const int g = g0 + e;
+        if (g < KG) {
+          const float I = (float)IS[(((g >> 1) * R + rt) * 2 + (g & 1)) * 16 + cj];
+          h = fmaf(I * XS[g * MX], (float)__builtin_bit_cast(_Float16, sl[e]), h);
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < 8; e++) sl[e] = sn[e];
+    }
+    if (jok) HS[j] = h;   // token 0
+  }
+  const int RB = (r + 63) / 64;   // 64-rank blocks of stage 2 (<= 2)
+  if (r > 0) {
+    for (int idx = tid; idx < 16 * RB * 64; idx += 64 * DW) {
+      const int row = idx / (RB * 64), j = idx % (RB * 64);
+      if (j >= r) QS[row * QSTR + j] = 0;
+    }
+  }
+  __syncthreads();
+
+  if (r > 0) {
+    // Re-quantize H per token and rank group (s_H stays fp32).  Half a
+    // wavefront per token row (wavefront w < 8: rows 2w, 2w + 1); lane j of
+    // the half takes ranks epl j .. epl j + epl - 1, so a rank group is a run
+    // of gr / epl lanes and its max is a shuffle reduction over them.
+    if (wave < 8) {
+      const int gr = geo.gr, rg = r / gr;
+      const int epl = r >= 32 ? r / 32 : 1;      // ranks per lane: 1, 2 or 4
+      const int row = 2 * wave + (lane >> 5), j = lane & 31;
+      const int lpg = gr / epl;                  // lanes per rank group (<= 32)
+      const int hg = j / lpg;
+      const bool valid = j * epl < r;
+      const bool live = valid && row < m;
+      const bool dbg = a.dbg_h != nullptr && blockIdx.x == 0;
+      float hv[4];
+      float amax = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 4; e++) {
+        hv[e] = live && e < epl ? HS[row * HSTR + j * epl + e] : 0.0f;
+        amax = fmaxf(amax, fabsf(hv[e]));
+      }
+      amax = run_max(amax, lpg, lane);
+      const float sh = amax / 7.0f;   // IEEE division
+      if (valid) {
+        uint32_t w = 0;
+#pragma unroll
+        for (int e = 0; e < 4; e++) {
+          if (e < epl) {
+            int qv = 0;
+            if (sh != 0.0f) {
+              float tq = __builtin_rintf(hv[e] / sh);
+              tq = tq > 7.0f ? 7.0f : (tq < -7.0f ? -7.0f : tq);
+              qv = (int)tq;
+            }
+            w |= code_to_fp8(qv) << (8 * e);
+            if (dbg && row < m) {
+              a.dbg_h[(int64_t)row * r + j * epl + e] = hv[e];
+              a.dbg_qh[(int64_t)row * r + j * epl + e] = (int8_t)qv;
+            }
+          }
+        }
+        uint8_t *qd = QS + row * QSTR + j * epl;
+        if (epl == 4) *reinterpret_cast<uint32_t *>(qd) = w;
+        else if (epl == 2) *reinterpret_cast<uint16_t *>(qd) = (uint16_t)w;
+        else *qd = (uint8_t)w;
+        if (j % lpg == 0) {
+          SHS[hg * 16 + row] = sh;
+          if (dbg && row < m) a.dbg_sh[(int64_t)row * rg + hg] = sh;
+        }
+      }
+    }
+    __syncthreads();
+  }
+
+  // ---- stage 2 and the single epilogue: wavefront j < CT stores tile j ----
+  if (wave < CT) {
+    const int j = wave;
+    const int ct = c0 + j;
+    if (ct < ct16) {
+      v4f ylr = v4f{0, 0, 0, 0};
+      const int orow0 = 4 * q;   // output rows 4q .. 4q + 3 of this lane
+      if (r > 0) {
+        const int rbq = min(q >> 1, RB - 1);
+        const int L = qh * 32 + (ct & 1) * 16 + c16;
+        const u32x4 l2raw = *reinterpret_cast<const u32x4 *>(
+            l2codes + (((int64_t)(ct >> 1) * (geo.r_pad64 / 64) + rbq) * 64 + L) * 16);
+        const int col = ct * 16 + c16;
+        const float s2a = half_bits_to_float(l2scales[col]);
+        const float s2b = RB > 1 ? half_bits_to_float(l2scales[(int64_t)geo.n_pad + col]) : 0.0f;
+        const v8i qa = lds_v8i(QS + c16 * QSTR + rbq * 64 + qh * 32);
+        const v8i lb = unpack32(l2raw);
+        {
+          const v4f cb = mfma_codes_16x16x128(q < 2 ? qa : z8, lb);
+#pragma unroll
+          for (int v = 0; v < 4; v++) ylr[v] = fmaf(cb[v], SHS[orow0 + v] * s2a, ylr[v]);
+        }
+        if (RB > 1) {
+          const v4f cb = mfma_codes_16x16x128(q < 2 ? z8 : qa, lb);
+#pragma unroll
+          for (int v = 0; v < 4; v++) ylr[v] = fmaf(cb[v], SHS[16 + orow0 + v] * s2b, ylr[v]);
+        }
+      }
+      // the matrix-core products above read operands from every lane: keep
+      // them out of the per-lane store branch below
+      asm volatile("" : "+v"(ylr));
+      const int col = ct * 16 + c16;
+      if (col < geo.n) {
+#pragma unroll
+        for (int v = 0; v < 4; v++) {
+          const int row = orow0 + v;
+          if (row < m) {
+            float yres = 0.0f;
+            for (int w2 = 0; w2 < NPH; w2++) yres += RES[((w2 * CT + j) * 16 + row) * 16 + c16];
+            const float yv = yres + ylr[v];
+            const uint16_t bits = a.bf16_out ? float_to_bf16_bits(yv) : float_to_half_bits(yv);
+            reinterpret_cast<uint16_t *>(a.y)[(int64_t)row * geo.n + col] = bits;
+          }
+        }
       }
     }
   }
 }
 
-template <int CT>
-hipError_t launch_decode(const GemmArgs &a, hipStream_t s) {
-  using C = SCfg<CT>;
+template <int MODE, int CT, bool FQ, bool TWO>
+hipError_t launch_decode(const GemmArgs &a, const uint16_t *xh, int ns, hipStream_t s) {
+  using MD = DMode<MODE>;
+  const int KG = a.geo.k / kGroup, NP = (KG + 1) / 2, R = rank_tiles(a.geo.r);
+  const DLayout LY(KG, MD::MX, MD::XB, CT, DW - (TWO ? ns : R), TWO ? NP * R * 64 : 0);
   const int tiles16 = a.geo.n_pad / 16;
-  const int ncol = (tiles16 + CT - 1) / CT;
-  const int nprod = (a.geo.r + 15) / 16;
-  auto kern = dual_gemm_decode_kernel<CT>;
+  auto kern = dual_gemm_decode_kernel<MODE, CT, FQ, TWO>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, LY.total);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, dim3(nprod + ncol), dim3(64 * SW), C::LDS, s, a, nprod);
+  hipLaunchKernelGGL(kern, dim3((tiles16 + CT - 1) / CT), dim3(64 * DW), LY.total, s, a, xh, ns);
   return hipGetLastError();
 }
 
+constexpr int kLdsBytes = 160 * 1024;
+
+// Single token with a low-rank branch: the two-pass path when its int16 sums
+// fit the LDS beside the activation codes, with ns stage-1 wavefronts chosen
+// so that the NP R products and the NP CT residual tile-pairs (~1.2 times the
+// work each) finish together, leaving every residual tile group a wavefront.
+template <int CT>
+int two_pass_waves(const GemmArgs &a) {
+  if (a.m != 1 || a.geo.r == 0) return 0;
+  const int KG = a.geo.k / kGroup, NP = (KG + 1) / 2, R = rank_tiles(a.geo.r);
+  const DLayout LY(KG, 1, 64, CT, DW - 1, NP * R * 64);   // the most residual wavefronts
+  if (LY.total > kLdsBytes) return 0;
+  const int tg = DRes<CT, 10>::TG;
+  int ns = (int)(DW * (float)R / ((float)R + 1.2f * CT) + 0.5f);
+  ns = ns < 1 ? 1 : (ns > DW - tg ? DW - tg : ns);
+  return ns;
+}
+
+template <int MODE, int CT, bool FQ>
+hipError_t launch_decode_ct(const GemmArgs &a, const uint16_t *xh, hipStream_t s) {
+  if constexpr (MODE == 1) {
+    const int ns = two_pass_waves<CT>(a);
+    if (ns > 0) return launch_decode<MODE, CT, FQ, true>(a, xh, ns, s);
+  }
+  return launch_decode<MODE, CT, FQ, false>(a, xh, 0, s);
+}
+
+template <int MODE, bool FQ>
+hipError_t launch_decode_mode(const GemmArgs &a, const uint16_t *xh, hipStream_t s) {
+  // the fewest 16-column tiles per work-group that keep the grid within one
+  // work-group per CU
+  const int tiles16 = a.geo.n_pad / 16;
+  if (tiles16 <= 256) return launch_decode_ct<MODE, 1, FQ>(a, xh, s);
+  if (tiles16 <= 512) return launch_decode_ct<MODE, 2, FQ>(a, xh, s);
+  if (tiles16 <= 1024) return launch_decode_ct<MODE, 4, FQ>(a, xh, s);
+  return launch_decode_ct<MODE, 8, FQ>(a, xh, s);
+}
+
+int decode_mode(int m) { return m == 1 ? 1 : (m == 2 ? 2 : (m <= 8 ? 4 : 16)); }
+
 }  // namespace
 
-hipError_t launch_dual_gemm_decode(const GemmArgs &a, hipStream_t s) {
-  // two 16-column tiles per work-group once one tile per work-group would not
-  // fit one round of resident work-groups (two per CU, 512 on the 256 CUs),
-  // the H producers included: a second round for a few work-groups costs a
-  // whole work-group's time (measured at N = 8192, r = 128, K = 28672: 68 us
-  // with 520 work-groups, 47 us with 264)
-  const int tiles16 = a.geo.n_pad / 16;
-  const int nprod = (a.geo.r + 15) / 16;
-  const int ct = tiles16 + nprod > 2 * 256 ? 2 : 1;
-  return ct == 2 ? launch_decode<2>(a, s) : launch_decode<1>(a, s);
+bool decode_fits(int m, int k) {
+  if (m < 1 || m > kDecodeMaxTokens) return false;
+  const int mode = decode_mode(m);
+  const int mx = mode == 16 ? 16 : (mode <= 2 ? mode : 8);
+  const int xb = mode <= 2 ? 64 : 32;
+  const int64_t kgp = (int64_t)(k / kGroup + 1) / 2 * 2;
+  return kgp * mx * xb <= kDecodeXBytes;
+}
+
+hipError_t launch_dual_gemm_decode(const GemmArgs &a, const uint16_t *xh, hipStream_t s) {
+  const bool fq = xh != nullptr;
+  switch (decode_mode(a.m)) {
+    case 1: return fq ? launch_decode_mode<1, true>(a, xh, s) : launch_decode_mode<1, false>(a, xh, s);
+    case 2: return fq ? launch_decode_mode<2, true>(a, xh, s) : launch_decode_mode<2, false>(a, xh, s);
+    case 4: return fq ? launch_decode_mode<4, true>(a, xh, s) : launch_decode_mode<4, false>(a, xh, s);
+    default: return fq ? launch_decode_mode<16, true>(a, xh, s) : launch_decode_mode<16, false>(a, xh, s);
+  }
 }
 
 }  // namespace tq

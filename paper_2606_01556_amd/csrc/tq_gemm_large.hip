@@ -30,7 +30,6 @@
 // one work-group barrier and refills their slots D groups ahead.  The stage-2
 // operands (L2 blocks and scales of the 8 column tiles) are loaded at the
 // start into a region of their own.
-#include <stdlib.h>
 
 #include <type_traits>
 

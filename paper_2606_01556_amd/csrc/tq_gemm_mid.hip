@@ -32,7 +32,6 @@
 // 1 KiB halves per group): each wavefront then issues two shared loads per
 // chunk, and the operands are read from the chunk slot as loaded, with no
 // expansion.
-#include <stdlib.h>
 
 #include <type_traits>
 
@@ -608,8 +607,7 @@ int mid_tiles(const GemmArgs &a, int *cost) {
   int ct = 1;
   for (int c : {2, 4})
     if (mid_cost(rt, c, n_rb, ct32) < mid_cost(rt, ct, n_rb, ct32)) ct = c;
-  // TQ_MID_CT=1|2|4 forces the tile count (the tests run all three)
-  if (const char *env = getenv("TQ_MID_CT")) ct = atoi(env);
+  if (a.mid_ct > 0) ct = a.mid_ct;   // forced by the test entry (1, 2 or 4, validated there)
   if (cost) *cost = mid_cost(rt, ct, n_rb, ct32);
   return ct;
 }

@@ -34,7 +34,6 @@
 // product -- exactly I * s_x * s_w -- to the fp32 accumulator in ascending
 // group order, the oracle's order for H and for the residual, so Y is
 // bit-identical to the oracle's rounded result.
-#include <stdlib.h>
 
 #include <type_traits>
 

@@ -6,10 +6,9 @@
 
 namespace tq {
 
-// Largest supported rank, and the size of the caller's workspace of
-// tq_dual_gemm (its layout is private to the decode kernel).
+// Largest supported rank; token counts served by the decode kernel.
 constexpr int kMaxRank = 128;
-constexpr size_t kWorkspaceBytes = 20480;
+constexpr int kDecodeMaxTokens = 16;
 
 // Token counts up to kMidMaxTokens run the decode and mid kernels, which take
 // the activation codes as TQ4 nibbles (k / 2 bytes per token).  Larger counts
@@ -49,7 +48,8 @@ struct GemmArgs {
   float *dbg_h;         // optional [m][r]
   float *dbg_sh;        // optional [m][r/gr]
   int8_t *dbg_qh;       // optional [m][r]
-  uint32_t *ws;         // kWorkspaceBytes, zero between calls (decode kernel)
+  int force_kernel;     // -1: chosen by choose_kernel; else a kKernel* value (tests)
+  int mid_ct;           // 0: chosen by the mid kernel's cost model; else 1, 2 or 4 (tests)
 };
 
 hipError_t launch_quant_act(const uint16_t *x, int m, int k, uint32_t *codes, uint16_t *scales,
@@ -60,7 +60,11 @@ hipError_t launch_export(const Geometry &g, const uint8_t *packed, uint32_t *wc,
                          uint32_t *l1c, uint16_t *l1s, uint32_t *l2c, uint16_t *l2s,
                          hipStream_t s);
 hipError_t launch_dual_gemm(const GemmArgs &a, hipStream_t s);
-hipError_t launch_dual_gemm_decode(const GemmArgs &a, hipStream_t s);  // m <= 16
+// m <= kDecodeMaxTokens; xh = NULL: codes from a.xc / a.xs, else fp16
+// activations [m][k] quantized inside the kernel
+hipError_t launch_dual_gemm_decode(const GemmArgs &a, const uint16_t *xh, hipStream_t s);
+// whether the decode kernel's LDS holds the activation codes of m tokens
+bool decode_fits(int m, int k);
 // the kernel launch_dual_gemm runs (values of tq_kernel in the C header)
 constexpr int kKernelDecode = 0, kKernelMid = 1, kKernelLarge = 2, kKernelPrefill = 3;
 int choose_kernel(const GemmArgs &a);

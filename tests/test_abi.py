@@ -81,23 +81,57 @@ def test_dual_gemm_validation(L):
     d = tq.weight_desc_init(128, 128, 16)
     bad = tq.WeightDesc()
     D = ctypes.byref
-    assert L.tq_dual_gemm(D(d), None, FAKE, FAKE, 4, FAKE, 0, FAKE, None) == 1
-    assert L.tq_dual_gemm(D(bad), FAKE, FAKE, FAKE, 4, FAKE, 0, FAKE, None) == 7
-    assert L.tq_dual_gemm(D(d), FAKE, FAKE, FAKE, 4, FAKE, 7, FAKE, None) == 5
-    assert L.tq_dual_gemm(D(d), FAKE, FAKE, FAKE, -2, FAKE, 0, FAKE, None) == 2
-    assert L.tq_dual_gemm(D(d), FAKE, FAKE + 4, FAKE, 4, FAKE, 0, FAKE, None) == 6
-    assert L.tq_dual_gemm(D(d), FAKE, FAKE, FAKE, 0, FAKE, 0, FAKE, None) == 0
-    d0 = tq.weight_desc_init(128, 128, 0)
-    assert L.tq_dual_gemm_debug(D(d0), FAKE, FAKE, FAKE, 4, FAKE, 0, FAKE, FAKE, FAKE, FAKE, None) == 4
-    assert L.tq_dual_gemm_debug(D(d), FAKE, FAKE, FAKE, 4, FAKE, 0, None, FAKE, FAKE, FAKE, None) == 1
-    # the workspace is required and 16-byte aligned
-    assert L.tq_dual_gemm(D(d), FAKE, FAKE, FAKE, 4, FAKE, 0, None, None) == 1
-    assert L.tq_dual_gemm(D(d), FAKE, FAKE, FAKE, 4, FAKE, 0, FAKE + 8, None) == 6
-    assert L.tq_workspace_bytes() >= 256 + 16 * 128 * 5 and L.tq_workspace_bytes() % 256 == 0
+    assert L.tq_dual_gemm(D(d), None, FAKE, FAKE, 4, FAKE, 0, None) == 1
+    assert L.tq_dual_gemm(D(bad), FAKE, FAKE, FAKE, 4, FAKE, 0, None) == 7
+    assert L.tq_dual_gemm(D(d), FAKE, FAKE, FAKE, 4, FAKE, 7, None) == 5
+    assert L.tq_dual_gemm(D(d), FAKE, FAKE, FAKE, -2, FAKE, 0, None) == 2
+    assert L.tq_dual_gemm(D(d), FAKE, FAKE + 4, FAKE, 4, FAKE, 0, None) == 6
+    assert L.tq_dual_gemm(D(d), FAKE, FAKE, FAKE, 0, FAKE, 0, None) == 0
     # a descriptor edited after init is rejected
     d3 = tq.weight_desc_init(128, 128, 16)
     d3.n_pad = 64
-    assert L.tq_dual_gemm(D(d3), FAKE, FAKE, FAKE, 4, FAKE, 0, FAKE, None) == 7
+    assert L.tq_dual_gemm(D(d3), FAKE, FAKE, FAKE, 4, FAKE, 0, None) == 7
+
+
+def test_debug_entry_validation(L):
+    """The test entry: H / s_H / Q_H copies all or none (and only with r > 0),
+    forced kernels only where they serve m, mid tile counts 1, 2, 4."""
+    d = tq.weight_desc_init(128, 128, 16)
+    d0 = tq.weight_desc_init(128, 128, 0)
+    D = ctypes.byref
+    dbg = lambda dd, m, kern, ct, h, sh, qh, x=None, xc=FAKE: L.tq_dual_gemm_debug(
+        D(dd), FAKE, xc, xc, x, m, FAKE, 0, kern, ct, h, sh, qh, None)
+    assert dbg(d0, 4, -1, 0, FAKE, FAKE, FAKE) == 4
+    assert dbg(d, 4, -1, 0, None, FAKE, FAKE) == 1
+    assert dbg(d, 4, 4, 0, None, None, None) == 2            # no such kernel
+    assert dbg(d, 4, -2, 0, None, None, None) == 2
+    assert dbg(d, 4, 2, 0, None, None, None) == 2            # large kernel needs m > 512
+    assert dbg(d, 100, 3, 0, None, None, None) == 2          # prefill kernel needs m > 512
+    assert dbg(d, 17, 0, 0, None, None, None) == 2           # decode kernel needs m <= 16
+    assert dbg(d, 4, 1, 3, None, None, None) == 2            # mid tiles 1, 2 or 4
+    # the fused-quantization path: no codes, decode kernel only
+    assert dbg(d, 4, -1, 0, None, None, None, x=FAKE) == 2
+    assert dbg(d, 4, 1, 0, None, None, None, x=FAKE, xc=None) == 2
+    assert dbg(d, 17, -1, 0, None, None, None, x=FAKE, xc=None) == 2
+
+
+def test_fused_quant_validation(L):
+    D = ctypes.byref
+    d = tq.weight_desc_init(128, 4096, 64)
+    assert L.tq_dual_gemm_fused_quant(D(d), FAKE, None, 4, FAKE, 0, None) == 1
+    assert L.tq_dual_gemm_fused_quant(D(d), FAKE, FAKE + 2, 4, FAKE, 0, None) == 6
+    assert L.tq_dual_gemm_fused_quant(D(d), FAKE, FAKE, 17, FAKE, 0, None) == 2
+    assert L.tq_dual_gemm_fused_quant(D(d), FAKE, FAKE, 0, FAKE, 0, None) == 0
+    # the activation codes of m tokens must fit the decode kernel's LDS
+    big = tq.weight_desc_init(128, 14400, 64)
+    assert L.tq_dual_gemm_fused_quant(D(big), FAKE, FAKE, 16, FAKE, 0, None) == 2
+
+
+def test_desc_rejects_4gib_packed_buffer(L):
+    d = tq.WeightDesc()
+    assert L.tq_weight_desc_init(1 << 17, 1 << 16, 0, 64, ctypes.byref(d)) == 2
+    assert L.tq_weight_desc_init(1 << 16, 1 << 16, 0, 64, ctypes.byref(d)) == 0
+    assert d.packed_bytes < (1 << 32)
 
 
 def test_noalloc_validation(L):
@@ -211,24 +245,22 @@ def test_unfused_sizes_and_validation(L):
     assert L.tq_dual_gemm_unfused(ctypes.byref(d), FAKE, FAKE, FAKE, 0, FAKE, 0, FAKE, None) == 0
 
 
-def test_kernel_choice(L, monkeypatch):
-    """tq_dual_gemm_kernel: the decode kernel up to 16 tokens, the mid kernel
-    up to 512, past that the large kernel where its 128 x 256 blocks fill the
-    CUs, the mid kernel where they would leave most CUs idle, the prefill
-    kernel for r > 64 beyond one round of blocks; the test hooks force each;
-    -1 for a bad descriptor or m."""
-    for k in ("TQ_LARGE", "TQ_MID", "TQ_MID_CT"):
-        monkeypatch.delenv(k, raising=False)
+def test_kernel_choice(L):
+    """tq_dual_gemm_kernel: the decode kernel up to 16 tokens (while their
+    activation codes fit its LDS), the mid kernel up to 512, past that the
+    large kernel where its 128 x 256 blocks fill the CUs, the mid kernel where
+    they would leave most CUs idle, the prefill kernel for r > 64 beyond one
+    round of blocks; -1 for a bad descriptor or m."""
     d = tq.weight_desc_init(4096, 4096, 64)           # n, k, r
     assert [tq.dual_gemm_kernel(d, m) for m in (1, 16, 17, 512, 2048)] == \
         ["decode", "decode", "mid", "mid", "large"]
     assert tq.dual_gemm_kernel(tq.weight_desc_init(96, 4096, 64), 600) == "mid"
     assert tq.dual_gemm_kernel(tq.weight_desc_init(14336, 4096, 128), 4096) == "prefill"
-    monkeypatch.setenv("TQ_MID", "1")
-    assert tq.dual_gemm_kernel(d, 2048) == "mid" and tq.dual_gemm_kernel(d, 8) == "decode"
-    monkeypatch.delenv("TQ_MID")
-    monkeypatch.setenv("TQ_LARGE", "0")
-    assert tq.dual_gemm_kernel(d, 2048) == "prefill" and tq.dual_gemm_kernel(d, 300) == "mid"
+    assert tq.dual_gemm_kernel(tq.weight_desc_init(8192, 28672, 128), 1) == "decode"
+    assert tq.dual_gemm_kernel(tq.weight_desc_init(8192, 28672, 128), 8) == "decode"
+    assert tq.dual_gemm_kernel(tq.weight_desc_init(8192, 28672, 128), 9) == "mid"
+    assert tq.dual_gemm_kernel(tq.weight_desc_init(4096, 14336, 64), 16) == "decode"
+    assert tq.dual_gemm_kernel(tq.weight_desc_init(4096, 14400, 64), 16) == "mid"
     assert L.tq_dual_gemm_kernel(ctypes.byref(d), 0) == -1
     assert L.tq_dual_gemm_kernel(ctypes.byref(tq.WeightDesc()), 100) == -1
     assert L.tq_dual_gemm_kernel(None, 100) == -1
