@@ -11,7 +11,7 @@
 
 namespace {
 
-constexpr int32_t kMagic = 0x54513401;  // "TQ4" + layout version 1
+constexpr int32_t kMagic = 0x54513402;  // "TQ4" + layout version 2
 
 inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 inline uint64_t round_up(uint64_t v, uint64_t a) { return (v + a - 1) / a * a; }
@@ -54,10 +54,13 @@ tq_status tq_weight_desc_init(int n, int k, int rank, int group, tq_weight_desc 
   d.magic = kMagic;
   const uint64_t kg = (uint64_t)k / 64;
   uint64_t off = 0;
-  d.off_w = off;   off = round_up(off + (uint64_t)d.n_pad / 32 * kg * 1024, 256);
-  d.off_ws = off;  off = round_up(off + kg * (uint64_t)d.n_pad * 2, 256);
-  d.off_l1 = off;  off = round_up(off + (uint64_t)d.r_pad32 / 32 * kg * 1024, 256);
-  d.off_l1s = off; off = round_up(off + kg * (uint64_t)d.r_pad32 * 2, 256);
+  // The code sections end in 1 KiB of zeros and the scale sections in one
+  // row of zero scales: a kernel may read one K-group past the last, where
+  // the activation codes are zero, and its products then add exactly zero.
+  d.off_w = off;   off = round_up(off + (uint64_t)d.n_pad / 32 * kg * 1024 + 1024, 256);
+  d.off_ws = off;  off = round_up(off + (kg + 1) * (uint64_t)d.n_pad * 2, 256);
+  d.off_l1 = off;  off = round_up(off + (uint64_t)d.r_pad32 / 32 * kg * 1024 + (rank ? 1024 : 0), 256);
+  d.off_l1s = off; off = round_up(off + (rank ? kg + 1 : 0) * (uint64_t)d.r_pad32 * 2, 256);
   d.off_l2 = off;  off = round_up(off + (uint64_t)d.n_pad / 32 * ((uint64_t)d.r_pad64 / 64) * 1024, 256);
   d.off_l2s = off;
   const uint64_t rgroups = rank == 0 ? 0 : (uint64_t)rank / (uint64_t)d.group_r;

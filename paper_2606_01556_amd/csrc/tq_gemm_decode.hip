@@ -8,19 +8,17 @@
 // (m x r) and every work-group forms all of it in its own registers, so no
 // work-group waits for another; the price is that each CU reads all of L1
 // (from L2, where the first reader leaves it) in addition to its columns.
-//  * Wavefront w < ceil(r / 16) owns rank tile w of H and walks every K-group
-//    pair in ascending order, so its fp32 chain (one fma per K-group,
-//    ascending, with the exact scale product s_x s_L1) stays in registers
-//    and H is bit-identical to the oracle's.
+//  * Wavefront w < ceil(r / 16) owns rank tile w of H and walks every
+//    K-group pair in ascending order, so its fp32 chain (one fma per K-group,
+//    ascending, with the exact product I s_x) stays in registers and H is
+//    bit-identical to the oracle's.
 //  * The other wavefronts take the residual work: each owns one or two of
 //    the column tiles and every NPH-th K-group pair (NPH wavefronts share a
 //    tile group); their partial sums are added in a fixed order at the end
 //    (the order of Y's fp32 accumulation is free; H's is not).
-//  * Operands stream from global memory straight into registers, 16 pairs
-//    ahead for a stage-1 wavefront and 16 / (its tiles) pairs ahead for a
-//    residual one, so a CU keeps ~256 KiB of loads in flight (the L1 bytes
-//    come from L2, at its latency); there is no LDS staging and no barrier in
-//    the K loop.  The
+//  * Operands stream from global memory straight into registers through
+//    per-wavefront rings of 8 to 10 pairs (the L1 bytes come from L2, at its
+//    latency); there is no LDS staging and no barrier in the K loop.  The
 //    activation codes (a few KiB at these sizes) are copied to LDS once, or,
 //    for the fp16 entry point, quantized into LDS by the work-group itself
 //    (Sec. 4.3: the activation tile is quantized once and reused by both
@@ -77,26 +75,32 @@ template <int CT, int RF> struct DRes {
 // and, aliased, the epilogue's residual partials, H, Q_H and s_H; the fp32
 // activation scales follow it.
 struct DLayout {
-  int xa, epi_res, epi_h, epi_q, epi_sh, xs, is, total;
+  int xa, epi_res, epi_h, epi_q, epi_sh, xs, total;
   static constexpr int HSTR = kMaxRank + 1;   // fp32 per H row
   static constexpr int QSTR = kMaxRank + 16;  // bytes per Q_H row
-  // is_bytes: the two-pass path's int16 integer sums (after the scales)
-  __host__ __device__ DLayout(int kg, int mx, int xb, int ct, int nres, int is_bytes = 0) {
+  // res_bytes: the residual partials [NPH][CT][16][16] fp32
+  __host__ __device__ DLayout(int kg, int mx, int xb, int res_bytes) {
     const int kgp = (kg + 1) / 2 * 2;
     xa = kgp * mx * xb + 32;   // + a 32-byte zero pad
     epi_res = 0;
-    epi_h = nres * ct * 256 * 4 / (ct == 1 ? 1 : ct / 2);   // [NPH][CT][16][16] fp32
+    epi_h = res_bytes;
     epi_q = epi_h + 16 * HSTR * 4;
     epi_sh = epi_q + 16 * QSTR;
     const int epi_end = epi_sh + 2 * 16 * 4;
     xs = ((xa > epi_end ? xa : epi_end) + 15) / 16 * 16;
-    is = (xs + kgp * mx * 4 + 15) / 16 * 16;
-    total = is + is_bytes;
+    total = xs + kgp * mx * 4;
   }
 };
 
 __host__ __device__ inline int rank_tiles(int r) { return (r + 15) / 16; }
-__host__ __device__ inline int res_waves(int r) { return DW - rank_tiles(r); }
+
+// The K-loop roles: wavefronts 0 .. R - 1 form H, the others the residual.
+template <int MODE, int CT>
+__host__ __device__ inline DLayout decode_layout(int kg, int r) {
+  using DR = DRes<CT, DMode<MODE>::RF>;
+  const int nph = (DW - rank_tiles(r)) / DR::TG;
+  return DLayout(kg, DMode<MODE>::MX, DMode<MODE>::XB, nph * CT * 1024);
+}
 
 // max over runs of n = 8, 16 or 32 aligned lanes, in every lane of the run
 __device__ __forceinline__ float dpp_max(float a, int ctrl_sel) {
@@ -153,16 +157,9 @@ struct ResSlot {
   uint32_t swa[CTW], swb[CTW];   // fp16 weight scales (TOK8: the lane's own group in swa)
 };
 
-// TWO (single token only): the stage-1 wavefronts share all (pair, rank
-// tile) products and park their exact integer sums as int16 in LDS; after
-// the K loop, ceil(16 R / 64) wavefronts run each rank's ascending chain over
-// them.  This spreads the products over ns wavefronts instead of one per
-// rank tile.
-template <int MODE, int CT, bool FQ, bool TWO>
+template <int MODE, int CT, bool FQ>
 __global__ __launch_bounds__(64 * DW) void dual_gemm_decode_kernel(GemmArgs a,
-                                                                   const uint16_t *__restrict__ xh,
-                                                                   int ns) {
-  static_assert(!TWO || MODE == 1, "the two-pass path serves a single token");
+                                                                   const uint16_t *__restrict__ xh) {
   using MD = DMode<MODE>;
   constexpr int MX = MD::MX, MV = MD::MV, XB = MD::XB;
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
@@ -173,12 +170,11 @@ __global__ __launch_bounds__(64 * DW) void dual_gemm_decode_kernel(GemmArgs a,
   const int KG = geo.k / kGroup, NP = (KG + 1) / 2;
   const int m = a.m;
   const int r = geo.r, R = rank_tiles(r);
-  const int NS = TWO ? ns : R;    // stage-1 wavefronts
+  const int NS = R;   // stage-1 wavefronts
   const int NRES = DW - NS;
   const int ct16 = geo.n_pad / 16;
   const int c0 = blockIdx.x * CT;
-  const DLayout LY(KG, MX, XB, CT, NRES, TWO ? NP * R * 64 : 0);
-  int16_t *IS = reinterpret_cast<int16_t *>(smem + LY.is);   // [pair][rank tile][group][16]
+  const DLayout LY = decode_layout<MODE, CT>(KG, r);
   uint8_t *XA = smem;
   float *XS = reinterpret_cast<float *>(smem + LY.xs);
   const uint8_t *wcodes = a.packed + geo.off_w;
@@ -206,24 +202,25 @@ __global__ __launch_bounds__(64 * DW) void dual_gemm_decode_kernel(GemmArgs a,
   // so the compiler can count the outstanding loads and wait only for the
   // slot it uses.  Lane quarters q < 2 take group A = 2p, q >= 2 group B.
   // Addresses are a wave-uniform base (pair p) plus a fixed 32-bit lane
-  // offset, so the compiler forms them mostly with scalar adds.  On an odd
-  // tail (group 2p + 1 == KG) the group-B lanes re-read group KG - 1, whose
-  // products the zero activation codes of group KG cancel.
+  // offset, kept to a few scalar operations per load: the scalar unit, which
+  // all wavefronts of a CU share, is what a costlier form saturates first.
+  // On an odd tail (group 2p + 1 == KG) the group-B lanes read the zero codes
+  // and zero scale row that follow each section in the packed buffer.
+  // (Section offsets fit 32 bits: the packed buffer is below 4 GiB.)
   const int gq = q >> 1;
-  auto tail_adj = [&](int p) -> uint32_t {
-    return (KG & 1) && p == NP - 1 ? (uint32_t)gq * 1024u : 0u;
-  };
   const uint32_t l1_lane = (uint32_t)(((wave >> 1) * KG * 64 + gq * 64 + qh * 32 + (wave & 1) * 16 + c16) * 16);
   const uint32_t l1s_lane = (uint32_t)(16 * wave + c16) * 2;
+  const uint32_t l1s_pair = (uint32_t)geo.r_pad32 * 4, ws_pair = (uint32_t)geo.n_pad * 4;
+  const uint8_t *l1sb = reinterpret_cast<const uint8_t *>(l1scales);
+  const uint8_t *wsb = reinterpret_cast<const uint8_t *>(wscales);
   auto load_s1 = [&](S1Slot &S, int p) {
-    S.l1 = *reinterpret_cast<const u32x4 *>(l1codes + (uint32_t)(p * 2048) + (l1_lane - tail_adj(p)));
-    // (section offsets fit 32 bits: the whole packed buffer is below 4 GiB)
-    const uint8_t *sb = reinterpret_cast<const uint8_t *>(l1scales) + (uint32_t)(2 * p * geo.r_pad32 * 2);
-    const uint8_t *sbb = reinterpret_cast<const uint8_t *>(l1scales) + (uint32_t)(min(2 * p + 1, KG - 1) * geo.r_pad32 * 2);
+    S.l1 = *reinterpret_cast<const u32x4 *>(l1codes + (uint32_t)(p * 2048) + l1_lane);
+    const uint8_t *sb = l1sb + (uint32_t)p * l1s_pair;
     S.sla = *reinterpret_cast<const uint16_t *>(sb + l1s_lane);
-    S.slb = *reinterpret_cast<const uint16_t *>(sbb + l1s_lane);
+    S.slb = *reinterpret_cast<const uint16_t *>(sb + (uint32_t)geo.r_pad32 * 2 + l1s_lane);
   };
   uint32_t w_lane[CTW], ws_lane[CTW];
+  const uint32_t ws_gq = (uint32_t)(gq * geo.n_pad * 2);   // the lane's own group (TOK8)
 #pragma unroll
   for (int j = 0; j < CTW; j++) {
     const int ct = min(ctw0 + j, ct16 - 1);
@@ -231,17 +228,15 @@ __global__ __launch_bounds__(64 * DW) void dual_gemm_decode_kernel(GemmArgs a,
     ws_lane[j] = (uint32_t)(16 * ct + c16) * 2;
   }
   auto load_res = [&](ResSlot<CTW> &S, int p) {
-    const uint8_t *sa = reinterpret_cast<const uint8_t *>(wscales) + (uint32_t)(2 * p * geo.n_pad * 2);
-    const uint8_t *sbb = reinterpret_cast<const uint8_t *>(wscales) + (uint32_t)(min(2 * p + 1, KG - 1) * geo.n_pad * 2);
+    const uint8_t *sa = wsb + (uint32_t)p * ws_pair;
 #pragma unroll
     for (int j = 0; j < CTW; j++) {
-      S.w[j] = *reinterpret_cast<const u32x4 *>(wcodes + (uint32_t)(p * 2048) + (w_lane[j] - tail_adj(p)));
+      S.w[j] = *reinterpret_cast<const u32x4 *>(wcodes + (uint32_t)(p * 2048) + w_lane[j]);
       if constexpr (MD::TOK8) {
-        // the lane's own group: A for quarters 0-1, B for 2-3
-        S.swa[j] = *reinterpret_cast<const uint16_t *>((gq ? sbb : sa) + ws_lane[j]);
+        S.swa[j] = *reinterpret_cast<const uint16_t *>(sa + (ws_lane[j] + ws_gq));
       } else {
         S.swa[j] = *reinterpret_cast<const uint16_t *>(sa + ws_lane[j]);
-        S.swb[j] = *reinterpret_cast<const uint16_t *>(sbb + ws_lane[j]);
+        S.swb[j] = *reinterpret_cast<const uint16_t *>(sa + (uint32_t)geo.n_pad * 2 + ws_lane[j]);
       }
     }
   };
@@ -433,38 +428,7 @@ __global__ __launch_bounds__(64 * DW) void dual_gemm_decode_kernel(GemmArgs a,
 
   // The two roles keep their rings in separate scopes, so their registers
   // overlap.  Each issues its first loads, then joins the prologue's barrier.
-  if (TWO && s1) {
-    // pass A: items it = wave, wave + NS, ... of the NP x R (pair, rank tile)
-    // products; the exact sums of token 0 (rows 0 and 8) go to LDS as int16
-    const int nit = NP * R;
-    const int nmy = wave < nit ? (nit - wave + NS - 1) / NS : 0;
-    const int ilast = nmy > 0 ? nmy - 1 : 0;
-    const uint32_t lanepart = (uint32_t)((gq * 64 + qh * 32 + c16) * 16);
-    auto load_a = [&](u32x4 &f, int i) {
-      const int it = wave + i * NS, p = it / R, rt = it - p * R;
-      const uint32_t off = (uint32_t)(((rt >> 1) * KG * 64) * 16 + (rt & 1) * 256 + p * 2048);
-      f = *reinterpret_cast<const u32x4 *>(l1codes + off + (lanepart - tail_adj(p)));
-    };
-    u32x4 F[D1];
-#pragma unroll
-    for (int s = 0; s < D1; s++) load_a(F[s], min(s, ilast));
-    prologue();
-    for (int i0 = 0; i0 < nmy; i0 += D1) {
-#pragma unroll
-      for (int s = 0; s < D1; s++) {
-        const int i = i0 + s;
-        if (i < nmy) {
-          const int it = wave + i * NS, p = it / R;
-          v4f I = mfma_codes_16x16x128(act_op(p), unpack32(F[s]));
-          // the product reads its operands from every lane: keep it (and the
-          // unpacking) out of the store branch below
-          asm volatile("" : "+v"(I));
-          if ((q & 1) == 0) IS[(it * 2 + gq) * 16 + c16] = (int16_t)(int)I[0];
-        }
-        load_a(F[s], min(i + D1, ilast));
-      }
-    }
-  } else if (s1) {
+  if (s1) {
     S1Slot S1[D1];
 #pragma unroll
     for (int s = 0; s < D1; s++) load_s1(S1[s], min(s, NP - 1));
@@ -521,42 +485,12 @@ __global__ __launch_bounds__(64 * DW) void dual_gemm_decode_kernel(GemmArgs a,
         if (store_lane) RES[((ph * CT + tg * CTW + j) * 16 + t) * 16 + c16] = val;
       }
   }
-  if (!TWO && s1) {
+  if (s1) {
 #pragma unroll
     for (int v = 0; v < MV; v++) {
       const int t = MD::TOK8 ? 4 * qh + v : 4 * q + v;
       if (store_lane) HS[t * HSTR + 16 * wave + c16] = hacc[v];
     }
-  }
-  if (TWO && wave * 64 < 16 * R) {
-    // pass B: rank j's chain over every K-group in ascending order,
-    // h = fma(I s_x, s_L1, h) (I s_x exact, as in the one-pass chain); the
-    // L1 scales are fetched 8 groups ahead
-    const int j = wave * 64 + lane;
-    const bool jok = j < 16 * R;
-    const int jj = jok ? j : 0;
-    const int rt = jj >> 4, cj = jj & 15;
-    const uint16_t *slp = l1scales + jj;
-    float h = 0.0f;
-    uint16_t sl[8];
-#pragma unroll
-    for (int e = 0; e < 8; e++) sl[e] = slp[(int64_t)min(e, KG - 1) * geo.r_pad32];
-    for (int g0 = 0; g0 < KG; g0 += 8) {
-      uint16_t sn[8];
-#pragma unroll
-      for (int e = 0; e < 8; e++) sn[e] = slp[(int64_t)min(g0 + 8 + e, KG - 1) * geo.r_pad32];
-#pragma unroll
-      for (int e = 0; e < 8; e++) {
-        const int g = g0 + e;
-        if (g < KG) {
-          const float I = (float)IS[(((g >> 1) * R + rt) * 2 + (g & 1)) * 16 + cj];
-          h = fmaf(I * XS[g * MX], (float)__builtin_bit_cast(_Float16, sl[e]), h);
-        }
-      }
-#pragma unroll
-      for (int e = 0; e < 8; e++) sl[e] = sn[e];
-    }
-    if (jok) HS[j] = h;   // token 0
   }
   const int RB = (r + 63) / 64;   // 64-rank blocks of stage 2 (<= 2)
   if (r > 0) {
@@ -670,45 +604,16 @@ __global__ __launch_bounds__(64 * DW) void dual_gemm_decode_kernel(GemmArgs a,
   }
 }
 
-template <int MODE, int CT, bool FQ, bool TWO>
-hipError_t launch_decode(const GemmArgs &a, const uint16_t *xh, int ns, hipStream_t s) {
-  using MD = DMode<MODE>;
-  const int KG = a.geo.k / kGroup, NP = (KG + 1) / 2, R = rank_tiles(a.geo.r);
-  const DLayout LY(KG, MD::MX, MD::XB, CT, DW - (TWO ? ns : R), TWO ? NP * R * 64 : 0);
+template <int MODE, int CT, bool FQ>
+hipError_t launch_decode(const GemmArgs &a, const uint16_t *xh, hipStream_t s) {
+  const DLayout LY = decode_layout<MODE, CT>(a.geo.k / kGroup, a.geo.r);
   const int tiles16 = a.geo.n_pad / 16;
-  auto kern = dual_gemm_decode_kernel<MODE, CT, FQ, TWO>;
+  auto kern = dual_gemm_decode_kernel<MODE, CT, FQ>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, LY.total);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, dim3((tiles16 + CT - 1) / CT), dim3(64 * DW), LY.total, s, a, xh, ns);
+  hipLaunchKernelGGL(kern, dim3((tiles16 + CT - 1) / CT), dim3(64 * DW), LY.total, s, a, xh);
   return hipGetLastError();
-}
-
-constexpr int kLdsBytes = 160 * 1024;
-
-// Single token with a low-rank branch: the two-pass path when its int16 sums
-// fit the LDS beside the activation codes, with ns stage-1 wavefronts chosen
-// so that the NP R products and the NP CT residual tile-pairs (~1.2 times the
-// work each) finish together, leaving every residual tile group a wavefront.
-template <int CT>
-int two_pass_waves(const GemmArgs &a) {
-  if (a.m != 1 || a.geo.r == 0) return 0;
-  const int KG = a.geo.k / kGroup, NP = (KG + 1) / 2, R = rank_tiles(a.geo.r);
-  const DLayout LY(KG, 1, 64, CT, DW - 1, NP * R * 64);   // the most residual wavefronts
-  if (LY.total > kLdsBytes) return 0;
-  const int tg = DRes<CT, 10>::TG;
-  int ns = (int)(DW * (float)R / ((float)R + 1.2f * CT) + 0.5f);
-  ns = ns < 1 ? 1 : (ns > DW - tg ? DW - tg : ns);
-  return ns;
-}
-
-template <int MODE, int CT, bool FQ>
-hipError_t launch_decode_ct(const GemmArgs &a, const uint16_t *xh, hipStream_t s) {
-  if constexpr (MODE == 1) {
-    const int ns = two_pass_waves<CT>(a);
-    if (ns > 0) return launch_decode<MODE, CT, FQ, true>(a, xh, ns, s);
-  }
-  return launch_decode<MODE, CT, FQ, false>(a, xh, 0, s);
 }
 
 template <int MODE, bool FQ>
@@ -716,10 +621,10 @@ hipError_t launch_decode_mode(const GemmArgs &a, const uint16_t *xh, hipStream_t
   // the fewest 16-column tiles per work-group that keep the grid within one
   // work-group per CU
   const int tiles16 = a.geo.n_pad / 16;
-  if (tiles16 <= 256) return launch_decode_ct<MODE, 1, FQ>(a, xh, s);
-  if (tiles16 <= 512) return launch_decode_ct<MODE, 2, FQ>(a, xh, s);
-  if (tiles16 <= 1024) return launch_decode_ct<MODE, 4, FQ>(a, xh, s);
-  return launch_decode_ct<MODE, 8, FQ>(a, xh, s);
+  if (tiles16 <= 256) return launch_decode<MODE, 1, FQ>(a, xh, s);
+  if (tiles16 <= 512) return launch_decode<MODE, 2, FQ>(a, xh, s);
+  if (tiles16 <= 1024) return launch_decode<MODE, 4, FQ>(a, xh, s);
+  return launch_decode<MODE, 8, FQ>(a, xh, s);
 }
 
 int decode_mode(int m) { return m == 1 ? 1 : (m == 2 ? 2 : (m <= 8 ? 4 : 16)); }

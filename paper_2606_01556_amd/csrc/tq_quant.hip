@@ -175,14 +175,29 @@ __global__ __launch_bounds__(256) void pack_l2_kernel(const uint16_t *__restrict
 
 static unsigned nblocks(int64_t threads) { return (unsigned)((threads + 255) / 256); }
 
+// Zero n16 16-byte words (the slack after a section).
+__global__ __launch_bounds__(256) void zero16_kernel(uint8_t *__restrict__ p, int64_t n16) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t < n16) *reinterpret_cast<u32x4 *>(p + 16 * t) = u32x4{0u, 0u, 0u, 0u};
+}
+
 hipError_t launch_pack(const Geometry &g, const uint16_t *w, const uint16_t *l1,
                        const uint16_t *l2, uint8_t *packed, hipStream_t s) {
   const int kg = g.k / kGroup;
   hipLaunchKernelGGL(pack_kgroups_kernel, dim3(nblocks((int64_t)g.n_pad * kg)), dim3(256), 0, s,
                      w, (int64_t)g.k, (int64_t)1, g.n, g.n_pad, kg, packed + g.off_w,
                      reinterpret_cast<uint16_t *>(packed + g.off_ws));
+  // the slack read past the last K-group: 1 KiB of codes, one scale row
+  hipLaunchKernelGGL(zero16_kernel, dim3(1), dim3(256), 0, s,
+                     packed + g.off_w + (uint64_t)g.n_pad / 32 * kg * 1024, (int64_t)64);
+  hipLaunchKernelGGL(zero16_kernel, dim3(nblocks(g.n_pad / 8)), dim3(256), 0, s,
+                     packed + g.off_ws + (uint64_t)kg * g.n_pad * 2, (int64_t)g.n_pad / 8);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || g.r == 0) return e;
+  hipLaunchKernelGGL(zero16_kernel, dim3(1), dim3(256), 0, s,
+                     packed + g.off_l1 + (uint64_t)g.r_pad32 / 32 * kg * 1024, (int64_t)64);
+  hipLaunchKernelGGL(zero16_kernel, dim3(1), dim3(256), 0, s,
+                     packed + g.off_l1s + (uint64_t)kg * g.r_pad32 * 2, (int64_t)g.r_pad32 / 8);
   hipLaunchKernelGGL(pack_kgroups_kernel, dim3(nblocks((int64_t)g.r_pad32 * kg)), dim3(256), 0,
                      s, l1, (int64_t)1, (int64_t)g.r, g.r, g.r_pad32, kg, packed + g.off_l1,
                      reinterpret_cast<uint16_t *>(packed + g.off_l1s));

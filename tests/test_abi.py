@@ -56,7 +56,11 @@ def test_desc_sizes(L):
     d = tq.weight_desc_init(4096, 4096, 64)
     assert d.n_pad == 4096 and d.r_pad32 == 64 and d.r_pad64 == 64 and d.group_r == 64
     # codes: n*k/2 + scales 2*n*k/64 + L1 codes k*r/2 + scales + L2 codes + scales
-    expect = 4096 * 4096 // 2 + 2 * 4096 * 64 + 4096 * 64 // 2 + 2 * 64 * 64 + 4096 * 64 // 2 + 2 * 4096
+    # + 1 KiB of zeros after each code section and a zero row after each
+    # K-group scale section; sections start at multiples of 256 bytes
+    up = lambda b: (b + 255) // 256 * 256
+    expect = (up(4096 * 4096 // 2 + 1024) + up(2 * 4096 * 65) + up(4096 * 64 // 2 + 1024) + up(2 * 64 * 65)
+              + up(4096 * 64 // 2) + up(2 * 4096))
     assert d.packed_bytes == expect
     offs = [d.off_w, d.off_ws, d.off_l1, d.off_l1s, d.off_l2, d.off_l2s, d.packed_bytes]
     assert offs == sorted(offs) and all(o % 256 == 0 for o in offs)
