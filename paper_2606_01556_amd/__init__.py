@@ -131,7 +131,7 @@ def _tensor(t, name, dtype=None, shape=None, min_bytes=None):
 def _act_checks(desc, x_codes, x_scales, m):
     k = desc.k
     _tensor(x_codes, "x_codes", min_bytes=act_codes_bytes(m, k))
-    _tensor(x_scales, "x_scales", min_bytes=(k // GROUP) * padded_tokens(m) * 2)
+    _tensor(x_scales, "x_scales", min_bytes=(k // desc.group) * padded_tokens(m) * 2)
 
 
 def _y_check(desc, y, m, bf16):
@@ -165,7 +165,7 @@ def quant_act(x, x_codes, x_scales, group: int = GROUP, stream=None):
         raise ValueError(f"x: expected [m, k], got shape {tuple(x.shape)}")
     m, k = x.shape
     _tensor(x_codes, "x_codes", min_bytes=act_codes_bytes(m, k))
-    _tensor(x_scales, "x_scales", min_bytes=(k // GROUP) * padded_tokens(m) * 2)
+    _tensor(x_scales, "x_scales", min_bytes=(k // group) * padded_tokens(m) * 2)
     _check(lib().tq_quant_act(_ptr(x), m, k, group, _ptr(x_codes), _ptr(x_scales), _stream(stream)),
            "tq_quant_act")
 
@@ -302,11 +302,11 @@ def act_codes_bytes(m: int, k: int) -> int:
     return int(lib().tq_act_codes_bytes(m, k))
 
 
-def empty_act(m: int, k: int, device="cuda"):
+def empty_act(m: int, k: int, device="cuda", group: int = GROUP):
     """(x_codes, x_scales) buffers for tq_quant_act / tq_dual_gemm:
     x_codes [m32/32, k/64, W] int32, one tile-major block per 32 tokens and
-    K-group (W = 256: 1 KiB of TQ4 nibbles for m <= 512; W = 512: 2 KiB of fp8
-    operand bytes for larger m), x_scales [k/64, m32] fp16, m32 =
+    64-wide K block (W = 256: 1 KiB of TQ4 nibbles for m <= 512; W = 512: 2 KiB
+    of fp8 operand bytes for larger m), x_scales [k/group, m32] fp16, m32 =
     padded_tokens(m)."""
     import torch
     m32 = padded_tokens(m)
@@ -314,7 +314,7 @@ def empty_act(m: int, k: int, device="cuda"):
     words = nbytes // (m32 // 32 * (k // GROUP) * 4)
     assert words in (256, 512), (m, k, nbytes)
     return (torch.empty((m32 // 32, k // GROUP, words), dtype=torch.int32, device=device),
-            torch.empty((k // GROUP, m32), dtype=torch.float16, device=device))
+            torch.empty((k // group, m32), dtype=torch.float16, device=device))
 
 
 class Layer:
@@ -338,9 +338,9 @@ class Layer:
         if x.dim() != 2 or x.shape[1] != self.k:
             raise ValueError(f"x: expected [m, {self.k}], got shape {tuple(x.shape)}")
         m = x.shape[0]
-        xc, xs = empty_act(m, self.k, x.device)
+        xc, xs = empty_act(m, self.k, x.device, self.desc.group)
         y = torch.empty((m, self.n), dtype=torch.bfloat16 if bf16 else torch.float16, device=x.device)
-        quant_act(x, xc, xs, stream=stream)
+        quant_act(x, xc, xs, self.desc.group, stream=stream)
         dual_gemm(self.desc, self.packed, xc, xs, m, y, bf16, stream)
         return y
 

@@ -17,7 +17,8 @@ inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 
 inline uint64_t round_up(uint64_t v, uint64_t a) { return (v + a - 1) / a * a; }
 
 bool desc_ok(const tq_weight_desc *d) {
-  return d != nullptr && d->magic == kMagic && d->group == 64 && d->k % 64 == 0 && d->n >= 1 &&
+  return d != nullptr && d->magic == kMagic && (d->group == 64 || d->group == 128) &&
+         d->k % d->group == 0 && d->n >= 1 &&
          d->n_pad == (int32_t)round_up((uint64_t)d->n, 32) &&
          d->r_pad32 == (int32_t)round_up((uint64_t)d->rank, 32) &&
          d->r_pad64 == (int32_t)round_up((uint64_t)d->rank, 64);
@@ -26,6 +27,7 @@ bool desc_ok(const tq_weight_desc *d) {
 tq::Geometry geometry(const tq_weight_desc *d) {
   tq::Geometry g;
   g.n = d->n; g.k = d->k; g.r = d->rank; g.gr = d->group_r;
+  g.gk = d->group / 64;
   g.n_pad = d->n_pad; g.r_pad32 = d->r_pad32; g.r_pad64 = d->r_pad64;
   g.off_w = d->off_w; g.off_ws = d->off_ws; g.off_l1 = d->off_l1;
   g.off_l1s = d->off_l1s; g.off_l2 = d->off_l2; g.off_l2s = d->off_l2s;
@@ -40,7 +42,7 @@ extern "C" {
 
 tq_status tq_weight_desc_init(int n, int k, int rank, int group, tq_weight_desc *out) {
   if (out == nullptr) return TQ_ERR_NULL;
-  if (group != 64) return TQ_ERR_GROUP;
+  if (group != 64 && group != 128) return TQ_ERR_GROUP;
   if (n < 1 || k < 1 || n > (1 << 24) || k > (1 << 24)) return TQ_ERR_SHAPE;
   if (k % group != 0) return TQ_ERR_GROUP;
   if (!(rank == 0 || rank == 8 || rank == 16 || rank == 32 || rank == 64 || rank == 128))
@@ -52,15 +54,16 @@ tq_status tq_weight_desc_init(int n, int k, int rank, int group, tq_weight_desc 
   d.r_pad32 = (int32_t)round_up((uint64_t)rank, 32);
   d.r_pad64 = (int32_t)round_up((uint64_t)rank, 64);
   d.magic = kMagic;
-  const uint64_t kg = (uint64_t)k / 64;
+  const uint64_t kg = (uint64_t)k / 64;         // 64-wide code blocks along K
+  const uint64_t kgs = (uint64_t)k / group;     // quantization groups along K
   uint64_t off = 0;
   // The code sections end in 1 KiB of zeros and the scale sections in one
   // row of zero scales: a kernel may read one K-group past the last, where
   // the activation codes are zero, and its products then add exactly zero.
   d.off_w = off;   off = round_up(off + (uint64_t)d.n_pad / 32 * kg * 1024 + 1024, 256);
-  d.off_ws = off;  off = round_up(off + (kg + 1) * (uint64_t)d.n_pad * 2, 256);
+  d.off_ws = off;  off = round_up(off + (kgs + 1) * (uint64_t)d.n_pad * 2, 256);
   d.off_l1 = off;  off = round_up(off + (uint64_t)d.r_pad32 / 32 * kg * 1024 + (rank ? 1024 : 0), 256);
-  d.off_l1s = off; off = round_up(off + (rank ? kg + 1 : 0) * (uint64_t)d.r_pad32 * 2, 256);
+  d.off_l1s = off; off = round_up(off + (rank ? kgs + 1 : 0) * (uint64_t)d.r_pad32 * 2, 256);
   d.off_l2 = off;  off = round_up(off + (uint64_t)d.n_pad / 32 * ((uint64_t)d.r_pad64 / 64) * 1024, 256);
   d.off_l2s = off;
   const uint64_t rgroups = rank == 0 ? 0 : (uint64_t)rank / (uint64_t)d.group_r;
@@ -89,13 +92,13 @@ tq_status tq_pack_weights(const tq_weight_desc *d, const void *w_res, const void
 tq_status tq_quant_act(const void *x, int m, int k, int group, void *x_codes, void *x_scales,
                        void *stream) {
   if (x == nullptr || x_codes == nullptr || x_scales == nullptr) return TQ_ERR_NULL;
-  if (group != 64) return TQ_ERR_GROUP;
+  if (group != 64 && group != 128) return TQ_ERR_GROUP;
   if (m < 0 || m > 65535 * 32 || k < 1 || k > (1 << 24)) return TQ_ERR_SHAPE;
   if (k % group != 0) return TQ_ERR_GROUP;
   if (!aligned16(x) || !aligned16(x_codes) || !aligned16(x_scales)) return TQ_ERR_ALIGN;
   if ((int64_t)m * k >= ((int64_t)1 << 40)) return TQ_ERR_SHAPE;
   if (m == 0) return TQ_OK;
-  return hip_status(tq::launch_quant_act(static_cast<const uint16_t *>(x), m, k,
+  return hip_status(tq::launch_quant_act(static_cast<const uint16_t *>(x), m, k, group / 64,
                                          static_cast<uint32_t *>(x_codes),
                                          static_cast<uint16_t *>(x_scales),
                                          static_cast<hipStream_t>(stream)));
@@ -208,6 +211,9 @@ static tq_status dual_gemm_impl(const tq_weight_desc *d, const void *packed, con
   a.dbg_qh = static_cast<int8_t *>(c.qh);
   a.force_kernel = c.kernel;
   a.mid_ct = c.mid_ct;
+  // 128-wide groups: the kernels built for them so far
+  if (a.geo.gk != 1 && (c.path != Path::Fused || (!fq && !tq::serves_group(tq::choose_kernel(a), a.geo.gk))))
+    return TQ_ERR_GROUP;
   const hipStream_t s = static_cast<hipStream_t>(stream);
   if (fq) return hip_status(tq::launch_dual_gemm_decode(a, static_cast<const uint16_t *>(c.x16), s));
   if (c.path == Path::Unfused) return hip_status(tq::launch_dual_gemm_unfused(a, c.scratch, s));

@@ -17,6 +17,7 @@ int choose_kernel(const GemmArgs &a) {
   // the activation code format follows the same token-count split
   if (a.m <= kDecodeMaxTokens && decode_fits(a.m, a.geo.k)) return kKernelDecode;
   if (!act_codes_fp8(a.m)) return kKernelMid;
+  if (a.geo.gk != 1) return kKernelMid;   // 128-wide groups: built in the mid kernel so far
   // 128 x 256 blocks: the large kernel (16 wavefronts, H formed in the main
   // loop of every block) is faster while its blocks fit in one round over the
   // 256 CUs, and for ranks up to 64 at any size (its H share is then at most a
@@ -31,6 +32,11 @@ int choose_kernel(const GemmArgs &a) {
   const bool mid = large && dual_gemm_mid_cost(a) < rounds * kLargeRound;
   if (mid) return kKernelMid;
   return large ? kKernelLarge : kKernelPrefill;
+}
+
+bool serves_group(int kernel, int gk) {
+  if (gk == 1) return true;
+  return gk == 2 && (kernel == kKernelDecode || kernel == kKernelMid);
 }
 
 hipError_t launch_dual_gemm(const GemmArgs &a, hipStream_t s) {

@@ -210,17 +210,22 @@ __global__ __launch_bounds__(64 * DW) void dual_gemm_decode_kernel(GemmArgs a,
   const int gq = q >> 1;
   const uint32_t l1_lane = (uint32_t)(((wave >> 1) * KG * 64 + gq * 64 + qh * 32 + (wave & 1) * 16 + c16) * 16);
   const uint32_t l1s_lane = (uint32_t)(16 * wave + c16) * 2;
-  const uint32_t l1s_pair = (uint32_t)geo.r_pad32 * 4, ws_pair = (uint32_t)geo.n_pad * 4;
+  // Scale rows: one per quantization group, so a pair of 64-wide blocks spans
+  // two rows (64-wide groups) or one (128-wide groups, gk = 2), and group B's
+  // row is the next one or the same.
+  const int gk = geo.gk;
+  const uint32_t l1s_pair = (uint32_t)geo.r_pad32 * 4 / gk, ws_pair = (uint32_t)geo.n_pad * 4 / gk;
+  const uint32_t l1s_b = gk == 1 ? (uint32_t)geo.r_pad32 * 2 : 0u, ws_b = gk == 1 ? (uint32_t)geo.n_pad * 2 : 0u;
   const uint8_t *l1sb = reinterpret_cast<const uint8_t *>(l1scales);
   const uint8_t *wsb = reinterpret_cast<const uint8_t *>(wscales);
   auto load_s1 = [&](S1Slot &S, int p) {
     S.l1 = *reinterpret_cast<const u32x4 *>(l1codes + (uint32_t)(p * 2048) + l1_lane);
     const uint8_t *sb = l1sb + (uint32_t)p * l1s_pair;
     S.sla = *reinterpret_cast<const uint16_t *>(sb + l1s_lane);
-    S.slb = *reinterpret_cast<const uint16_t *>(sb + (uint32_t)geo.r_pad32 * 2 + l1s_lane);
+    S.slb = *reinterpret_cast<const uint16_t *>(sb + l1s_b + l1s_lane);
   };
   uint32_t w_lane[CTW], ws_lane[CTW];
-  const uint32_t ws_gq = (uint32_t)(gq * geo.n_pad * 2);   // the lane's own group (TOK8)
+  const uint32_t ws_gq = gq * ws_b;   // the lane's own block's group (TOK8)
 #pragma unroll
   for (int j = 0; j < CTW; j++) {
     const int ct = min(ctw0 + j, ct16 - 1);
@@ -236,7 +241,7 @@ __global__ __launch_bounds__(64 * DW) void dual_gemm_decode_kernel(GemmArgs a,
         S.swa[j] = *reinterpret_cast<const uint16_t *>(sa + (ws_lane[j] + ws_gq));
       } else {
         S.swa[j] = *reinterpret_cast<const uint16_t *>(sa + ws_lane[j]);
-        S.swb[j] = *reinterpret_cast<const uint16_t *>(sa + (uint32_t)geo.n_pad * 2 + ws_lane[j]);
+        S.swb[j] = *reinterpret_cast<const uint16_t *>(sa + ws_b + ws_lane[j]);
       }
     }
   };
@@ -246,37 +251,49 @@ __global__ __launch_bounds__(64 * DW) void dual_gemm_decode_kernel(GemmArgs a,
   const int KGP = 2 * NP;
   auto prologue = [&]() {
     if constexpr (FQ) {
-      // eight lanes per (token, group), eight values each; the steps are those
-      // of the quantizer kernel, so the codes and scales are the same bits
+      // eight lanes per (token, quantization group), eight values of each of
+      // the group's gk 64-wide blocks; the steps are those of the quantizer
+      // kernel, so the codes and scales are the same bits
       const int e = lane & 7;
-      const int nitem = m * KG;
+      const int KQ = KG / gk;
+      const int nitem = m * KQ;
       for (int it0 = 0; it0 < nitem; it0 += 64 * DW / 8) {
         const int it = it0 + tid / 8;
         const bool live = it < nitem;
-        const int t = live ? it / KG : 0, g = live ? it % KG : 0;
-        const u32x4 raw = *reinterpret_cast<const u32x4 *>(xh + (int64_t)t * geo.k + g * kGroup + 8 * e);
-        float v[8];
+        const int t = live ? it / KQ : 0, g0 = live ? it % KQ * gk : 0, g1 = g0 + gk - 1;
+        const uint16_t *src = xh + (int64_t)t * geo.k + 8 * e;
+        const u32x4 raw0 = *reinterpret_cast<const u32x4 *>(src + g0 * kGroup);
+        u32x4 raw1 = raw0;
+        if (gk == 2) raw1 = *reinterpret_cast<const u32x4 *>(src + g1 * kGroup);
+        float v0[8], v1[8];
 #pragma unroll
         for (int i = 0; i < 4; i++) {
-          v[2 * i] = half_bits_to_float((uint16_t)(raw[i] & 0xffffu));
-          v[2 * i + 1] = half_bits_to_float((uint16_t)(raw[i] >> 16));
+          v0[2 * i] = half_bits_to_float((uint16_t)(raw0[i] & 0xffffu));
+          v0[2 * i + 1] = half_bits_to_float((uint16_t)(raw0[i] >> 16));
+          v1[2 * i] = half_bits_to_float((uint16_t)(raw1[i] & 0xffffu));
+          v1[2 * i + 1] = half_bits_to_float((uint16_t)(raw1[i] >> 16));
         }
         float amax = 0.0f;
 #pragma unroll
-        for (int i = 0; i < 8; i++) amax = fmaxf(amax, fabsf(v[i]));
+        for (int i = 0; i < 8; i++) amax = fmaxf(amax, fmaxf(fabsf(v0[i]), fabsf(v1[i])));
         amax = max8_dpp(amax);
         uint16_t s16;
         const float sc = q4_scale(amax, s16);
         const float y = sc == 0.0f ? 0.0f : __builtin_amdgcn_rcpf(sc);
-        uint32_t b0, b1;
-        quant8_fp8(v, sc, y, b0, b1);
-        if (live) {
-          uint8_t *dst = XA + (g * MX + t) * XB;
-          if constexpr (MD::XFP8)
-            *reinterpret_cast<uint2 *>(dst + 8 * e) = make_uint2(b0, b1);
-          else
-            *reinterpret_cast<uint32_t *>(dst + 4 * e) = b0 | __builtin_amdgcn_alignbit(b1, b1, 28);
-          if (e == 0) XS[g * MX + t] = sc;
+#pragma unroll
+        for (int b = 0; b < 2; b++) {
+          if (b == 1 && gk == 1) break;
+          uint32_t b0, b1;
+          quant8_fp8(b == 0 ? v0 : v1, sc, y, b0, b1);
+          const int g = b == 0 ? g0 : g1;
+          if (live) {
+            uint8_t *dst = XA + (g * MX + t) * XB;
+            if constexpr (MD::XFP8)
+              *reinterpret_cast<uint2 *>(dst + 8 * e) = make_uint2(b0, b1);
+            else
+              *reinterpret_cast<uint32_t *>(dst + 4 * e) = b0 | __builtin_amdgcn_alignbit(b1, b1, 28);
+            if (e == 0) XS[g * MX + t] = sc;
+          }
         }
       }
       for (int idx = tid; idx < KGP * MX; idx += 64 * DW)
@@ -299,7 +316,7 @@ __global__ __launch_bounds__(64 * DW) void dual_gemm_decode_kernel(GemmArgs a,
       }
       for (int idx = tid; idx < KGP * MX; idx += 64 * DW) {
         const int g = idx / MX, t = idx % MX;
-        XS[idx] = g < KG && t < m ? half_bits_to_float(a.xs[(int64_t)g * a.ms + t]) : 0.0f;
+        XS[idx] = g < KG && t < m ? half_bits_to_float(a.xs[(int64_t)(g / gk) * a.ms + t]) : 0.0f;
       }
     }
     // zero codes for the token slots past m, the odd tail group and the pad
@@ -395,8 +412,12 @@ __global__ __launch_bounds__(64 * DW) void dual_gemm_decode_kernel(GemmArgs a,
 #pragma unroll
     for (int v = 0; v < MV; v++) {
       const float ib = MD::TOK8 ? upper_half(P.I[v]) : P.I2[v];
-      hacc[v] = fmaf(P.I[v] * P.sxa[v], (float)sla, hacc[v]);
-      hacc[v] = fmaf(ib * P.sxb[v], (float)slb, hacc[v]);
+      // a 128-wide group: its two halves' sums add exactly (|I| < 2^13) and
+      // the second step adds +0, which leaves the (never negative-zero) h as is
+      const float i1 = gk == 2 ? P.I[v] + ib : P.I[v];
+      const float i2 = gk == 2 ? 0.0f : ib;
+      hacc[v] = fmaf(i1 * P.sxa[v], (float)sla, hacc[v]);
+      hacc[v] = fmaf(i2 * P.sxb[v], (float)slb, hacc[v]);
     }
   };
   auto residual = [&](const ResSlot<CTW> &Sl, int p) {
@@ -569,7 +590,8 @@ __global__ __launch_bounds__(64 * DW) void dual_gemm_decode_kernel(GemmArgs a,
             l2codes + (((int64_t)(ct >> 1) * (geo.r_pad64 / 64) + rbq) * 64 + L) * 16);
         const int col = ct * 16 + c16;
         const float s2a = half_bits_to_float(l2scales[col]);
-        const float s2b = RB > 1 ? half_bits_to_float(l2scales[(int64_t)geo.n_pad + col]) : 0.0f;
+        const int hg1 = 64 / geo.gr;   // rank group of the second 64-rank block (0 if gr = 128)
+        const float s2b = RB > 1 ? half_bits_to_float(l2scales[(int64_t)hg1 * geo.n_pad + col]) : 0.0f;
         const v8i qa = lds_v8i(QS + c16 * QSTR + rbq * 64 + qh * 32);
         const v8i lb = unpack32(l2raw);
         {
@@ -580,7 +602,7 @@ __global__ __launch_bounds__(64 * DW) void dual_gemm_decode_kernel(GemmArgs a,
         if (RB > 1) {
           const v4f cb = mfma_codes_16x16x128(q < 2 ? z8 : qa, lb);
 #pragma unroll
-          for (int v = 0; v < 4; v++) ylr[v] = fmaf(cb[v], SHS[16 + orow0 + v] * s2b, ylr[v]);
+          for (int v = 0; v < 4; v++) ylr[v] = fmaf(cb[v], SHS[16 * hg1 + orow0 + v] * s2b, ylr[v]);
         }
       }
       // the matrix-core products above read operands from every lane: keep

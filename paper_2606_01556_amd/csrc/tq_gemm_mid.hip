@@ -159,6 +159,11 @@ __device__ __forceinline__ v16f m_codes_half(v8i a, v8i b) {
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, z, 0, 0, 0, kScale2p9 - 1, 0,
                                                          kScale2p9);
 }
+// the same added to c (exact: half sums of a 128-wide group stay below 2^13)
+__device__ __forceinline__ v16f m_codes_half_acc(v8i a, v8i b, v16f c) {
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, kScale2p9 - 1, 0,
+                                                         kScale2p9);
+}
 
 template <int RT, int CT, bool FP8>
 __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, int n_rb) {
@@ -197,14 +202,18 @@ __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, i
   // Shared load sh < MCG * SHL is half sh % SHL of the activation block of
   // group sh / SHL of the chunk, the rest are scale pieces 64 s + lane.
   // Wavefront w issues loads w and (fp8) w + MW, modulo NSH: loads past NSH
-  // repeat one (same bytes, same place).
+  // repeat one (same bytes, same place).  A scale row serves gk = group / 64
+  // blocks (shift = 1 for 128-wide groups): block g reads row g >> shift, so
+  // each block of a chunk slot holds its group's scales.
+  const int gk = geo.gk;
   struct Shared {
     const uint8_t *base;
     uint32_t stride, dst;
-    int gi;
+    int gi, shift;
   };
   auto shared_load = [&](int sh) {
     Shared L;
+    L.shift = 0;
     if (sh < MCG * C::SHL) {
       const int gi = sh / C::SHL, half = sh % C::SHL;
       L.base = xc + half * 1024 + lane * 16;
@@ -212,6 +221,7 @@ __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, i
       L.gi = gi;
       L.dst = C::S_X + gi * C::XB + half * 1024;
     } else {
+      L.shift = gk - 1;
       const int s = sh - MCG * C::SHL;
       const int p0 = 64 * s + lane;
       const int p = p0 < C::NP ? p0 : 0;
@@ -257,7 +267,8 @@ __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, i
         const int q0 = lane, q = q0 < C::RB * CT * 4 ? q0 : 0;
         const int h = q / (4 * CT), j = (q / 4) % CT, part = q % 4;
         const int col = min(32 * (cb * CT + j) + 8 * part, geo.n_pad - 8);
-        mdma(l2scales + ((int64_t)h * geo.n_pad + col) * 2, lds0 + C::OFF_L2 + CT * C::RB * 1024);
+        const int hg = h * 64 / geo.gr;   // rank group of 64-rank block h (gr >= 64 here)
+        mdma(l2scales + ((int64_t)hg * geo.n_pad + col) * 2, lds0 + C::OFF_L2 + CT * C::RB * 1024);
       }
     }
   };
@@ -296,10 +307,10 @@ __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, i
     // block loads (wave-uniform bases in scalar registers, lane offset
     // 16 * lane, MCG KiB per chunk).  A chunk that runs past the last K-group
     // clamps its groups to the last one.
-    const uint8_t *sh_addr = sl0.base + (uint64_t)sl0.gi * sl0.stride;
-    const uint64_t sh_inc = (uint64_t)MCG * sl0.stride;
-    const uint8_t *sh_addr1 = sl1.base + (uint64_t)sl1.gi * sl1.stride;
-    const uint64_t sh_inc1 = (uint64_t)MCG * sl1.stride;
+    const uint8_t *sh_addr = sl0.base + (uint64_t)(sl0.gi >> sl0.shift) * sl0.stride;
+    const uint64_t sh_inc = (uint64_t)(MCG >> sl0.shift) * sl0.stride;
+    const uint8_t *sh_addr1 = sl1.base + (uint64_t)(sl1.gi >> sl1.shift) * sl1.stride;
+    const uint64_t sh_inc1 = (uint64_t)(MCG >> sl1.shift) * sl1.stride;
     const uint32_t lane16 = lane * 16;
     const uint8_t *fb[NF > 0 ? NF : 1];
 #pragma unroll
@@ -318,9 +329,9 @@ __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, i
           fb[k] += MCG * 1024;
         }
       } else {
-        mdma(sl0.base + (uint64_t)min(MCG * c + sl0.gi, KG - 1) * sl0.stride, slot + sl0.dst);
+        mdma(sl0.base + (uint64_t)(min(MCG * c + sl0.gi, KG - 1) >> sl0.shift) * sl0.stride, slot + sl0.dst);
         if constexpr (FP8)
-          mdma(sl1.base + (uint64_t)min(MCG * c + sl1.gi, KG - 1) * sl1.stride, slot + sl1.dst);
+          mdma(sl1.base + (uint64_t)(min(MCG * c + sl1.gi, KG - 1) >> sl1.shift) * sl1.stride, slot + sl1.dst);
 #pragma unroll
         for (int k = 0; k < NF; k++) {
           const int g = min(MCG * c + item_gi(k), KG - 1);
@@ -374,6 +385,21 @@ __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, i
           const int so = H ? (C::NPX + C::NPW) * 16 + (gi * 32 * RT + 32 * wave + l32) * 2
                            : C::NPX * 16 + (gi * 32 * CT + 32 * item_tile(k) + l32) * 2;
           sb[k] = *reinterpret_cast<const uint16_t *>(S + C::S_SC + so);
+        }
+        if (H && gk == 2) {
+          // 128-wide groups: the half sums of a group's two blocks add
+          // exactly in the matrix core, then one fma per element and group
+          // (the oracle's step)
+#pragma unroll
+          for (int kp = 0; kp < NF / 2; kp++) {
+            const v16f c0 = m_codes_half(av[2 * kp], unpack32(bv[2 * kp]));
+            const v16f cg = m_codes_half_acc(av[2 * kp + 1], unpack32(bv[2 * kp + 1]), c0);
+            const v16f pg = m_outer2(sa[2 * kp], sb[2 * kp]);
+#pragma unroll
+            for (int v = 0; v < 16; v++) acc[0][v] = fmaf(cg[v], pg[v], acc[0][v]);
+          }
+          rslot = rslot + C::SLOT == D * C::SLOT ? 0 : rslot + C::SLOT;
+          continue;
         }
         // Every operand of the chunk is read before the first product; then
         // item k's two products go to the matrix core while the vector ALU
@@ -525,7 +551,7 @@ __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, i
           const v16f cbv = mfma_codes_32x32x64(qa, lb);
 #pragma unroll
           for (int v = 0; v < 16; v++)
-            ylr[v] = fmaf(cbv[v], SHS[rb * 32 + row_of_32x32(lane, v)] * sl2, ylr[v]);
+            ylr[v] = fmaf(cbv[v], SHS[(rb * 64 / geo.gr) * 32 + row_of_32x32(lane, v)] * sl2, ylr[v]);
         }
       }
       // the matrix-core products above read operands from every lane: keep

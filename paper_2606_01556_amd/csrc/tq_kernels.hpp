@@ -32,6 +32,7 @@ inline size_t act_codes_bytes(int m, int k) {
 //               reduction axis (zero past r).  Scales: [r/group_r][n_pad].
 struct Geometry {
   int n, k, r, gr, n_pad, r_pad32, r_pad64;
+  int gk;   // 64-wide K blocks per quantization group (group / 64: 1 or 2)
   uint64_t off_w, off_ws, off_l1, off_l1s, off_l2, off_l2s;
 };
 
@@ -52,8 +53,9 @@ struct GemmArgs {
   int mid_ct;           // 0: chosen by the mid kernel's cost model; else 1, 2 or 4 (tests)
 };
 
-hipError_t launch_quant_act(const uint16_t *x, int m, int k, uint32_t *codes, uint16_t *scales,
-                            hipStream_t s);
+// gk: 64-wide K blocks per quantization group (1 or 2)
+hipError_t launch_quant_act(const uint16_t *x, int m, int k, int gk, uint32_t *codes,
+                            uint16_t *scales, hipStream_t s);
 hipError_t launch_pack(const Geometry &g, const uint16_t *w, const uint16_t *l1,
                        const uint16_t *l2, uint8_t *packed, hipStream_t s);
 hipError_t launch_export(const Geometry &g, const uint8_t *packed, uint32_t *wc, uint16_t *ws,
@@ -68,6 +70,8 @@ bool decode_fits(int m, int k);
 // the kernel launch_dual_gemm runs (values of tq_kernel in the C header)
 constexpr int kKernelDecode = 0, kKernelMid = 1, kKernelLarge = 2, kKernelPrefill = 3;
 int choose_kernel(const GemmArgs &a);
+// whether a kernel takes quantization groups of gk 64-wide blocks
+bool serves_group(int kernel, int gk);
 hipError_t launch_dual_gemm_mid(const GemmArgs &a, hipStream_t s);      // mid sizes
 // relative time of the mid kernel's launch: rounds of work-groups over the
 // CUs x tile-groups per work-group and chunk (+3 for its fixed latency)

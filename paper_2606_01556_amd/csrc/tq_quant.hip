@@ -1,20 +1,22 @@
 // Activation quantizer, weight packing and weight export kernels.
 //
 // Quantizer: paper Sec. 2 Eq. (1) with q_max = 7, one fp16 scale per group of
-// 64 consecutive values along the reduction axis (Sec. 5.1), round half to
-// even, codes clamped to [-7, 7], an all-zero group gets scale 0.
+// 64 or 128 consecutive values along the reduction axis (Sec. 5.1), round half
+// to even, codes clamped to [-7, 7], an all-zero group gets scale 0.  Codes
+// are stored in 64-wide K blocks whatever the group; a 128-wide group spans two
+// blocks and has one scale.
 #include "tq_device.hpp"
 #include "tq_kernels.hpp"
 
 namespace tq {
 
 // ---------------------------------------------------------------------------
-// Activations: one work-group of 4 wavefronts per QG consecutive 1 KiB
-// matrix-core blocks of one token tile (32 tokens x QG K-groups).  Wavefront
-// w takes tokens 8 w .. 8 w + 7 of the tile; for each of the QG groups, lane
+// Activations: one work-group of 4 wavefronts per quantization group (GK
+// consecutive 1 KiB matrix-core blocks) of one token tile.  Wavefront
+// w takes tokens 8 w .. 8 w + 7 of the tile; for each of the GK blocks, lane
 // 8 j + 4 h + l quantizes codes 32 h + 8 l .. + 7 of the group for token
 // 8 w + j (16 bytes of the row) into one TQ4 word, and the 8 lanes of a token
-// share the group max through three DPP lane swizzles.  All QG loads of a
+// share the group max through three DPP lane swizzles.  All GK loads of a
 // lane are issued before any is used.  TQ4 output (m <= kMidMaxTokens): token
 // 32 t + i, codes 32 h .. 32 h + 31 of group g land at byte
 // ((t * KG + g) * 64 + 32 h + i) * 16 (the lane order of one matrix-core
@@ -29,70 +31,76 @@ namespace tq {
 // (max8_dpp and quant8_fp8, the per-lane quantizer step, are in tq_device.hpp:
 // the decode kernel quantizes fp16 activations with the same code.)
 
-template <bool FP8, int QG>
+template <bool FP8, int GK>
 __global__ __launch_bounds__(256) void quant_act_kernel(const uint16_t *__restrict__ x, int m,
                                                         int k, uint32_t *__restrict__ codes,
                                                         uint16_t *__restrict__ scales) {
+  // one quantization group of GK 64-wide blocks: the group's max spans them
   const int KG = k / kGroup;
-  const int g0 = blockIdx.x * QG, t = blockIdx.y;
+  const int q0 = blockIdx.x, g0 = q0 * GK, t = blockIdx.y;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int j = lane >> 3, h = (lane >> 2) & 1, l = lane & 3;
   const int i = 8 * w + j;          // token within the tile
   const int row = 32 * t + i;
   const int m32 = (int)gridDim.y * 32;
-  u32x4 raw[QG];
+  u32x4 raw[GK];
   // padding tokens read the last real row (m >= 1) and quantize zeros; every
   // load is issued before the first is used
   const bool live = row < m;
   const uint16_t *src = x + (int64_t)(live ? row : m - 1) * k + g0 * kGroup + 32 * h + 8 * l;
 #pragma unroll
-  for (int q = 0; q < QG; q++) raw[q] = *reinterpret_cast<const u32x4 *>(src + q * kGroup);
+  for (int q = 0; q < GK; q++) raw[q] = *reinterpret_cast<const u32x4 *>(src + q * kGroup);
 #pragma unroll
-  for (int q = 0; q < QG; q++)
+  for (int q = 0; q < GK; q++)
     if (!live) raw[q] = u32x4{0, 0, 0, 0};
+  float v[GK][8];
+  float amax = 0.0f;
 #pragma unroll
-  for (int q = 0; q < QG; q++) {
-    const int g = g0 + q;
-    float v[8];
+  for (int q = 0; q < GK; q++) {
 #pragma unroll
     for (int e = 0; e < 4; e++) {
-      v[2 * e] = half_bits_to_float((uint16_t)(raw[q][e] & 0xffffu));
-      v[2 * e + 1] = half_bits_to_float((uint16_t)(raw[q][e] >> 16));
+      v[q][2 * e] = half_bits_to_float((uint16_t)(raw[q][e] & 0xffffu));
+      v[q][2 * e + 1] = half_bits_to_float((uint16_t)(raw[q][e] >> 16));
     }
-    float amax = 0.0f;
 #pragma unroll
-    for (int e = 0; e < 8; e++) amax = fmaxf(amax, fabsf(v[e]));
-    amax = max8_dpp(amax);
-    uint16_t s16;
-    const float s = q4_scale(amax, s16);
-    const float y = s == 0.0f ? 0.0f : __builtin_amdgcn_rcpf(s);
+    for (int e = 0; e < 8; e++) amax = fmaxf(amax, fabsf(v[q][e]));
+  }
+  amax = max8_dpp(amax);
+  uint16_t s16;
+  const float s = q4_scale(amax, s16);
+  const float y = s == 0.0f ? 0.0f : __builtin_amdgcn_rcpf(s);
+#pragma unroll
+  for (int q = 0; q < GK; q++) {
+    const int g = g0 + q;   // the launch covers the K blocks exactly
     uint32_t b0, b1;
-    quant8_fp8(v, s, y, b0, b1);
-    {   // the launch covers the K-groups exactly (QG divides k / 64)
-      if constexpr (FP8) {
-        const int64_t off = (((int64_t)t * KG + g) * 2 + (l >> 1)) * 256 + (32 * h + i) * 4 + 2 * (l & 1);
-        *reinterpret_cast<uint2 *>(codes + off) = make_uint2(b0, b1);
-      } else {
-        // TQ4 word: the inverse of tq4_to_fp8 (codes 4..7 rotated into the
-        // bits 0x78787878 that codes 0..3 leave free)
-        codes[(((int64_t)t * KG + g) * 64 + 32 * h + i) * 4 + l] = b0 | __builtin_amdgcn_alignbit(b1, b1, 28);
-      }
-      if ((lane & 7) == 0) scales[(int64_t)g * m32 + row] = row < m ? s16 : (uint16_t)0;
+    quant8_fp8(v[q], s, y, b0, b1);
+    if constexpr (FP8) {
+      const int64_t off = (((int64_t)t * KG + g) * 2 + (l >> 1)) * 256 + (32 * h + i) * 4 + 2 * (l & 1);
+      *reinterpret_cast<uint2 *>(codes + off) = make_uint2(b0, b1);
+    } else {
+      // TQ4 word: the inverse of tq4_to_fp8 (codes 4..7 rotated into the
+      // bits 0x78787878 that codes 0..3 leave free)
+      codes[(((int64_t)t * KG + g) * 64 + 32 * h + i) * 4 + l] = b0 | __builtin_amdgcn_alignbit(b1, b1, 28);
     }
   }
+  if ((lane & 7) == 0) scales[(int64_t)q0 * m32 + row] = row < m ? s16 : (uint16_t)0;
 }
 
-hipError_t launch_quant_act(const uint16_t *x, int m, int k, uint32_t *codes, uint16_t *scales,
-                            hipStream_t s) {
+hipError_t launch_quant_act(const uint16_t *x, int m, int k, int gk, uint32_t *codes,
+                            uint16_t *scales, hipStream_t s) {
   const int m32 = (m + 31) / 32 * 32;
   const int KG = k / kGroup;
-  // one K-group per work-group: the kernel is bound by its vector ALU work,
-  // and more groups per work-group measured slower at every size
-  const dim3 grid((unsigned)KG, (unsigned)(m32 / 32));
-  if (act_codes_fp8(m))
-    hipLaunchKernelGGL((quant_act_kernel<true, 1>), grid, dim3(256), 0, s, x, m, k, codes, scales);
-  else
-    hipLaunchKernelGGL((quant_act_kernel<false, 1>), grid, dim3(256), 0, s, x, m, k, codes, scales);
+  // one quantization group per work-group: the kernel is bound by its vector
+  // ALU work, and more groups per work-group measured slower at every size
+  const dim3 grid((unsigned)(KG / gk), (unsigned)(m32 / 32));
+  const bool f8 = act_codes_fp8(m);
+  if (gk == 2) {
+    if (f8) hipLaunchKernelGGL((quant_act_kernel<true, 2>), grid, dim3(256), 0, s, x, m, k, codes, scales);
+    else hipLaunchKernelGGL((quant_act_kernel<false, 2>), grid, dim3(256), 0, s, x, m, k, codes, scales);
+  } else {
+    if (f8) hipLaunchKernelGGL((quant_act_kernel<true, 1>), grid, dim3(256), 0, s, x, m, k, codes, scales);
+    else hipLaunchKernelGGL((quant_act_kernel<false, 1>), grid, dim3(256), 0, s, x, m, k, codes, scales);
+  }
   return hipGetLastError();
 }
 
@@ -103,48 +111,59 @@ hipError_t launch_quant_act(const uint16_t *x, int m, int k, uint32_t *codes, ui
 // Vectors past the real sizes (padding to 32 columns / 64 ranks) get zero
 // codes and zero scales, so every byte of the packed buffer is written.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ void quantize_group_strided(const uint16_t *src, int64_t stride,
-                                                       int len, bool present, uint32_t out[8],
-                                                       uint16_t &s16) {
-  // len <= 64 values starting at src with the given element stride; codes past
-  // len are zero (len is a multiple of 8).
+// The fp16 scale of `len` values at src with the given element stride (0 if
+// !present), and the TQ4 words of the 64 of them starting at element e0
+// (codes past len are zero).
+__device__ __forceinline__ float group_scale_strided(const uint16_t *src, int64_t stride, int len,
+                                                     bool present, uint16_t &s16) {
   float amax = 0.0f;
   if (present)
     for (int i = 0; i < len; i++) amax = fmaxf(amax, fabsf(half_bits_to_float(src[i * stride])));
-  const float s = q4_scale(amax, s16);
+  return q4_scale(amax, s16);
+}
+__device__ __forceinline__ void codes_strided(const uint16_t *src, int64_t stride, int len, int e0,
+                                              bool present, float s, uint32_t out[8]) {
   for (int wd = 0; wd < 8; wd++) {
     int c[8];
     for (int i = 0; i < 8; i++) {
-      const int e = wd * 8 + i;
+      const int e = e0 + wd * 8 + i;
       c[i] = (present && e < len) ? q4_code(half_bits_to_float(src[e * stride]), s) : 0;
     }
     out[wd] = tq4_pack8(c);
   }
 }
 
-// W_res [n][k] rows and L1 [k][r] columns share the block format.
+// W_res [n][k] rows and L1 [k][r] columns share the block format: one thread
+// per (vector, quantization group of gk 64-wide blocks).
 __global__ __launch_bounds__(256) void pack_kgroups_kernel(const uint16_t *__restrict__ src,
                                                            int64_t vec_stride, int64_t elem_stride,
-                                                           int nvec, int nvec_pad, int kgroups,
+                                                           int nvec, int nvec_pad, int kblocks, int gk,
                                                            uint8_t *__restrict__ codes,
                                                            uint16_t *__restrict__ scales) {
+  const int kq = kblocks / gk;
   const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (t >= (int64_t)nvec_pad * kgroups) return;
-  const int g = (int)(t % kgroups);
-  const int v = (int)(t / kgroups);
+  if (t >= (int64_t)nvec_pad * kq) return;
+  const int g = (int)(t % kq);
+  const int v = (int)(t / kq);
   const bool present = v < nvec;
-  uint32_t w[8];
+  const int len = gk * kGroup;
+  const uint16_t *p = present ? src + (int64_t)v * vec_stride + (int64_t)g * len * elem_stride : src;
   uint16_t s16;
-  const uint16_t *p = present ? src + (int64_t)v * vec_stride + (int64_t)g * kGroup * elem_stride : src;
-  quantize_group_strided(p, elem_stride, kGroup, present, w, s16);
-  uint8_t *blk = codes + ((int64_t)(v >> 5) * kgroups + g) * 1024;
-  const int c = v & 31;
-  *reinterpret_cast<u32x4 *>(blk + c * 16) = u32x4{w[0], w[1], w[2], w[3]};
-  *reinterpret_cast<u32x4 *>(blk + (32 + c) * 16) = u32x4{w[4], w[5], w[6], w[7]};
+  const float s = group_scale_strided(p, elem_stride, len, present, s16);
+  for (int b = 0; b < gk; b++) {
+    uint32_t w[8];
+    codes_strided(p, elem_stride, len, b * kGroup, present, s, w);
+    uint8_t *blk = codes + ((int64_t)(v >> 5) * kblocks + g * gk + b) * 1024;
+    const int c = v & 31;
+    *reinterpret_cast<u32x4 *>(blk + c * 16) = u32x4{w[0], w[1], w[2], w[3]};
+    *reinterpret_cast<u32x4 *>(blk + (32 + c) * 16) = u32x4{w[4], w[5], w[6], w[7]};
+  }
   scales[(int64_t)g * nvec_pad + v] = s16;
 }
 
-// L2 [r][n]: column n along the rank axis, one 64-rank block per thread.
+// L2 [r][n]: column n along the rank axis, one 64-rank block per thread.  A
+// rank group is gr <= 64 ranks inside the block, or (gr = 128) two blocks,
+// whose threads each compute the group's scale and code their own half.
 __global__ __launch_bounds__(256) void pack_l2_kernel(const uint16_t *__restrict__ l2, int n,
                                                       int n_pad, int r, int gr, int rblocks,
                                                       uint8_t *__restrict__ codes,
@@ -155,17 +174,26 @@ __global__ __launch_bounds__(256) void pack_l2_kernel(const uint16_t *__restrict
   const int col = (int)(t / rblocks);
   const bool present = col < n;
   uint32_t w[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  // groups of gr ranks inside this 64-rank block (gr is 64 or r < 64)
   const int j0 = rb * 64;
-  const int jend = r < j0 + 64 ? r : j0 + 64;
-  for (int jg = j0; jg < jend; jg += gr) {
-    uint32_t part[8];
-    uint16_t s16;
+  if (gr > 64) {
+    const int jg = j0 / gr * gr;
     const uint16_t *p = present ? l2 + (int64_t)jg * n + col : l2;
-    quantize_group_strided(p, n, gr, present, part, s16);
-    const int w0 = (jg - j0) / 8;
-    for (int i = 0; i < gr / 8; i++) w[w0 + i] = part[i];
-    scales[(int64_t)(jg / gr) * n_pad + col] = s16;
+    uint16_t s16;
+    const float s = group_scale_strided(p, n, gr, present, s16);
+    codes_strided(p, n, gr, j0 - jg, present, s, w);
+    if (j0 == jg) scales[(int64_t)(jg / gr) * n_pad + col] = s16;
+  } else {
+    const int jend = r < j0 + 64 ? r : j0 + 64;
+    for (int jg = j0; jg < jend; jg += gr) {
+      uint32_t part[8];
+      uint16_t s16;
+      const uint16_t *p = present ? l2 + (int64_t)jg * n + col : l2;
+      const float s = group_scale_strided(p, n, gr, present, s16);
+      codes_strided(p, n, gr, 0, present, s, part);
+      const int w0 = (jg - j0) / 8;
+      for (int i = 0; i < gr / 8; i++) w[w0 + i] = part[i];
+      scales[(int64_t)(jg / gr) * n_pad + col] = s16;
+    }
   }
   uint8_t *blk = codes + ((int64_t)(col >> 5) * rblocks + rb) * 1024;
   const int c = col & 31;
@@ -183,23 +211,23 @@ __global__ __launch_bounds__(256) void zero16_kernel(uint8_t *__restrict__ p, in
 
 hipError_t launch_pack(const Geometry &g, const uint16_t *w, const uint16_t *l1,
                        const uint16_t *l2, uint8_t *packed, hipStream_t s) {
-  const int kg = g.k / kGroup;
-  hipLaunchKernelGGL(pack_kgroups_kernel, dim3(nblocks((int64_t)g.n_pad * kg)), dim3(256), 0, s,
-                     w, (int64_t)g.k, (int64_t)1, g.n, g.n_pad, kg, packed + g.off_w,
+  const int kg = g.k / kGroup, kq = kg / g.gk;   // 64-wide blocks, quantization groups
+  hipLaunchKernelGGL(pack_kgroups_kernel, dim3(nblocks((int64_t)g.n_pad * kq)), dim3(256), 0, s,
+                     w, (int64_t)g.k, (int64_t)1, g.n, g.n_pad, kg, g.gk, packed + g.off_w,
                      reinterpret_cast<uint16_t *>(packed + g.off_ws));
-  // the slack read past the last K-group: 1 KiB of codes, one scale row
+  // the slack read past the last K block: 1 KiB of codes, one scale row
   hipLaunchKernelGGL(zero16_kernel, dim3(1), dim3(256), 0, s,
                      packed + g.off_w + (uint64_t)g.n_pad / 32 * kg * 1024, (int64_t)64);
   hipLaunchKernelGGL(zero16_kernel, dim3(nblocks(g.n_pad / 8)), dim3(256), 0, s,
-                     packed + g.off_ws + (uint64_t)kg * g.n_pad * 2, (int64_t)g.n_pad / 8);
+                     packed + g.off_ws + (uint64_t)kq * g.n_pad * 2, (int64_t)g.n_pad / 8);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || g.r == 0) return e;
   hipLaunchKernelGGL(zero16_kernel, dim3(1), dim3(256), 0, s,
                      packed + g.off_l1 + (uint64_t)g.r_pad32 / 32 * kg * 1024, (int64_t)64);
   hipLaunchKernelGGL(zero16_kernel, dim3(1), dim3(256), 0, s,
-                     packed + g.off_l1s + (uint64_t)kg * g.r_pad32 * 2, (int64_t)g.r_pad32 / 8);
-  hipLaunchKernelGGL(pack_kgroups_kernel, dim3(nblocks((int64_t)g.r_pad32 * kg)), dim3(256), 0,
-                     s, l1, (int64_t)1, (int64_t)g.r, g.r, g.r_pad32, kg, packed + g.off_l1,
+                     packed + g.off_l1s + (uint64_t)kq * g.r_pad32 * 2, (int64_t)g.r_pad32 / 8);
+  hipLaunchKernelGGL(pack_kgroups_kernel, dim3(nblocks((int64_t)g.r_pad32 * kq)), dim3(256), 0,
+                     s, l1, (int64_t)1, (int64_t)g.r, g.r, g.r_pad32, kg, g.gk, packed + g.off_l1,
                      reinterpret_cast<uint16_t *>(packed + g.off_l1s));
   e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -215,21 +243,22 @@ hipError_t launch_pack(const Geometry &g, const uint16_t *w, const uint16_t *l1,
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void export_kgroups_kernel(const uint8_t *__restrict__ codes,
                                                              const uint16_t *__restrict__ scales,
-                                                             int nvec, int nvec_pad, int kgroups,
-                                                             uint32_t *__restrict__ out_c,
+                                                             int nvec, int nvec_pad, int kblocks,
+                                                             int gk, uint32_t *__restrict__ out_c,
                                                              uint16_t *__restrict__ out_s) {
   const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (t >= (int64_t)nvec * kgroups) return;
-  const int g = (int)(t % kgroups);
-  const int v = (int)(t / kgroups);
-  const uint8_t *blk = codes + ((int64_t)(v >> 5) * kgroups + g) * 1024;
+  if (t >= (int64_t)nvec * kblocks) return;
+  const int g = (int)(t % kblocks);
+  const int v = (int)(t / kblocks);
+  const uint8_t *blk = codes + ((int64_t)(v >> 5) * kblocks + g) * 1024;
   const int c = v & 31;
   const u32x4 a = *reinterpret_cast<const u32x4 *>(blk + c * 16);
   const u32x4 b = *reinterpret_cast<const u32x4 *>(blk + (32 + c) * 16);
-  uint32_t *o = out_c + (int64_t)v * kgroups * 8 + g * 8;
+  uint32_t *o = out_c + (int64_t)v * kblocks * 8 + g * 8;
   o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w;
   o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
-  out_s[(int64_t)v * kgroups + g] = scales[(int64_t)g * nvec_pad + v];
+  const int kq = kblocks / gk;
+  if (g % gk == 0) out_s[(int64_t)v * kq + g / gk] = scales[(int64_t)(g / gk) * nvec_pad + v];
 }
 
 __global__ __launch_bounds__(256) void export_l2_kernel(const uint8_t *__restrict__ codes,
@@ -261,12 +290,12 @@ hipError_t launch_export(const Geometry &g, const uint8_t *packed, uint32_t *wc,
   const int kg = g.k / kGroup;
   hipLaunchKernelGGL(export_kgroups_kernel, dim3(nblocks((int64_t)g.n * kg)), dim3(256), 0, s,
                      packed + g.off_w, reinterpret_cast<const uint16_t *>(packed + g.off_ws), g.n,
-                     g.n_pad, kg, wc, ws);
+                     g.n_pad, kg, g.gk, wc, ws);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || g.r == 0) return e;
   hipLaunchKernelGGL(export_kgroups_kernel, dim3(nblocks((int64_t)g.r * kg)), dim3(256), 0, s,
                      packed + g.off_l1, reinterpret_cast<const uint16_t *>(packed + g.off_l1s),
-                     g.r, g.r_pad32, kg, l1c, l1s);
+                     g.r, g.r_pad32, kg, g.gk, l1c, l1s);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int rblocks = g.r_pad64 / 64;

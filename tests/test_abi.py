@@ -40,7 +40,8 @@ def test_status_strings(L):
 
 @pytest.mark.parametrize("n,k,r,g,code", [
     (512, 512, 16, 64, 0), (4096, 4096, 64, 64, 0), (100, 64, 0, 64, 0), (1, 64, 128, 64, 0),
-    (512, 512, 16, 128, 3), (512, 500, 16, 64, 3), (0, 512, 16, 64, 2), (512, 0, 16, 64, 2),
+    (512, 512, 16, 128, 0), (512, 576, 16, 128, 3), (512, 512, 16, 32, 3), (512, 512, 16, 256, 3),
+    (512, 500, 16, 64, 3), (0, 512, 16, 64, 2), (512, 0, 16, 64, 2),
     (512, 512, 24, 64, 4), (512, 512, 256, 64, 4), (512, 512, -8, 64, 4),
 ])
 def test_desc_init_validation(L, n, k, r, g, code):
@@ -66,6 +67,12 @@ def test_desc_sizes(L):
     assert offs == sorted(offs) and all(o % 256 == 0 for o in offs)
     d2 = tq.weight_desc_init(100, 128, 16)
     assert d2.n_pad == 128 and d2.r_pad32 == 32 and d2.r_pad64 == 64 and d2.group_r == 16
+    # 128-wide groups: codes in the same 64-wide blocks, one scale row per 128
+    d3 = tq.weight_desc_init(4096, 4096, 128, 128)
+    assert d3.group == 128 and d3.group_r == 128
+    expect3 = (up(4096 * 4096 // 2 + 1024) + up(2 * 4096 * 33) + up(4096 * 128 // 2 + 1024) + up(2 * 128 * 33)
+               + up(4096 * 128 // 2) + up(2 * 4096))
+    assert d3.packed_bytes == expect3
 
 
 FAKE = 1 << 20     # 16-byte aligned fake device address; never dereferenced

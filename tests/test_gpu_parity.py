@@ -49,17 +49,18 @@ def dev(a):
     return torch.from_numpy(np.ascontiguousarray(a)).cuda()
 
 
-def run_gpu(X, W, L1, L2, bf16=False, debug=True, kernel=None, mid_tiles=0, fused_quant=False):
+def run_gpu(X, W, L1, L2, bf16=False, debug=True, kernel=None, mid_tiles=0, fused_quant=False,
+            group=GROUP):
     """One layer call through the C ABI (the kernel forced when given) plus
     the canonical export of the packed weights; returns host copies."""
     M, K = X.shape
     N = W.shape[0]
     r = 0 if L1 is None else L1.shape[1]
-    lay = tq.Layer(dev(W), None if L1 is None else dev(L1), None if L2 is None else dev(L2))
+    lay = tq.Layer(dev(W), None if L1 is None else dev(L1), None if L2 is None else dev(L2), group=group)
     d = lay.desc
     xd = dev(X)
-    xc, xs = tq.empty_act(M, K)
-    tq.quant_act(xd, xc, xs)
+    xc, xs = tq.empty_act(M, K, group=group)
+    tq.quant_act(xd, xc, xs, group)
     y = torch.empty((M, N), dtype=torch.bfloat16 if bf16 else torch.float16, device="cuda")
     out = {"kernel": kernel or tq.dual_gemm_kernel(d, M)}
     dbg = {}
@@ -73,11 +74,11 @@ def run_gpu(X, W, L1, L2, bf16=False, debug=True, kernel=None, mid_tiles=0, fuse
         tq.dual_gemm_debug(d, lay.packed, xc, xs, M, y, bf16=bf16, kernel=kernel,
                            mid_tiles=mid_tiles, **dbg)
     wc = torch.empty((N, K // 8), dtype=torch.int32, device="cuda")
-    ws = torch.empty((N, K // GROUP), dtype=torch.float16, device="cuda")
+    ws = torch.empty((N, K // group), dtype=torch.float16, device="cuda")
     ex = [wc, ws]
     if r:
         l1c = torch.empty((r, K // 8), dtype=torch.int32, device="cuda")
-        l1s = torch.empty((r, K // GROUP), dtype=torch.float16, device="cuda")
+        l1s = torch.empty((r, K // group), dtype=torch.float16, device="cuda")
         l2c = torch.empty((N, r // 8), dtype=torch.int32, device="cuda")
         l2s = torch.empty((N, r // d.group_r), dtype=torch.float16, device="cuda")
         ex += [l1c, l1s, l2c, l2s]
@@ -128,21 +129,22 @@ def check_tolerance(Y, ref64, bf16=False, wide_range=True):
 
 
 def full_parity(oracle_mod, X, W, L1, L2, bf16=False, wide_range=True, kernel=None, mid_tiles=0,
-                fused_quant=False):
-    g = run_gpu(X, W, L1, L2, bf16, kernel=kernel, mid_tiles=mid_tiles, fused_quant=fused_quant)
-    o = oracle_mod.layer(X, W, L1, L2, GROUP)
-    qx, sx = oracle_mod.quantize(X, GROUP)
+                fused_quant=False, group=GROUP):
+    g = run_gpu(X, W, L1, L2, bf16, kernel=kernel, mid_tiles=mid_tiles, fused_quant=fused_quant,
+                group=group)
+    o = oracle_mod.layer(X, W, L1, L2, group)
+    qx, sx = oracle_mod.quantize(X, group)
     np.testing.assert_array_equal(g["xq"], qx)
     np.testing.assert_array_equal(g["xs"].view(np.uint16), sx.view(np.uint16))
-    qw, sw = oracle_mod.quantize(W, GROUP)
+    qw, sw = oracle_mod.quantize(W, group)
     np.testing.assert_array_equal(g["wq"], qw)
     np.testing.assert_array_equal(g["ws"].view(np.uint16), sw.view(np.uint16))
     if L1 is not None:
         r = L1.shape[1]
-        q1, s1 = oracle_mod.quantize(L1, GROUP, axis=0)
+        q1, s1 = oracle_mod.quantize(L1, group, axis=0)
         np.testing.assert_array_equal(g["l1q"], q1)
         np.testing.assert_array_equal(g["l1s"].view(np.uint16), s1.view(np.uint16))
-        q2, s2 = oracle_mod.quantize(L2, min(GROUP, r), axis=0)
+        q2, s2 = oracle_mod.quantize(L2, min(group, r), axis=0)
         np.testing.assert_array_equal(g["l2q"], q2)
         np.testing.assert_array_equal(g["l2s"].view(np.uint16), s2.view(np.uint16))
         np.testing.assert_array_equal(g["H"].view(np.uint32), o["H"].view(np.uint32))
@@ -535,6 +537,45 @@ def test_prepared_layer(oracle_mod, M):
         best, errs = prep.search_alpha(X, weight, r, alphas=(0.3, 0.5, 0.7))
         assert best in errs and all(np.isfinite(v) for v in errs.values())
         assert errs[best] == min(errs.values())
+
+
+# ---------------------------------------------------------------- 128-wide groups
+# The paper's default group (Sec. 5.1): one scale per 128 values along K (and
+# along r for r = 128); the codes keep the 64-wide blocks.  The oracle takes
+# the group as a parameter.
+G128_CASES = [(1, 4096, 256, 128), (16, 4096, 256, 128), (3, 1024, 96, 64), (8, 512, 64, 16),
+              (1, 384, 32, 8), (12, 2048, 160, 128), (2, 128, 48, 32)]
+
+
+@pytest.mark.parametrize("M,K,N,r", G128_CASES)
+def test_group128_decode(oracle_mod, M, K, N, r):
+    say(f"group 128 decode M={M} K={K} N={N} r={r}")
+    d = random_codes_layer(M, K, N, r, seed=M + K + r)
+    full_parity(oracle_mod, d["X"], d["W_res"], d["L1"], d["L2"], group=128)
+
+
+@pytest.mark.parametrize("M", [1, 4, 16])
+def test_group128_fused_quant(oracle_mod, M):
+    say(f"group 128 fused quantization M={M}")
+    d = random_codes_layer(M, 1024, 128, 128, seed=11 + M)
+    full_parity(oracle_mod, d["X"], d["W_res"], d["L1"], d["L2"], fused_quant=True, group=128)
+
+
+@pytest.mark.parametrize("M,K,N,r,ct", [(17, 1024, 96, 128, 0), (100, 2048, 160, 64, 2), (33, 512, 64, 16, 1),
+                                        (600, 1024, 128, 128, 0), (300, 384, 64, 8, 4), (64, 768, 200, 32, 0)])
+def test_group128_mid(oracle_mod, M, K, N, r, ct):
+    say(f"group 128 mid M={M} K={K} N={N} r={r} ct={ct}")
+    d = random_codes_layer(M, K, N, r, seed=3 * M + r)
+    full_parity(oracle_mod, d["X"], d["W_res"], d["L1"], d["L2"], kernel="mid", mid_tiles=ct, group=128)
+
+
+def test_group128_qo_shape(oracle_mod):
+    """The paper's default configuration (G = 128, r = 128) on the LLaMA3-8B
+    q_proj shape, synthetic workload weights, single-token decode."""
+    say("group 128 r 128 q_proj M=1")
+    d = layer_inputs("llama3-8b-qo", 0, 1, rank=128)
+    full_parity(oracle_mod, d["X"], d["W_res"], d["L1"], d["L2"], group=128)
+
 
 
 @pytest.mark.parametrize("M,K,N,r", [(1, 256, 96, 64), (16, 320, 4096, 128), (100, 192, 520, 16),
