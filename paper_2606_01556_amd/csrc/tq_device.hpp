@@ -100,6 +100,10 @@ __device__ __forceinline__ v16f mfma_codes_32x32x64(v8i a, v8i b) {
   const v16f z = {0};
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, z, 0, 0, 0, kScale2p9, 0, kScale2p9);
 }
+// the same added to c (exact while the sums stay integers below 2^24)
+__device__ __forceinline__ v16f mfma_codes_32x32x64_acc(v8i a, v8i b, v16f c) {
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, kScale2p9, 0, kScale2p9);
+}
 
 // Same for 16x16 tiles over 128 k: operand lane l holds row/column l % 16,
 // k in [32 * (l / 16), +32); result lane l: column l % 16, rows 4 * (l / 16) + v.

@@ -17,14 +17,14 @@ int choose_kernel(const GemmArgs &a) {
   // the activation code format follows the same token-count split
   if (a.m <= kDecodeMaxTokens && decode_fits(a.m, a.geo.k)) return kKernelDecode;
   if (!act_codes_fp8(a.m)) return kKernelMid;
-  if (a.geo.gk != 1) return kKernelMid;   // 128-wide groups: built in the mid kernel so far
   // 128 x 256 blocks: the large kernel (16 wavefronts, H formed in the main
   // loop of every block) is faster while its blocks fit in one round over the
   // 256 CUs, and for ranks up to 64 at any size (its H share is then at most a
   // quarter of a block's work); beyond, the prefill kernel forms H once per
   // run of column blocks
   const int blocks = (a.m + 127) / 128 * ((a.geo.n_pad + 255) / 256);
-  const bool large = blocks <= 256 || a.geo.r_pad32 <= 64;
+  // (the prefill kernel takes 64-wide groups only)
+  const bool large = blocks <= 256 || a.geo.r_pad32 <= 64 || a.geo.gk != 1;
   // Few large blocks leave most CUs idle (a round of them costs about as much
   // as kLargeRound tile-group units of the mid kernel, whose 32-token blocks
   // fill the CUs at these sizes too): take the cheaper of the two.
@@ -36,7 +36,7 @@ int choose_kernel(const GemmArgs &a) {
 
 bool serves_group(int kernel, int gk) {
   if (gk == 1) return true;
-  return gk == 2 && (kernel == kKernelDecode || kernel == kKernelMid);
+  return gk == 2 && kernel != kKernelPrefill;
 }
 
 hipError_t launch_dual_gemm(const GemmArgs &a, hipStream_t s) {

@@ -130,14 +130,21 @@ __device__ __forceinline__ v16f l_codes_half(v8i a, v8i b) {
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, z, 0, 0, 0, kScale2p9 - 1, 0,
                                                          kScale2p9);
 }
+// the same added to c (the second block of a 128-wide group: exact)
+__device__ __forceinline__ v16f l_codes_half_acc(v8i a, v8i b, v16f c) {
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, kScale2p9 - 1, 0,
+                                                         kScale2p9);
+}
 
-// A wave load of one K-group: lane reads 16 bytes at base + off + g * stride
-// (base wave-uniform, off and stride per lane) into LDS at slot + dst + 16 *
-// lane.
+// A wave load of one 64-wide K block g: lane reads 16 bytes at base + off +
+// (g >> shift) * stride (base wave-uniform, off and stride per lane) into LDS
+// at slot + dst + 16 * lane.  Scale rows are per quantization group, so scale
+// items shift by log2(group / 64); each slot holds its block's group scales.
 struct LItem {
   const uint8_t *base;
   uint32_t off, stride;
   uint32_t dst;          // offset within a slot
+  int shift;
 };
 
 template <int RT>
@@ -146,6 +153,7 @@ __device__ __forceinline__ LItem l_item(const GemmArgs &a, int it, int lane, int
   const Geometry &geo = a.geo;
   const int KG = geo.k / kGroup;
   LItem d;
+  d.shift = it < 16 + RT ? 0 : geo.gk - 1;
   if (it < 8) {                       // activation tile it / 2, half it % 2 (fp8 bytes)
     const int t = min(m0 / 32 + it / 2, a.ms / 32 - 1);
     d.base = reinterpret_cast<const uint8_t *>(a.xc) + (int64_t)t * KG * 2048 + (it & 1) * 1024;
@@ -185,7 +193,9 @@ __device__ __forceinline__ LItem l_item(const GemmArgs &a, int it, int lane, int
   return d;
 }
 
-template <int RT>
+// GK: 64-wide K blocks per quantization group (1 or 2, the descriptor's
+// group / 64), a template parameter so that each variant keeps its registers
+template <int RT, int GK>
 __global__ __launch_bounds__(64 * LW, 1) void dual_gemm_large_kernel(GemmArgs a, int m_tiles,
                                                                      int n_tiles, int band) {
   using C = LCfg<RT>;
@@ -236,7 +246,8 @@ __global__ __launch_bounds__(64 * LW, 1) void dual_gemm_large_kernel(GemmArgs a,
         const int q = lane < 8 * C::RB * 4 ? lane : 0;   // 4 pieces per (rank group, tile)
         const int h = q / 32, j = (q / 4) % 8, part = q % 4;
         const int col = min(n0 + 32 * j + 8 * part, geo.n_pad - 8);
-        ldma(a.packed + geo.off_l2s + ((int64_t)h * geo.n_pad + col) * 2,
+        const int hg = h * 64 / geo.gr;   // rank group of 64-rank block h (gr >= 64 here)
+        ldma(a.packed + geo.off_l2s + ((int64_t)hg * geo.n_pad + col) * 2,
              lds0 + C::OFF_L2 + 8 * C::RB * 1024);
       }
     }
@@ -261,10 +272,10 @@ __global__ __launch_bounds__(64 * LW, 1) void dual_gemm_large_kernel(GemmArgs a,
     constexpr bool HW = decltype(HC)::value;   // this wavefront forms an H tile
     auto issue = [&](int g) {
       const uint32_t slot = lds0 + (g % D) * C::SLOT;
-      ldma_s(it0.off + (uint32_t)g * it0.stride, l_uniform(it0.base), slot + it0.dst);
+      ldma_s(it0.off + (uint32_t)(GK == 1 ? g : g >> it0.shift) * it0.stride, l_uniform(it0.base), slot + it0.dst);
       if constexpr (PER == 2) {
         const LItem it1 = l_item<RT>(a, wave + LW, lane, m0, n0);
-        ldma_s(it1.off + (uint32_t)g * it1.stride, l_uniform(it1.base), slot + it1.dst);
+        ldma_s(it1.off + (uint32_t)(GK == 1 ? g : g >> it1.shift) * it1.stride, l_uniform(it1.base), slot + it1.dst);
       }
     };
     auto group = [&](int g) {
@@ -296,6 +307,32 @@ __global__ __launch_bounds__(64 * LW, 1) void dual_gemm_large_kernel(GemmArgs a,
         for (int v = 0; v < 16; v++) hacc[v] = fmaf(c[v], p[v], hacc[v]);
       }
     };
+    // a 128-wide group (blocks g and g + 1): each tile's two half sums add
+    // exactly in the matrix core, then one fma per element (the oracle's step)
+    auto group2 = [&](int g) {
+      const uint8_t *S0 = smem + (g % D) * C::SLOT;
+      const uint8_t *S1 = smem + ((g + 1) % D) * C::SLOT;
+      const uint32_t sb = *reinterpret_cast<const uint16_t *>(S0 + C::S_SW + (32 * cc + l32) * 2);
+      const v8i b0 = unpack32(*reinterpret_cast<const u32x4 *>(S0 + C::S_B + cc * 1024 + lane * 16));
+      const v8i b1 = unpack32(*reinterpret_cast<const u32x4 *>(S1 + C::S_B + cc * 1024 + lane * 16));
+      // one tile at a time, each finished before the next starts (registers)
+      auto tile = [&](int t, const v8i &w0, const v8i &w1, uint32_t sw, v16f &acc) {
+        const uint32_t sx = *reinterpret_cast<const uint16_t *>(S0 + C::S_SX + (32 * t + l32) * 2);
+        const v16f c = l_codes_half_acc(l_v8h(S1 + C::S_A + t * 2048 + lane * 16), w1,
+                                        l_codes_half(l_v8h(S0 + C::S_A + t * 2048 + lane * 16), w0));
+        const v16f p = l_outer2(sx, sw);
+#pragma unroll
+        for (int v = 0; v < 16; v++) acc[v] = fmaf(c[v], p[v], acc[v]);
+      };
+      tile(tA, b0, b1, sb, acc0);
+      tile(tB, b0, b1, sb, acc1);
+      if constexpr (HW) {
+        const v8i l0 = unpack32(*reinterpret_cast<const u32x4 *>(S0 + C::S_L + hrt * 1024 + lane * 16));
+        const v8i l1 = unpack32(*reinterpret_cast<const u32x4 *>(S1 + C::S_L + hrt * 1024 + lane * 16));
+        const uint32_t sl = *reinterpret_cast<const uint16_t *>(S0 + C::S_SW + 512 + (32 * hrt + l32) * 2);
+        tile(tA, l0, l1, sl, hacc);
+      }
+    };
     lwait_vm<0>();
     stage2_loads();
     for (int s = 0; s < D - 2; s++)
@@ -308,8 +345,12 @@ __global__ __launch_bounds__(64 * LW, 1) void dual_gemm_large_kernel(GemmArgs a,
       __syncthreads();   // groups g2, g2 + 1 are visible; g2 - 2, g2 - 1 are consumed everywhere
       if (g2 + D - 2 < KG) issue(g2 + D - 2);   // into group g2 - 2's slot
       if (g2 + D - 1 < KG) issue(g2 + D - 1);   // into group g2 - 1's slot
-      group(g2);
-      if (g2 + 1 < KG) group(g2 + 1);
+      if constexpr (GK == 2) {
+        group2(g2);   // K is a multiple of 128 here
+      } else {
+        group(g2);
+        if (g2 + 1 < KG) group(g2 + 1);
+      }
     }
   };
   if constexpr (RT == 0) {
@@ -395,16 +436,25 @@ __global__ __launch_bounds__(64 * LW, 1) void dual_gemm_large_kernel(GemmArgs a,
     v16f ylr = v16f{0};
     if constexpr (RT > 0) {
       const uint8_t *L2S = smem + C::OFF_L2;
+      // one fma per rank group (the oracle's step): a 128-rank group (r = 128
+      // in 128-wide groups) first adds its two 64-rank blocks' exact integer
+      // sums in the matrix core
+      constexpr int bpg = RT == 4 && GK == 2 ? 2 : 1;   // 64-rank blocks per rank group
 #pragma unroll
-      for (int rb = 0; rb < C::RB; rb++) {
-        const v8i qa = l_v8i(QS + (32 * ti + l32) * C::QSTR + rb * 64 + (lane >> 5) * 32);
-        const v8i lb = unpack32(*reinterpret_cast<const u32x4 *>(L2S + (jt * C::RB + rb) * 1024 + lane * 16));
+      for (int hg = 0; hg < C::RB / bpg; hg++) {
+        v16f cbv = v16f{0};
+#pragma unroll
+        for (int q = 0; q < bpg; q++) {
+          const int rb = hg * bpg + q;
+          const v8i qa = l_v8i(QS + (32 * ti + l32) * C::QSTR + rb * 64 + (lane >> 5) * 32);
+          const v8i lb = unpack32(*reinterpret_cast<const u32x4 *>(L2S + (jt * C::RB + rb) * 1024 + lane * 16));
+          cbv = q == 0 ? mfma_codes_32x32x64(qa, lb) : mfma_codes_32x32x64_acc(qa, lb, cbv);
+        }
         const float sl2 = half_bits_to_float(*reinterpret_cast<const uint16_t *>(
-            L2S + 8 * C::RB * 1024 + ((rb * 8 + jt) * 32 + l32) * 2));
-        const v16f cbv = mfma_codes_32x32x64(qa, lb);
+            L2S + 8 * C::RB * 1024 + ((hg * bpg * 8 + jt) * 32 + l32) * 2));
 #pragma unroll
         for (int v = 0; v < 16; v++)
-          ylr[v] = fmaf(cbv[v], SHS[rb * LBM + 32 * ti + row_of_32x32(lane, v)] * sl2, ylr[v]);
+          ylr[v] = fmaf(cbv[v], SHS[hg * LBM + 32 * ti + row_of_32x32(lane, v)] * sl2, ylr[v]);
       }
     }
     // the matrix-core products above read operands from every lane: keep
@@ -426,13 +476,13 @@ __global__ __launch_bounds__(64 * LW, 1) void dual_gemm_large_kernel(GemmArgs a,
   }
 }
 
-template <int RT>
+template <int RT, int GK>
 hipError_t launch_large(const GemmArgs &a, hipStream_t s) {
   using C = LCfg<RT>;
   const int m_tiles = (a.m + LBM - 1) / LBM;
   const int n_tiles = (a.geo.n_pad + LBN - 1) / LBN;
   const int band = m_tiles < 8 ? m_tiles : 8;   // token blocks per band of the XCD order
-  auto kern = dual_gemm_large_kernel<RT>;
+  auto kern = dual_gemm_large_kernel<RT, GK>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
   if (e != hipSuccess) return e;
@@ -441,16 +491,21 @@ hipError_t launch_large(const GemmArgs &a, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <int GK>
+hipError_t launch_large_rt(const GemmArgs &a, hipStream_t s) {
+  switch (a.geo.r_pad32 / 32) {
+    case 0: return launch_large<0, GK>(a, s);
+    case 1: return launch_large<1, GK>(a, s);
+    case 2: return launch_large<2, GK>(a, s);
+    case 4: return launch_large<4, GK>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 }  // namespace
 
 hipError_t launch_dual_gemm_large(const GemmArgs &a, hipStream_t s) {
-  switch (a.geo.r_pad32 / 32) {
-    case 0: return launch_large<0>(a, s);
-    case 1: return launch_large<1>(a, s);
-    case 2: return launch_large<2>(a, s);
-    case 4: return launch_large<4>(a, s);
-    default: return hipErrorInvalidValue;
-  }
+  return a.geo.gk == 2 ? launch_large_rt<2>(a, s) : launch_large_rt<1>(a, s);
 }
 
 }  // namespace tq
