@@ -265,18 +265,20 @@ class LayerBench:
     """One layer's packed weights (rotated copies), and per token count the
     fp16 activations, activation codes and outputs (rotated copies)."""
 
-    def __init__(self, wl, layer, ms, stream, with_fp16=True):
+    def __init__(self, wl, layer, ms, stream, with_fp16=True, group=GROUP, rank=None):
         import torch
         import paper_2606_01556_amd as tq
         from tq_synth import weights, activations
         dev = torch.device("cuda")
         self.layer = layer
-        self.K, self.N, self.r = layer.K, layer.N, layer.r
-        w = weights(wl, layer)
+        self.group = group
+        self.K, self.N = layer.K, layer.N
+        self.r = layer.r if rank is None else rank
+        w = weights(wl, layer, rank=self.r)
         with torch.cuda.stream(stream):
             W = torch.from_numpy(w["W_res"]).to(dev)
             lay = tq.Layer(W, torch.from_numpy(w["L1"]).to(dev), torch.from_numpy(w["L2"]).to(dev),
-                           stream=stream)
+                           group=group, stream=stream)
             self.desc = lay.desc
             self.ncopy = max(2, int(np.ceil(ROTATE_BYTES / self.desc.packed_bytes)))
             self.packed = [lay.packed] + [lay.packed.clone() for _ in range(self.ncopy - 1)]
@@ -292,7 +294,7 @@ class LayerBench:
                 per = 2 * m * (self.K + self.N) + tq.act_codes_bytes(m, self.K)
                 nx = max(2, min(self.ncopy, int(np.ceil(ROTATE_BYTES / per))))
                 self.X[m] = [x] + [x.clone() for _ in range(nx - 1)]
-                self.act[m] = [tq.empty_act(m, self.K) for _ in range(nx)]
+                self.act[m] = [tq.empty_act(m, self.K, group=group) for _ in range(nx)]
                 self.Y[m] = [torch.empty((m, self.N), dtype=torch.float16, device=dev) for _ in range(nx)]
         self.i = 0
 
@@ -315,7 +317,7 @@ class LayerBench:
                 ev[0].record()
             tq.dual_gemm_fused_quant(self.desc, p, x, y, stream=s)
         else:
-            tq.quant_act(x, xc, xs, stream=s)
+            tq.quant_act(x, xc, xs, self.group, stream=s)
             if ev is not None:
                 ev[0].record()
             tq.dual_gemm(self.desc, p, xc, xs, m, y, stream=s)
@@ -360,7 +362,7 @@ def detail_rows(L, ms, stream, wl_name):
         def quant():
             i = nxt()
             xc, xs = L.act[m][i % len(L.act[m])]
-            tq.quant_act(L.X[m][i % len(L.X[m])], xc, xs, stream=s)
+            tq.quant_act(L.X[m][i % len(L.X[m])], xc, xs, L.group, stream=s)
 
         def f16():
             i = nxt()
@@ -371,7 +373,7 @@ def detail_rows(L, ms, stream, wl_name):
         def unf():
             i = nxt()
             xc, xs = L.act[m][i % len(L.act[m])]
-            tq.quant_act(L.X[m][i % len(L.X[m])], xc, xs, stream=s)
+            tq.quant_act(L.X[m][i % len(L.X[m])], xc, xs, L.group, stream=s)
             tq.dual_gemm_unfused(L.desc, L.packed[i % L.ncopy], xc, xs, m, L.Y[m][i % len(L.Y[m])],
                                  scratch, stream=s)
 
@@ -382,7 +384,7 @@ def detail_rows(L, ms, stream, wl_name):
         us_fp16 = timed(stream, f16, reps)
         us_unf = timed(stream, unf, reps)
         del scratch
-        row = {"workload": wl_name, "layer": L.layer.name, "K": L.K, "N": L.N, "r": L.r, "M": m,
+        row = {"workload": wl_name, "layer": L.layer.name, "K": L.K, "N": L.N, "r": L.r, "group": L.group, "M": m,
                "kernel": L.kernel(m), "us_layer": round(us_layer, 3),
                "layer_launches": 1 if m <= FUSED_QUANT_MAX_M else 2,
                "us_quant_act_plus_dual_gemm": round(us_two, 3),
@@ -521,6 +523,11 @@ def main_bench(args):
         wl2 = WORKLOADS[DETAIL_EXTRA]
         L2 = LayerBench(wl2, wl2.layers[0], wl2.Ms, stream)
         rows += detail_rows(L2, wl2.Ms, stream, DETAIL_EXTRA)
+        del L2
+        torch.cuda.empty_cache()
+        # the paper's default configuration (group 128, rank 128) on the same shape
+        L3 = LayerBench(wl2, wl2.layers[0], wl2.Ms, stream, group=128, rank=128)
+        rows += detail_rows(L3, wl2.Ms, stream, DETAIL_EXTRA + "-g128-r128")
         out["per_m"] = rows
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(step_flops)

@@ -12,7 +12,8 @@
  * L2 = V' [r,n] the low-rank factors.  Q is the symmetric 4-bit group
  * quantizer of Sec. 2 Eq. (1): codes q in [-7, 7], one fp16 scale
  * s = fp16(max|v| / 7) per group of `group` consecutive values along the
- * reduction axis (Sec. 5.1 uses groups of contiguous elements).  The low-rank
+ * reduction axis (Sec. 5.1 uses groups of contiguous elements; 64 or 128
+ * here, 128 being the paper's default).  The low-rank
  * branch is two integer products: H = Q(X) Q(L1) is formed on chip,
  * re-quantized per token and group of min(group, r) rank columns with an fp32
  * scale s_H, and multiplied by Q(L2); both branches are merged in one
@@ -83,9 +84,9 @@ typedef struct {
 
 /* Validate a layer shape and fill `out` (host only, touches no GPU).
  *   n >= 1 output features, k input features with k % group == 0,
- *   group == 64 (the only group size built), rank r in {0, 8, 16, 32, 64,
- *   128}.  r == 0 is the plain 4-bit linear layer of Sec. 2 Eq. (2).  The
- *   packed buffer must stay below 4 GiB (TQ_ERR_SHAPE otherwise).
+ *   group 64 or 128, rank r in {0, 8, 16, 32, 64, 128}.  r == 0 is the plain
+ *   4-bit linear layer of Sec. 2 Eq. (2).  The packed buffer must stay below
+ *   4 GiB (TQ_ERR_SHAPE otherwise).
  * Errors: TQ_ERR_NULL, TQ_ERR_SHAPE, TQ_ERR_GROUP, TQ_ERR_RANK. */
 tq_status tq_weight_desc_init(int n, int k, int rank, int group, tq_weight_desc *out);
 
@@ -104,10 +105,12 @@ tq_status tq_pack_weights(const tq_weight_desc *d, const void *w_res, const void
 /* Per-token, per-group activation quantizer (Sec. 2 Eq. 1; Sec. 4.3: the
  * activation is quantized once and shared by both branches).
  *   x         [m,k] fp16 row-major, 0 <= m <= 2097120 (65535 tiles of 32),
- *             k % group == 0, group == 64
+ *             k % group == 0, group 64 or 128 (the layer's group)
  *   x_codes   tq_act_codes_bytes(m, k) bytes, tile-major.  The tokens are
  *             cut into tiles of 32 (m32 = m rounded up to a multiple of 32)
- *             and K into groups of 64.  For m <= 512 each code is a TQ4
+ *             and K into blocks of 64 (called groups below; a 128-wide
+ *             quantization group spans two blocks and has one scale).  The
+ *             layout does not depend on the group.  For m <= 512 each code is a TQ4
  *             nibble (m32 * k / 2 bytes): tile t, group g is one 1 KiB block
  *             at byte (t * (k / 64) + g) * 1024, whose 16-byte lane slot
  *             32 h + i (h = 0, 1; i = 0 .. 31) holds the four TQ4 words of
@@ -185,7 +188,9 @@ int tq_dual_gemm_kernel(const tq_weight_desc *d, int m);
  *   kernel     -1: the kernel tq_dual_gemm would launch; otherwise the
  *              tq_kernel value to run (TQ_KERNEL_DECODE needs a decode-sized
  *              m that fits its LDS, TQ_KERNEL_LARGE / TQ_KERNEL_PREFILL need
- *              m > 512, TQ_KERNEL_MID serves any m; TQ_ERR_SHAPE otherwise)
+ *              m > 512, TQ_KERNEL_MID serves any m; TQ_ERR_SHAPE otherwise;
+ *              TQ_KERNEL_PREFILL takes 64-wide groups only, TQ_ERR_GROUP
+ *              otherwise -- tq_dual_gemm never picks it for 128-wide ones)
  *   mid_tiles  0: the mid kernel's own choice of 32-column tiles per
  *              work-group; 1, 2 or 4 forces it (TQ_ERR_SHAPE otherwise)
  *   h, sh, qh  all NULL, or all set (r > 0, else TQ_ERR_RANK) to copy the

@@ -60,11 +60,12 @@ __global__ __launch_bounds__(64 * kS1Waves) void unfused_stage1_kernel(GemmArgs 
   v8i av[kS1Gpw];
   u32x4 lraw[kS1Gpw];
   uint32_t sc[kS1Gpw];   // lanes 0-31: token scale, lanes 32-63: rank scale
+  const int gk = geo.gk;   // 64-wide blocks per quantization group: scale row g / gk
   auto load = [&](int i, int g) {
     av[i] = act_operand<FP8>(xc, KG, t, g, lane);
     lraw[i] = *reinterpret_cast<const u32x4 *>(l1 + (int64_t)g * 1024);
-    sc[i] = lane < 32 ? a.xs[(int64_t)g * a.ms + 32 * t + l32]
-                      : l1s[(int64_t)g * geo.r_pad32 + 32 * rt + l32];
+    sc[i] = lane < 32 ? a.xs[(int64_t)(g / gk) * a.ms + 32 * t + l32]
+                      : l1s[(int64_t)(g / gk) * geo.r_pad32 + 32 * rt + l32];
   };
 #pragma unroll
   for (int i = 0; i < kS1Gpw; i++)
@@ -87,10 +88,17 @@ __global__ __launch_bounds__(64 * kS1Waves) void unfused_stage1_kernel(GemmArgs 
     }
     __syncthreads();
     const int ng = min(kS1Chunk, KG - c0);
-    for (int gl = 0; gl < ng; gl++) {
+    // one step per quantization group: a 128-wide group adds its two blocks'
+    // exact integer sums first (chunks start on group boundaries)
+    for (int gl = 0; gl < ng; gl += gk) {
       const float sl = SL[gl * 32 + l32];
-      acc0 = fmaf(CS[(gl * 16 + v0) * 64 + lane], SX[gl * 32 + row0] * sl, acc0);
-      acc1 = fmaf(CS[(gl * 16 + v0 + 1) * 64 + lane], SX[gl * 32 + row1] * sl, acc1);
+      float c0v = CS[(gl * 16 + v0) * 64 + lane], c1v = CS[(gl * 16 + v0 + 1) * 64 + lane];
+      if (gk == 2) {
+        c0v += CS[((gl + 1) * 16 + v0) * 64 + lane];
+        c1v += CS[((gl + 1) * 16 + v0 + 1) * 64 + lane];
+      }
+      acc0 = fmaf(c0v, SX[gl * 32 + row0] * sl, acc0);
+      acc1 = fmaf(c1v, SX[gl * 32 + row1] * sl, acc1);
     }
     __syncthreads();
   }
@@ -100,13 +108,38 @@ __global__ __launch_bounds__(64 * kS1Waves) void unfused_stage1_kernel(GemmArgs 
 
 // Re-quantization: one lane per element of H; a wavefront covers 64 ranks of
 // one token (a rank group is gr <= 64 consecutive lanes: its max comes from a
-// butterfly over those lanes).
+// butterfly over those lanes).  A 128-rank group: one wavefront per token,
+// two ranks per lane (j and j + 64).
 __global__ __launch_bounds__(256) void unfused_requant_kernel(const float *__restrict__ h, int m,
                                                               int m32, int r, int gr, int r_pad32,
                                                               int r_pad64, uint8_t *__restrict__ qh,
                                                               float *__restrict__ sh) {
   const int lane = threadIdx.x & 63;
   const int64_t wv = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);   // (token, 64-rank block)
+  if (gr > 64) {
+    if (wv >= m32) return;
+    const int row = (int)wv;
+    float hv[2];
+    float amax = 0.0f;
+    for (int b = 0; b < 2; b++) {
+      const int j = 64 * b + lane;
+      hv[b] = row < m && j < r ? h[(int64_t)row * r_pad32 + j] : 0.0f;
+      amax = fmaxf(amax, fabsf(hv[b]));
+    }
+    for (int msk = 1; msk < 64; msk <<= 1) amax = fmaxf(amax, __shfl_xor(amax, msk));
+    const float s = amax / 7.0f;
+    for (int b = 0; b < 2; b++) {
+      int q = 0;
+      if (row < m && s != 0.0f) {
+        float tq = __builtin_rintf(hv[b] / s);
+        tq = tq > 7.0f ? 7.0f : (tq < -7.0f ? -7.0f : tq);
+        q = (int)tq;
+      }
+      qh[(int64_t)row * r_pad64 + 64 * b + lane] = (uint8_t)code_to_fp8(q);
+    }
+    if (lane == 0) sh[row] = row < m ? s : 0.0f;
+    return;
+  }
   const int RB = r_pad64 / 64;
   if (wv >= (int64_t)m32 * RB) return;
   const int row = (int)(wv / RB), j = (int)(wv % RB) * 64 + lane;
@@ -144,11 +177,12 @@ __global__ __launch_bounds__(256) void unfused_stage2_kernel(GemmArgs a, const u
     const v8i qa = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
     const v8i lb = unpack32(*reinterpret_cast<const u32x4 *>(
         a.packed + geo.off_l2 + (((int64_t)ct * RB + rb) * 64 + lane) * 16));
-    const float sl2 = half_bits_to_float(l2s[(int64_t)rb * geo.n_pad + ct * 32 + l32]);
+    const int hg = rb * 64 / geo.gr;   // rank group of this 64-rank block (gr >= 64 when RB > 1)
+    const float sl2 = half_bits_to_float(l2s[(int64_t)hg * geo.n_pad + ct * 32 + l32]);
     const v16f cbv = mfma_codes_32x32x64(qa, lb);
 #pragma unroll
     for (int v = 0; v < 16; v++)
-      ylr[v] = fmaf(cbv[v], sh[(int64_t)rb * a.ms + 32 * t + row_of_32x32(lane, v)] * sl2, ylr[v]);
+      ylr[v] = fmaf(cbv[v], sh[(int64_t)hg * a.ms + 32 * t + row_of_32x32(lane, v)] * sl2, ylr[v]);
   }
   asm volatile("" : "+v"(ylr));
   const int col = ct * 32 + l32;
@@ -203,7 +237,7 @@ hipError_t launch_dual_gemm_unfused(const GemmArgs &a, void *scratch, hipStream_
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(s1, dim3(tiles, g.r_pad32 / 32), dim3(64 * kS1Waves), kS1Lds, s, a, h);
   // 3. re-quantization: Q_H and s_H to global memory
-  const int64_t waves = (int64_t)m32 * (g.r_pad64 / 64);
+  const int64_t waves = (int64_t)m32 * (g.gr > 64 ? 1 : g.r_pad64 / 64);
   hipLaunchKernelGGL(unfused_requant_kernel, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s, h,
                      a.m, m32, g.r, g.gr, g.r_pad32, g.r_pad64, qh, sh);
   // 4. stage 2 added to the residual output

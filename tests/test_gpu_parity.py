@@ -609,25 +609,28 @@ def test_group128_qo_shape(oracle_mod):
 
 
 
-@pytest.mark.parametrize("M,K,N,r", [(1, 256, 96, 64), (16, 320, 4096, 128), (100, 192, 520, 16),
-                                     (600, 576, 1000, 64), (40, 128, 64, 0), (530, 256, 300, 8)])
-def test_unfused_baseline(oracle_mod, M, K, N, r):
+@pytest.mark.parametrize("M,K,N,r,group", [(1, 256, 96, 64, 64), (16, 320, 4096, 128, 64),
+                                           (100, 192, 520, 16, 64), (600, 576, 1000, 64, 64),
+                                           (40, 128, 64, 0, 64), (530, 256, 300, 8, 64),
+                                           (1, 512, 96, 128, 128), (100, 384, 200, 128, 128),
+                                           (600, 640, 300, 64, 128), (17, 256, 64, 16, 128)])
+def test_unfused_baseline(oracle_mod, M, K, N, r, group):
     """The layer without fusion: H, s_H and Q_H read back from its scratch
     are bit-identical to the oracle's, and Y is within the tolerance (its
     residual is rounded to fp16 once more than the fused layer's)."""
-    say(f"unfused M={M} K={K} N={N} r={r}")
+    say(f"unfused M={M} K={K} N={N} r={r} group={group}")
     d = random_codes_layer(M, K, N, r, seed=M + K + N + r + 11)
     X, W, L1, L2 = d["X"], d["W_res"], d["L1"], d["L2"]
-    lay = tq.Layer(dev(W), None if L1 is None else dev(L1), None if L2 is None else dev(L2))
-    xc, xs = tq.empty_act(M, K)
-    tq.quant_act(dev(X), xc, xs)
+    lay = tq.Layer(dev(W), None if L1 is None else dev(L1), None if L2 is None else dev(L2), group=group)
+    xc, xs = tq.empty_act(M, K, group=group)
+    tq.quant_act(dev(X), xc, xs, group)
     y = torch.empty((M, N), dtype=torch.float16, device="cuda")
     scratch = tq.empty_unfused_scratch(lay.desc, M)
     tq.dual_gemm_unfused(lay.desc, lay.packed, xc, xs, M, y, scratch)
     yf = torch.empty_like(y)
     tq.dual_gemm(lay.desc, lay.packed, xc, xs, M, yf)
     torch.cuda.synchronize()
-    o = oracle_mod.layer(X, W, L1, L2, GROUP)
+    o = oracle_mod.layer(X, W, L1, L2, group)
     if r:
         h, qh, sh = (t.cpu().numpy() for t in tq.unfused_parts(lay.desc, M, scratch))
         np.testing.assert_array_equal(h[:M, :r].view(np.uint32), o["H"].view(np.uint32))

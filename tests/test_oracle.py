@@ -202,13 +202,12 @@ def test_quantizer_axis0_groups(oracle_mod):
 
 
 # ---------------------------------------------------------------- designed layers
-def _designed_integer_layer(M, K, N, r, seed):
+def _designed_integer_layer(M, K, N, r, seed, G=GROUP):
     """fp16 inputs whose every group has max |value| = 7, so all stored scales
     are exactly 1 and the codes are the values themselves.  The low-rank part
     is built so that H = X L1 is integer with max |H| = 7 per r-group, so
     s_H = 1 and q_H = H (no rounding anywhere)."""
     g = np.random.default_rng(seed)
-    G = GROUP
     X = g.integers(-6, 7, size=(M, K)).astype(np.float64)
     W = g.integers(-7, 8, size=(N, K)).astype(np.float64)
     for kg in range(K // G):
@@ -237,10 +236,11 @@ def _designed_integer_layer(M, K, N, r, seed):
             dict(X=X, W_res=W, L1=L1 if r else None, L2=L2 if r else None).items() if a is not None}, X, W, L1, L2
 
 
-@pytest.mark.parametrize("M,K,N,r", [(5, 128, 48, 16), (3, 192, 64, 64), (4, 128, 32, 128), (2, 64, 16, 0)])
-def test_integer_designed_layer(oracle_mod, M, K, N, r):
-    d, X, W, L1, L2 = _designed_integer_layer(M, K, N, r, seed=M * 7 + r)
-    out = oracle_mod.layer(d["X"], d["W_res"], d.get("L1"), d.get("L2"), GROUP)
+@pytest.mark.parametrize("M,K,N,r,G", [(5, 128, 48, 16, 64), (3, 192, 64, 64, 64), (4, 128, 32, 128, 64),
+                                       (2, 64, 16, 0, 64), (3, 256, 40, 128, 128), (4, 384, 24, 32, 128)])
+def test_integer_designed_layer(oracle_mod, M, K, N, r, G):
+    d, X, W, L1, L2 = _designed_integer_layer(M, K, N, r, seed=M * 7 + r, G=G)
+    out = oracle_mod.layer(d["X"], d["W_res"], d.get("L1"), d.get("L2"), G)
     Xi, Wi = X.astype(np.int64), W.astype(np.int64)
     Y = Xi @ Wi.T
     if r:
@@ -306,13 +306,22 @@ def _brute_force(X, W, L1, L2, G):
     return res
 
 
-@pytest.mark.parametrize("M,K,N,r", [(4, 128, 24, 16), (3, 192, 16, 64), (2, 128, 8, 128), (3, 128, 16, 0)])
-def test_brute_force_fp64(oracle_mod, M, K, N, r):
-    d = random_codes_layer(M, K, N, r, seed=r + 1)
+@pytest.mark.parametrize("M,K,N,r,G", [(4, 128, 24, 16, 64), (3, 192, 16, 64, 64), (2, 128, 8, 128, 64),
+                                       (3, 128, 16, 0, 64), (4, 256, 24, 128, 128), (3, 384, 16, 64, 128),
+                                       (2, 128, 8, 16, 128), (3, 256, 16, 0, 128)])
+def test_brute_force_fp64(oracle_mod, M, K, N, r, G):
+    d = random_codes_layer(M, K, N, r, seed=r + 1 + G)
+    if G == 128:
+        # halves of very different size: a 128-wide group codes the smaller
+        # half with the larger half's scale, which 64-wide groups would not
+        d["X"][:, 64:128] = (d["X"][:, 64:128].astype(np.float32) * 40).astype(np.float16)
     bf = _brute_force(d["X"].astype(np.float64), d["W_res"].astype(np.float64),
                       None if d["L1"] is None else d["L1"].astype(np.float64),
-                      None if d["L2"] is None else d["L2"].astype(np.float64), GROUP)
-    out = oracle_mod.layer(d["X"], d["W_res"], d["L1"], d["L2"], GROUP)
+                      None if d["L2"] is None else d["L2"].astype(np.float64), G)
+    out = oracle_mod.layer(d["X"], d["W_res"], d["L1"], d["L2"], G)
+    if G == 128:
+        o64 = oracle_mod.layer(d["X"], d["W_res"], d["L1"], d["L2"], 64)
+        assert not np.array_equal(o64["Y32"], out["Y32"]), "the group width must matter here"
     if r:
         np.testing.assert_allclose(out["H"], bf["H"], rtol=1e-6, atol=1e-6 * np.abs(bf["H"]).max())
         near_tie = np.abs(np.abs(bf["t"] - np.floor(bf["t"])) - 0.5) < 1e-4
