@@ -246,7 +246,8 @@ tq_status tq_dual_gemm_unfused_noalloc(const tq_weight_desc *d, const void *pack
                                        const void *x_codes, const void *x_scales, int m, void *y,
                                        tq_dtype y_dtype, void *stream);
 
-/* Copy the packed weights out in the canonical layout (for tests/debug):
+/* Copy the packed weights out (for tests/debug), codes as TQ4 words (the
+ * packed layout's sign-magnitude encoding, 8 codes per word):
  *   w_codes  [n, k/8] TQ4 words      w_scales  [n, k/group] fp16
  *   l1_codes [r, k/8] TQ4 words (row j = column j of L1, along k)
  *   l1_scales[r, k/group] fp16
@@ -257,6 +258,25 @@ tq_status tq_dual_gemm_unfused_noalloc(const tq_weight_desc *d, const void *pack
 tq_status tq_export_weights(const tq_weight_desc *d, const void *packed, void *w_codes,
                             void *w_scales, void *l1_codes, void *l1_scales, void *l2_codes,
                             void *l2_scales, void *stream);
+
+/* The same in the canonical 4-bit layout: two's-complement nibbles (codes in
+ * [-7, 7]), element 2i in the low and 2i+1 in the high nibble of byte i,
+ * contiguous along the reduction axis; scales as fp16 bit patterns.
+ *   wq  [n, k/2]  bytes          ws  [n, k/group] fp16
+ *   l1q [r, k/2]  (row j = column j of L1)   l1s [k/group, r] fp16
+ *   l2q [n, r/2]  (row c = column c of L2)   l2s [r/group_r, n] fp16
+ * The l1/l2 pointers may be NULL iff r == 0.
+ * Errors: TQ_ERR_NULL, TQ_ERR_BUFFER, TQ_ERR_ALIGN, TQ_ERR_HIP. */
+tq_status tq_export_weights_canonical(const tq_weight_desc *d, const void *packed, void *wq, void *ws,
+                                      void *l1q, void *l1s, void *l2q, void *l2s, void *stream);
+
+/* Activation codes and scales written by tq_quant_act (m tokens, reduction
+ * size k, quantization group `group`) copied out in the canonical layout:
+ *   codes_out  [m, k/2] bytes, two's-complement nibbles as above
+ *   scales_out [m, k/group] fp16
+ * Errors: TQ_ERR_NULL, TQ_ERR_SHAPE, TQ_ERR_GROUP, TQ_ERR_ALIGN, TQ_ERR_HIP. */
+tq_status tq_act_codes_canonical(const void *x_codes, const void *x_scales, int m, int k, int group,
+                                 void *codes_out, void *scales_out, void *stream);
 
 /* Static description of a status code; never NULL. */
 const char *tq_status_string(tq_status s);

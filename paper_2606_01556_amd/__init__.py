@@ -42,7 +42,8 @@ class WeightDesc(ctypes.Structure):
 EXPORTS = ("tq_weight_desc_init", "tq_pack_weights", "tq_quant_act", "tq_dual_gemm",
            "tq_dual_gemm_fused_quant", "tq_dual_gemm_debug", "tq_export_weights",
            "tq_act_codes_bytes", "tq_unfused_scratch_bytes", "tq_dual_gemm_unfused",
-           "tq_dual_gemm_unfused_noalloc", "tq_dual_gemm_kernel", "tq_status_string")
+           "tq_dual_gemm_unfused_noalloc", "tq_dual_gemm_kernel", "tq_status_string",
+           "tq_export_weights_canonical", "tq_act_codes_canonical")
 
 _lib = None
 
@@ -72,6 +73,8 @@ def lib() -> ctypes.CDLL:
         L.tq_dual_gemm_unfused.argtypes = [D, P, P, P, I, P, I, P, P]
         L.tq_dual_gemm_unfused_noalloc.argtypes = [D, P, P, P, I, P, I, P]
         L.tq_export_weights.argtypes = [D, P, P, P, P, P, P, P, P]
+        L.tq_export_weights_canonical.argtypes = [D, P, P, P, P, P, P, P, P]
+        L.tq_act_codes_canonical.argtypes = [P, P, I, I, I, P, P, P]
         L.tq_status_string.argtypes = [I]
         L.tq_status_string.restype = ctypes.c_char_p
         for name in EXPORTS:
@@ -275,6 +278,50 @@ def export_weights(desc: WeightDesc, packed, w_codes, w_scales, l1_codes=None, l
     _check(lib().tq_export_weights(ctypes.byref(desc), _ptr(packed), _ptr(w_codes), _ptr(w_scales),
                                    _ptr(l1_codes), _ptr(l1_scales), _ptr(l2_codes), _ptr(l2_scales),
                                    _stream(stream)), "tq_export_weights")
+
+
+def export_weights_canonical(desc: WeightDesc, packed, stream=None):
+    """The packed weights in the canonical layout (tq_export_weights_canonical):
+    (wq [n, k/2] uint8, ws [n, k/group] fp16, l1q [r, k/2], l1s [k/group, r],
+    l2q [n, r/2], l2s [r/group_r, n]); the low-rank ones are None for r = 0."""
+    import torch
+    n, k, r, g, gr = desc.n, desc.k, desc.rank, desc.group, desc.group_r
+    dv = packed.device
+    wq = torch.empty((n, k // 2), dtype=torch.uint8, device=dv)
+    ws = torch.empty((n, k // g), dtype=torch.float16, device=dv)
+    l1q = l1s = l2q = l2s = None
+    if r:
+        l1q = torch.empty((r, k // 2), dtype=torch.uint8, device=dv)
+        l1s = torch.empty((k // g, r), dtype=torch.float16, device=dv)
+        l2q = torch.empty((n, r // 2), dtype=torch.uint8, device=dv)
+        l2s = torch.empty((r // gr, n), dtype=torch.float16, device=dv)
+    _check(lib().tq_export_weights_canonical(ctypes.byref(desc), _ptr(packed), _ptr(wq), _ptr(ws), _ptr(l1q),
+                                             _ptr(l1s), _ptr(l2q), _ptr(l2s), _stream(stream)),
+           "tq_export_weights_canonical")
+    return wq, ws, l1q, l1s, l2q, l2s
+
+
+def act_codes_canonical(x_codes, x_scales, m: int, k: int, group: int = GROUP, stream=None):
+    """Activation codes and scales of tq_quant_act in the canonical layout
+    (tq_act_codes_canonical): (codes [m, k/2] uint8, scales [m, k/group] fp16)."""
+    import torch
+    _tensor(x_codes, "x_codes", min_bytes=act_codes_bytes(m, k))
+    _tensor(x_scales, "x_scales", min_bytes=(k // group) * padded_tokens(m) * 2)
+    q = torch.empty((m, k // 2), dtype=torch.uint8, device=x_codes.device)
+    s = torch.empty((m, k // group), dtype=torch.float16, device=x_codes.device)
+    _check(lib().tq_act_codes_canonical(_ptr(x_codes), _ptr(x_scales), m, k, group, _ptr(q), _ptr(s),
+                                        _stream(stream)), "tq_act_codes_canonical")
+    return q, s
+
+
+def canonical_decode(b) -> np.ndarray:
+    """Canonical nibble bytes [..., w] (uint8) -> int8 codes [..., 2w] (host side)."""
+    b = np.ascontiguousarray(b).astype(np.uint8)
+    lo = (b & 0xF).astype(np.int8)
+    hi = (b >> 4).astype(np.int8)
+    lo = np.where(lo >= 8, lo - 16, lo).astype(np.int8)
+    hi = np.where(hi >= 8, hi - 16, hi).astype(np.int8)
+    return np.stack([lo, hi], axis=-1).reshape(*b.shape[:-1], 2 * b.shape[-1])
 
 
 # ------------------------------------------------------------------ buffers

@@ -311,6 +311,37 @@ tq_status tq_export_weights(const tq_weight_desc *d, const void *packed, void *w
       static_cast<uint16_t *>(l2_scales), static_cast<hipStream_t>(stream)));
 }
 
+tq_status tq_export_weights_canonical(const tq_weight_desc *d, const void *packed, void *wq, void *ws,
+                                      void *l1q, void *l1s, void *l2q, void *l2s, void *stream) {
+  if (d == nullptr || packed == nullptr || wq == nullptr || ws == nullptr) return TQ_ERR_NULL;
+  if (!desc_ok(d)) return TQ_ERR_BUFFER;
+  if (d->rank > 0 && (!l1q || !l1s || !l2q || !l2s)) return TQ_ERR_NULL;
+  if (!aligned16(packed) || !aligned16(wq) || !aligned16(ws)) return TQ_ERR_ALIGN;
+  if (d->rank > 0 && (!aligned16(l1q) || !aligned16(l1s) || !aligned16(l2q) || !aligned16(l2s)))
+    return TQ_ERR_ALIGN;
+  return hip_status(tq::launch_export_canonical(
+      geometry(d), static_cast<const uint8_t *>(packed), static_cast<uint8_t *>(wq),
+      static_cast<uint16_t *>(ws), static_cast<uint8_t *>(l1q), static_cast<uint16_t *>(l1s),
+      static_cast<uint8_t *>(l2q), static_cast<uint16_t *>(l2s), static_cast<hipStream_t>(stream)));
+}
+
+tq_status tq_act_codes_canonical(const void *x_codes, const void *x_scales, int m, int k, int group,
+                                 void *codes_out, void *scales_out, void *stream) {
+  if (x_codes == nullptr || x_scales == nullptr || codes_out == nullptr || scales_out == nullptr)
+    return TQ_ERR_NULL;
+  if (group != 64 && group != 128) return TQ_ERR_GROUP;
+  if (m < 0 || m > 65535 * 32 || k < 1 || k > (1 << 24)) return TQ_ERR_SHAPE;
+  if (k % group != 0) return TQ_ERR_GROUP;
+  if (!aligned16(x_codes) || !aligned16(x_scales) || !aligned16(codes_out) || !aligned16(scales_out))
+    return TQ_ERR_ALIGN;
+  if (m == 0) return TQ_OK;
+  return hip_status(tq::launch_act_canonical(static_cast<const uint8_t *>(x_codes),
+                                             static_cast<const uint16_t *>(x_scales), m, k, group / 64,
+                                             static_cast<uint8_t *>(codes_out),
+                                             static_cast<uint16_t *>(scales_out),
+                                             static_cast<hipStream_t>(stream)));
+}
+
 const char *tq_status_string(tq_status s) {
   switch (s) {
     case TQ_OK: return "ok";

@@ -58,6 +58,11 @@ hipError_t launch_quant_act(const uint16_t *x, int m, int k, int gk, uint32_t *c
                             uint16_t *scales, hipStream_t s);
 hipError_t launch_pack(const Geometry &g, const uint16_t *w, const uint16_t *l1,
                        const uint16_t *l2, uint8_t *packed, hipStream_t s);
+hipError_t launch_export_canonical(const Geometry &g, const uint8_t *packed, uint8_t *wq, uint16_t *ws,
+                                   uint8_t *l1q, uint16_t *l1s, uint8_t *l2q, uint16_t *l2s,
+                                   hipStream_t s);
+hipError_t launch_act_canonical(const uint8_t *x_codes, const uint16_t *x_scales, int m, int k, int gk,
+                                uint8_t *out_q, uint16_t *out_s, hipStream_t s);
 hipError_t launch_export(const Geometry &g, const uint8_t *packed, uint32_t *wc, uint16_t *ws,
                          uint32_t *l1c, uint16_t *l1s, uint32_t *l2c, uint16_t *l2s,
                          hipStream_t s);

@@ -284,6 +284,152 @@ __global__ __launch_bounds__(256) void export_l2_kernel(const uint8_t *__restric
     out_s[(int64_t)col * ng + jg / gr] = scales[(int64_t)(jg / gr) * n_pad + col];
 }
 
+// ---------------------------------------------------------------------------
+// Canonical layout: two's-complement nibbles, element 2 i in the low nibble
+// and 2 i + 1 in the high nibble of byte i, contiguous along the reduction
+// axis; scales as IEEE fp16 bit patterns.
+// ---------------------------------------------------------------------------
+// fp8 code byte (sign << 7 | |q|) -> the code's two's-complement nibble
+__device__ __forceinline__ uint32_t fp8_code_to_nibble(uint32_t b) {
+  const int m = (int)(b & 7u);
+  return (uint32_t)((b & 0x80u) ? -m : m) & 0xfu;
+}
+// 8 codes (one TQ4 word) -> 4 canonical bytes
+__device__ __forceinline__ uint32_t tq4_to_canonical(uint32_t w) {
+  uint32_t lo, hi;
+  tq4_to_fp8(w, lo, hi);   // bytes of codes 0..3, 4..7
+  const uint32_t c[8] = {lo & 0xffu, (lo >> 8) & 0xffu, (lo >> 16) & 0xffu, lo >> 24,
+                         hi & 0xffu, (hi >> 8) & 0xffu, (hi >> 16) & 0xffu, hi >> 24};
+  uint32_t out = 0;
+#pragma unroll
+  for (int i = 0; i < 4; i++)
+    out |= (fp8_code_to_nibble(c[2 * i]) | (fp8_code_to_nibble(c[2 * i + 1]) << 4)) << (8 * i);
+  return out;
+}
+
+// W_res rows / L1 columns: one thread per (vector, 64-wide block).  Scales go
+// to [vector][k / group] (vec_major) or [k / group][vector].
+__global__ __launch_bounds__(256) void export_canonical_kgroups_kernel(
+    const uint8_t *__restrict__ codes, const uint16_t *__restrict__ scales, int nvec, int nvec_pad,
+    int kblocks, int gk, bool vec_major, uint8_t *__restrict__ out_q, uint16_t *__restrict__ out_s) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (int64_t)nvec * kblocks) return;
+  const int g = (int)(t % kblocks);
+  const int v = (int)(t / kblocks);
+  const uint8_t *blk = codes + ((int64_t)(v >> 5) * kblocks + g) * 1024;
+  const int c = v & 31;
+  const u32x4 a = *reinterpret_cast<const u32x4 *>(blk + c * 16);
+  const u32x4 b = *reinterpret_cast<const u32x4 *>(blk + (32 + c) * 16);
+  uint8_t *o = out_q + (int64_t)v * kblocks * 32 + g * 32;
+  *reinterpret_cast<u32x4 *>(o) = u32x4{tq4_to_canonical(a.x), tq4_to_canonical(a.y),
+                                        tq4_to_canonical(a.z), tq4_to_canonical(a.w)};
+  *reinterpret_cast<u32x4 *>(o + 16) = u32x4{tq4_to_canonical(b.x), tq4_to_canonical(b.y),
+                                             tq4_to_canonical(b.z), tq4_to_canonical(b.w)};
+  const int kq = kblocks / gk;
+  if (g % gk == 0) {
+    const uint16_t sv = scales[(int64_t)(g / gk) * nvec_pad + v];
+    if (vec_major) out_s[(int64_t)v * kq + g / gk] = sv;
+    else out_s[(int64_t)(g / gk) * nvec + v] = sv;
+  }
+}
+
+// L2 columns along the rank axis: one thread per (column, 64-rank block);
+// codes [n][r / 2], scales [r / group_r][n].
+__global__ __launch_bounds__(256) void export_canonical_l2_kernel(
+    const uint8_t *__restrict__ codes, const uint16_t *__restrict__ scales, int n, int n_pad, int r,
+    int gr, int rblocks, uint8_t *__restrict__ out_q, uint16_t *__restrict__ out_s) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (int64_t)n * rblocks) return;
+  const int rb = (int)(t % rblocks);
+  const int col = (int)(t / rblocks);
+  const uint8_t *blk = codes + ((int64_t)(col >> 5) * rblocks + rb) * 1024;
+  const int c = col & 31;
+  const u32x4 a = *reinterpret_cast<const u32x4 *>(blk + c * 16);
+  const u32x4 b = *reinterpret_cast<const u32x4 *>(blk + (32 + c) * 16);
+  const uint32_t w[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+  const int j0 = rb * 64;
+  const int words = ((r < j0 + 64 ? r : j0 + 64) - j0) / 8;   // 8 ranks per word
+  uint32_t *o = reinterpret_cast<uint32_t *>(out_q + (int64_t)col * (r / 2) + j0 / 2);
+  for (int i = 0; i < words; i++) o[i] = tq4_to_canonical(w[i]);
+  for (int jg = j0 / gr * gr; jg < j0 + words * 8; jg += gr)
+    if (jg >= j0) out_s[(int64_t)(jg / gr) * n + col] = scales[(int64_t)(jg / gr) * n_pad + col];
+}
+
+// Activation codes (either tiled format) -> canonical [m][k / 2], scales
+// [m][k / group]: one thread per (token, 64-wide block).
+__global__ __launch_bounds__(256) void act_canonical_kernel(const uint8_t *__restrict__ x_codes,
+                                                            const uint16_t *__restrict__ x_scales,
+                                                            int m, int k, int gk, bool fp8,
+                                                            uint8_t *__restrict__ out_q,
+                                                            uint16_t *__restrict__ out_s) {
+  const int KG = k / kGroup, m32 = (m + 31) / 32 * 32;
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (int64_t)m * KG) return;
+  const int g = (int)(t % KG), row = (int)(t / KG);
+  const int tile = row / 32, i = row % 32;
+  uint32_t outw[8];
+  if (fp8) {
+    // block of 2 KiB: half p, lane slot 32 h + i holds bytes 16 p .. 16 p + 15
+    // of codes 32 h .. 32 h + 31
+    const uint8_t *blk = x_codes + ((int64_t)tile * KG + g) * 2048;
+    for (int h = 0; h < 2; h++)
+      for (int pp = 0; pp < 2; pp++) {
+        const u32x4 v = *reinterpret_cast<const u32x4 *>(blk + pp * 1024 + (32 * h + i) * 16);
+        const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+        for (int q = 0; q < 4; q++) {   // 4 codes -> 2 canonical bytes
+          const uint32_t x = wv[q];
+          const uint32_t b0 = fp8_code_to_nibble(x & 0xffu) | (fp8_code_to_nibble((x >> 8) & 0xffu) << 4);
+          const uint32_t b1 = fp8_code_to_nibble((x >> 16) & 0xffu) | (fp8_code_to_nibble(x >> 24) << 4);
+          const int e = 32 * h + 16 * pp + 4 * q;   // first code of the four
+          const int wi = e / 8, sh = (e % 8) * 4;
+          if (sh == 0) outw[wi] = b0 | (b1 << 8);
+          else outw[wi] |= (b0 | (b1 << 8)) << 16;
+        }
+      }
+  } else {
+    const uint8_t *blk = x_codes + ((int64_t)tile * KG + g) * 1024;
+    for (int h = 0; h < 2; h++) {
+      const u32x4 v = *reinterpret_cast<const u32x4 *>(blk + (32 * h + i) * 16);
+      outw[4 * h + 0] = tq4_to_canonical(v.x);
+      outw[4 * h + 1] = tq4_to_canonical(v.y);
+      outw[4 * h + 2] = tq4_to_canonical(v.z);
+      outw[4 * h + 3] = tq4_to_canonical(v.w);
+    }
+  }
+  uint8_t *o = out_q + (int64_t)row * (k / 2) + g * 32;
+  *reinterpret_cast<u32x4 *>(o) = u32x4{outw[0], outw[1], outw[2], outw[3]};
+  *reinterpret_cast<u32x4 *>(o + 16) = u32x4{outw[4], outw[5], outw[6], outw[7]};
+  if (g % gk == 0) out_s[(int64_t)row * (KG / gk) + g / gk] = x_scales[(int64_t)(g / gk) * m32 + row];
+}
+
+hipError_t launch_export_canonical(const Geometry &g, const uint8_t *packed, uint8_t *wq, uint16_t *ws,
+                                   uint8_t *l1q, uint16_t *l1s, uint8_t *l2q, uint16_t *l2s,
+                                   hipStream_t s) {
+  const int kg = g.k / kGroup;
+  hipLaunchKernelGGL(export_canonical_kgroups_kernel, dim3(nblocks((int64_t)g.n * kg)), dim3(256), 0, s,
+                     packed + g.off_w, reinterpret_cast<const uint16_t *>(packed + g.off_ws), g.n,
+                     g.n_pad, kg, g.gk, true, wq, ws);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || g.r == 0) return e;
+  hipLaunchKernelGGL(export_canonical_kgroups_kernel, dim3(nblocks((int64_t)g.r * kg)), dim3(256), 0, s,
+                     packed + g.off_l1, reinterpret_cast<const uint16_t *>(packed + g.off_l1s), g.r,
+                     g.r_pad32, kg, g.gk, false, l1q, l1s);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int rblocks = g.r_pad64 / 64;
+  hipLaunchKernelGGL(export_canonical_l2_kernel, dim3(nblocks((int64_t)g.n * rblocks)), dim3(256), 0, s,
+                     packed + g.off_l2, reinterpret_cast<const uint16_t *>(packed + g.off_l2s), g.n,
+                     g.n_pad, g.r, g.gr, rblocks, l2q, l2s);
+  return hipGetLastError();
+}
+
+hipError_t launch_act_canonical(const uint8_t *x_codes, const uint16_t *x_scales, int m, int k, int gk,
+                                uint8_t *out_q, uint16_t *out_s, hipStream_t s) {
+  hipLaunchKernelGGL(act_canonical_kernel, dim3(nblocks((int64_t)m * (k / kGroup))), dim3(256), 0, s,
+                     x_codes, x_scales, m, k, gk, act_codes_fp8(m), out_q, out_s);
+  return hipGetLastError();
+}
+
 hipError_t launch_export(const Geometry &g, const uint8_t *packed, uint32_t *wc, uint16_t *ws,
                          uint32_t *l1c, uint16_t *l1s, uint32_t *l2c, uint16_t *l2s,
                          hipStream_t s) {

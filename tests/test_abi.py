@@ -168,6 +168,29 @@ def test_pack_export_validation(L):
     assert L.tq_export_weights(D(d0), FAKE, FAKE, FAKE + 1, None, None, None, None, None) == 6
 
 
+def test_canonical_export_validation(L):
+    d = tq.weight_desc_init(256, 256, 16)
+    assert L.tq_export_weights_canonical(None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == 1
+    assert L.tq_export_weights_canonical(ctypes.byref(d), FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, None) == 1
+    assert L.tq_export_weights_canonical(ctypes.byref(d), FAKE + 4, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == 6
+    bad = tq.WeightDesc()
+    assert L.tq_export_weights_canonical(ctypes.byref(bad), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == 7
+    assert L.tq_act_codes_canonical(None, FAKE, 4, 64, 64, FAKE, FAKE, None) == 1
+    assert L.tq_act_codes_canonical(FAKE, FAKE, 4, 64, 32, FAKE, FAKE, None) == 3
+    assert L.tq_act_codes_canonical(FAKE, FAKE, 4, 192, 128, FAKE, FAKE, None) == 3
+    assert L.tq_act_codes_canonical(FAKE, FAKE, -1, 64, 64, FAKE, FAKE, None) == 2
+    assert L.tq_act_codes_canonical(FAKE, FAKE, 4, 64, 64, FAKE + 2, FAKE, None) == 6
+    assert L.tq_act_codes_canonical(FAKE, FAKE, 0, 64, 64, FAKE, FAKE, None) == 0
+
+
+def test_canonical_decode_helper():
+    """Two's-complement nibbles, element 2i low: the binding's host decoder."""
+    codes = np.array([[0, 1, -1, 7, -7, 3, -4, 2]], dtype=np.int8)
+    b = (codes[:, 0::2].astype(np.uint8) & 0xF) | ((codes[:, 1::2].astype(np.uint8) & 0xF) << 4)
+    assert b.tolist() == [[0x10, 0x7F, 0x39, 0x2C]]
+    np.testing.assert_array_equal(tq.canonical_decode(b), codes)
+
+
 def test_tq4_roundtrip():
     g = np.random.default_rng(0)
     c = g.integers(-7, 8, size=(5, 64)).astype(np.int8)

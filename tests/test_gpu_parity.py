@@ -600,6 +600,36 @@ def test_group128_rejects_prefill():
         tq.dual_gemm_debug(lay.desc, lay.packed, xc, xs, 600, y, kernel="prefill")
 
 
+@pytest.mark.parametrize("M,K,N,r,group", [(5, 256, 96, 64, 64), (600, 384, 64, 128, 128),
+                                           (33, 512, 100, 8, 128), (700, 192, 40, 0, 64)])
+def test_canonical_exports(oracle_mod, M, K, N, r, group):
+    """The canonical-layout exports of the weights and of the activation codes
+    (both tiled formats) equal the oracle's codes and scales."""
+    say(f"canonical exports M={M} K={K} N={N} r={r} group={group}")
+    d = random_codes_layer(M, K, N, r, seed=M + r + group)
+    lay = tq.Layer(dev(d["W_res"]), None if r == 0 else dev(d["L1"]), None if r == 0 else dev(d["L2"]),
+                   group=group)
+    wq, ws, l1q, l1s, l2q, l2s = tq.export_weights_canonical(lay.desc, lay.packed)
+    xc, xs = tq.empty_act(M, K, group=group)
+    tq.quant_act(dev(d["X"]), xc, xs, group)
+    aq, as_ = tq.act_codes_canonical(xc, xs, M, K, group)
+    torch.cuda.synchronize()
+    bits = lambda t: t.cpu().numpy().view(np.uint16)
+    qw, sw = oracle_mod.quantize(d["W_res"], group)
+    np.testing.assert_array_equal(tq.canonical_decode(wq.cpu().numpy()), qw)
+    np.testing.assert_array_equal(bits(ws), sw.view(np.uint16))
+    qx, sx = oracle_mod.quantize(d["X"], group)
+    np.testing.assert_array_equal(tq.canonical_decode(aq.cpu().numpy()), qx)
+    np.testing.assert_array_equal(bits(as_), sx.view(np.uint16))
+    if r:
+        q1, s1 = oracle_mod.quantize(d["L1"], group, axis=0)     # [K, r], [K/G, r]
+        np.testing.assert_array_equal(tq.canonical_decode(l1q.cpu().numpy()).T, q1)
+        np.testing.assert_array_equal(bits(l1s), s1.view(np.uint16))
+        q2, s2 = oracle_mod.quantize(d["L2"], min(group, r), axis=0)   # [r, N], [r/Gr, N]
+        np.testing.assert_array_equal(tq.canonical_decode(l2q.cpu().numpy()).T, q2)
+        np.testing.assert_array_equal(bits(l2s), s2.view(np.uint16))
+
+
 def test_group128_qo_shape(oracle_mod):
     """The paper's default configuration (G = 128, r = 128) on the LLaMA3-8B
     q_proj shape, synthetic workload weights, single-token decode."""
