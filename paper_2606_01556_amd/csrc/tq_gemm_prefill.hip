@@ -342,9 +342,6 @@ struct PKernel {
       __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);
       __builtin_amdgcn_sched_barrier(0);
       advance(P, three, ring_lds, g, KG);
-      Raw Rn;
-      read_raw(smem + ((g + 1) % D) * C::STAGE, lane, wr, wc, Rn);
-      asm volatile("" ::: "memory");   // issue the reads here, ahead of their use
       __builtin_amdgcn_sched_barrier(0);
       const v16f c10 = codes_half(a1, b0);
       __builtin_amdgcn_sched_barrier(0);
@@ -354,17 +351,19 @@ struct PKernel {
       __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);
       __builtin_amdgcn_sched_barrier(0);
       c11 = codes_half(a1, b1);
-      a0 = Rn.a[0];
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 12, 0);
+      const uint32_t sa1 = R.sa[1], sb1 = R.sb[1];
+      // this group's operand registers are free once its last code product is
+      // issued: the next group's operands are read into them (no copies)
+      read_raw(smem + ((g + 1) % D) * C::STAGE, lane, wr, wc, R);
+      asm volatile("" ::: "memory");   // issue the reads here, ahead of their use
       __builtin_amdgcn_sched_barrier(0);
-      p11 = outer2(R.sa[1], R.sb[1]);
+      p11 = outer2(sa1, sb1);
       fma16(acc[1][0], c10, p10);
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);
       __builtin_amdgcn_sched_barrier(0);
-      b0 = unpack32(Rn.b[0]);
-      R = Rn;
+      a0 = R.a[0];
+      b0 = unpack32(R.b[0]);
     }
     fma16(acc[1][1], c11, p11);
     wait_vm<0>();   // the refills past the end have landed before the ring is reused
