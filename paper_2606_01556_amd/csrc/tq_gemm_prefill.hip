@@ -17,14 +17,16 @@
 // expanded, so no wavefront unpacks an activation operand), the 256 weight
 // columns, the rank columns of L1 (first block only) and all their scales --
 // arrives once per workgroup by direct global->LDS loads
-// (global_load_lds_dwordx4) into a D-slot ring, D - 1 groups ahead; the loads
-// of a group are spread over the 8 wavefronts.  One workgroup barrier per
-// group publishes the group and frees the slot read in the previous step.
-// Each step issues the matrix-core products of group g first, then passes the
-// barrier, starts the loads of group g + D, reads and expands group g + 1's
-// operands, and applies group g's fp32 rescaling fmas, so the matrix core and
-// the vector ALU overlap inside a wavefront and across the two wavefronts of
-// a SIMD.
+// (global_load_lds_dwordx4) into a D-slot ring; the loads of a group are
+// spread over the 8 wavefronts, and one workgroup barrier per group hands
+// slots over.  A wavefront's group step has a matrix-core phase (the eight
+// products of the group) and a vector phase (the rescaling fmas of those
+// products, the next group's LDS reads and operand expansion, its share of
+// the loads).  The two wavefronts of a SIMD run these phases out of step --
+// their barrier sits after the matrix-core phase on one and after the vector
+// phase on the other -- so one issues matrix-core work while the other issues
+// vector work: on gfx950 a wavefront that interleaves both itself overlaps
+// them poorly, two wavefronts that split them overlap well.
 //
 // Arithmetic per 32x32 tile and group (Eq. 2): the exact integer group sum of
 // code products comes from v_mfma_scale_f32_32x32x64_f8f6f4 (codes as fp8
@@ -68,11 +70,12 @@ struct PCfg {
   static constexpr int QSTR = RB * 64 + 16;          // Q_H bytes per token row
   static constexpr int OFF_Q = RING;
   static constexpr int OFF_SH = OFF_Q + (RT > 0 ? PBM * QSTR : 0);
-  // stage-2 operands of each wavefront, loaded while the K loop starts:
-  // its 2 x RB L2 blocks, then a 1 KiB scale region
+  // stage-2 operands of each column pair (the two wavefronts with the same
+  // wc share them), loaded while the K loop starts: 2 x RB L2 blocks, then a
+  // 1 KiB scale region
   static constexpr int L2W = 2 * RB * 1024 + 1024;
   static constexpr int OFF_L2 = OFF_SH + (RT > 0 ? RB * PBM * 4 : 0);
-  static constexpr int LDS = OFF_L2 + (RT > 0 ? PNW * L2W : 0);
+  static constexpr int LDS = OFF_L2 + (RT > 0 ? 4 * L2W : 0);
   static constexpr int HT = RT >= 2 ? RT / 2 : 1;    // H tiles of an H wavefront
   static_assert(PBM * HSTR * 4 <= RING, "H staging fits in the ring");
   static_assert(LDS <= 160 * 1024, "fits the 160 KiB LDS of a CU");
@@ -146,8 +149,10 @@ struct PPlan {
 };
 
 __device__ __forceinline__ void p_issue(const PPlan &P, bool three, int g, uint32_t slot_lds) {
-  dma_s(P.v1, uniform_ptr(P.b1 + (uint64_t)g * P.inc1), slot_lds + P.l1);
-  dma_s(P.v2, uniform_ptr(P.b2 + (uint64_t)g * P.inc2), slot_lds + P.l2);
+  // the bases are wave-uniform (scalar registers): the group offset is added
+  // with scalar instructions
+  dma_s(P.v1, P.b1 + (uint32_t)g * P.inc1, slot_lds + P.l1);
+  dma_s(P.v2, P.b2 + (uint32_t)g * P.inc2, slot_lds + P.l2);
   if (three) dma_v(P.s3 + (uint64_t)g * P.inc3, slot_lds + P_SW);
 }
 
@@ -169,11 +174,11 @@ __device__ __forceinline__ void plan_main(const GemmArgs &a, int lane, int wave,
   const Geometry &geo = a.geo;
   const int KG = geo.k / kGroup;
   const int ct = min(n0 / 32 + wave, geo.n_pad / 32 - 1);   // past the last tile: never stored
-  P.b1 = a.packed + geo.off_w + (int64_t)ct * KG * 1024;
+  P.b1 = uniform_ptr(a.packed + geo.off_w + (int64_t)ct * KG * 1024);
   P.inc1 = 1024;
   P.v1 = lane * 16;
   P.l1 = P_B + wave * 1024;
-  P.b2 = act_tile(a, m0, wave >> 1) + (wave & 1) * 1024;
+  P.b2 = uniform_ptr(act_tile(a, m0, wave >> 1) + (wave & 1) * 1024);
   P.inc2 = 2048;
   P.v2 = lane * 16;
   P.l2 = P_A + wave * 1024;
@@ -244,128 +249,129 @@ template <int RT, int D>
 struct PKernel {
   using C = PCfg<RT, D>;
 
-  // prologue of a K loop: groups 0 .. D-1 into slots 0 .. D-1 (past the end:
-  // the last group again, so every step waits for the same count); returns
-  // when group 0 is visible to the workgroup
-  template <typename Pre>
-  __device__ __forceinline__ static void prologue(const PPlan &P, bool three, uint32_t ring_lds,
-                                                  int KG, Pre pre) {
-    // Every load the compiler itself issued (e.g. spill reloads) is complete
-    // here, so it has no reason to wait on the vector-memory counter inside
-    // the K loop -- a wait there would also drain the ring's loads.
-    wait_vm<0>();
-    pre();   // loads issued here complete before the ring's first group
-#pragma unroll
-    for (int s = 0; s < D; s++) p_issue(P, three, min(s, KG - 1), ring_lds + s * C::STAGE);
-    if (three) wait_vm<3 * (D - 1)>();
-    else wait_vm<2 * (D - 1)>();
-    __syncthreads();
-  }
-
-  // one step's hand-over: group g + 1 has landed (own loads), this wavefront's
-  // reads are done, every wavefront is past step g - 1, so group g + 1 is
-  // visible and slot g % D is free for group g + D
-  __device__ __forceinline__ static void advance(const PPlan &P, bool three, uint32_t ring_lds,
-                                                 int g, int KG) {
-    if (three) wait_vm<3 * (D - 2)>();
-    else wait_vm<2 * (D - 2)>();
-    wait_lgkm0();
-    __syncthreads();
-    p_issue(P, three, min(g + D, KG - 1), ring_lds + (g % D) * C::STAGE);
-  }
-
   struct Raw {
     v8i a[2];      // fp8 activation operands, ready for the matrix cores
     u32x4 b[2];    // TQ4 weight operands
     uint32_t sa[2], sb[2];
   };
 
-  __device__ __forceinline__ static void read_raw(const uint8_t *S, int lane, int wr, int wc,
-                                                  Raw &R) {
+  // This lane's byte offsets within a slot (loop-invariant): one address add
+  // per operand kind and group, the rest are immediate offsets.
+  struct RawOff {
+    uint32_t a, b, sa, sb;
+  };
+  __device__ __forceinline__ static RawOff raw_off(int lane, int wr, int wc) {
     const int l32 = lane & 31;
+    RawOff o;
+    o.a = P_A + 2 * wr * 2048 + lane * 16;
+    o.b = P_B + 2 * wc * 1024 + lane * 16;
+    o.sa = P_SX + (64 * wr + l32) * 2;
+    o.sb = P_SW + (64 * wc + l32) * 2;
+    return o;
+  }
+
+  __device__ __forceinline__ static void read_raw(const uint8_t *S, const RawOff &o, Raw &R) {
+    const uint8_t *pa = S + o.a, *pb = S + o.b, *psa = S + o.sa, *psb = S + o.sb;
 #pragma unroll
     for (int i = 0; i < 2; i++) {
-      const int ti = 2 * wr + i;
-      R.a[i] = join(*reinterpret_cast<const u32x4 *>(S + P_A + ti * 2048 + lane * 16),
-                    *reinterpret_cast<const u32x4 *>(S + P_A + ti * 2048 + 1024 + lane * 16));
-      R.sa[i] = *reinterpret_cast<const uint16_t *>(S + P_SX + (32 * ti + l32) * 2);
+      R.a[i] = join(*reinterpret_cast<const u32x4 *>(pa + i * 2048),
+                    *reinterpret_cast<const u32x4 *>(pa + i * 2048 + 1024));
+      R.sa[i] = *reinterpret_cast<const uint16_t *>(psa + i * 64);
     }
 #pragma unroll
     for (int j = 0; j < 2; j++) {
-      const int tj = 2 * wc + j;
-      R.b[j] = *reinterpret_cast<const u32x4 *>(S + P_B + tj * 1024 + lane * 16);
-      R.sb[j] = *reinterpret_cast<const uint16_t *>(S + P_SW + (32 * tj + l32) * 2);
+      R.b[j] = *reinterpret_cast<const u32x4 *>(pb + j * 1024);
+      R.sb[j] = *reinterpret_cast<const uint16_t *>(psb + j * 64);
     }
   }
 
-  // The residual K loop of one column block: this wavefront's 2 x 2 tiles,
-  // ascending K-groups.  The eight matrix-core instructions of a group (code
-  // product c and scale product p of tiles 00, 01, 10, 11) are each followed
-  // by independent vector work -- operand expansion, or the fmas of a tile
-  // whose products were issued two matrix instructions earlier -- so the
-  // matrix core and the vector ALU overlap inside the wavefront without
-  // dependency stalls.  Only tile 11's products are carried into the next
-  // group.  Each accumulator still receives its fmas in ascending group order.
-  // (Each region between scheduling barriers is pinned to "one matrix-core
-  // instruction, then the vector work".)
-  template <typename Pre>
-  __device__ __forceinline__ static void main_loop(const PPlan &P, bool three, uint8_t *smem,
-                                                   uint32_t ring_lds, int KG, int lane, int wr,
-                                                   int wc, v16f (&acc)[2][2], Pre pre) {
-    prologue(P, three, ring_lds, KG, pre);
+  // The residual K loop as two phases per group that the two wavefronts of a
+  // SIMD run out of step, so that one issues matrix-core work while the other
+  // issues vector work:
+  //   X(g): the eight matrix-core products of group g (code and scale products
+  //         of tiles 00, 01, 10, 11);
+  //   Y(g): the LDS reads of group g + 1, the 64 rescaling fmas of group g (on
+  //         products that X(g) has finished), this wavefront's loads of a later
+  //         group and the expansion of the weight operands of group g + 1.
+  // Every wavefront runs X(0) Y(0) X(1) Y(1) ... with one workgroup barrier per
+  // group, placed after X(g) on wavefronts 0-3 (GA) and after Y(g) on
+  // wavefronts 4-7 (each SIMD holds one of each), so between barriers k - 1 and
+  // k wavefront A runs Y(k - 1) X(k) while wavefront B runs X(k) Y(k).
+  //
+  // Ring hand-over.  In that interval A reads group k and B group k + 1, so
+  // the barrier that opens it must publish groups <= k + 1; slot s is free
+  // once both readers of its group have passed the barrier after their reads.
+  // Each wavefront issues its loads of group k + D - 1 into slot (k - 1) % D
+  // during interval k (A from Y(k - 1), B from Y(k)), and before barrier k
+  // waits until only its loads of groups k + 3 .. k + D - 1 may be in flight
+  // (D - 3 groups), so groups <= k + 2 are complete when barrier k opens.  The
+  // prologue loads groups 0 .. D - 1; loads past the last group repeat the
+  // last group into its free slot.
+  // (THREE: this wavefront also loads the scales, three loads per group; a
+  // template parameter, so that the loop body is one basic block)
+  template <bool GA, bool THREE, typename Pre>
+  __device__ __forceinline__ static void main_loop_pp(const PPlan &P, uint8_t *smem,
+                                                      uint32_t ring_lds, int KG, int lane, int wr,
+                                                      int wc, v16f (&acc)[2][2], Pre pre) {
+    static_assert(D >= 4, "the hand-over keeps D - 3 groups of loads in flight");
+    constexpr int L = THREE ? 3 : 2;   // loads per group
+    wait_vm<0>();
+    pre();
+#pragma unroll
+    for (int s = 0; s < D; s++) p_issue(P, THREE, min(s, KG - 1), ring_lds + s * C::STAGE);
+    wait_vm<L * (D - 3)>();
+    __syncthreads();
+    const RawOff ro = raw_off(lane, wr, wc);
     Raw R;
-    read_raw(smem, lane, wr, wc, R);
-    v8i a0 = R.a[0];
-    v8i b0 = unpack32(R.b[0]);
-    // tile 11's products of the previous group (none yet: fma(0, 0, +0)
-    // leaves the accumulator at +0)
-    v16f c11 = v16f{0}, p11 = v16f{0};
+    read_raw(smem, ro, R);
+    wait_lgkm0();
+    v8i b0 = unpack32(R.b[0]), b1 = unpack32(R.b[1]);
+    auto hand_over = [&]() {
+      wait_vm<L * (D - 3)>();
+      wait_lgkm0();
+      __syncthreads();
+    };
     for (int g = 0; g < KG; g++) {
-      const v16f c00 = codes_half(a0, b0);
-      fma16(acc[1][1], c11, p11);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);
+      // ---- X(g) ----
       __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_s_setprio(1);
+      const v16f c00 = codes_half(R.a[0], b0);
       const v16f p00 = outer2(R.sa[0], R.sb[0]);
-      const v8i b1 = unpack32(R.b[1]);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 12, 0);
-      __builtin_amdgcn_sched_barrier(0);
-      const v16f c01 = codes_half(a0, b1);
-      const v8i a1 = R.a[1];
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 12, 0);
-      __builtin_amdgcn_sched_barrier(0);
+      const v16f c01 = codes_half(R.a[0], b1);
       const v16f p01 = outer2(R.sa[0], R.sb[1]);
-      fma16(acc[0][0], c00, p00);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);
-      __builtin_amdgcn_sched_barrier(0);
-      advance(P, three, ring_lds, g, KG);
-      __builtin_amdgcn_sched_barrier(0);
-      const v16f c10 = codes_half(a1, b0);
-      __builtin_amdgcn_sched_barrier(0);
+      const v16f c10 = codes_half(R.a[1], b0);
       const v16f p10 = outer2(R.sa[1], R.sb[0]);
+      const v16f c11 = codes_half(R.a[1], b1);
+      const v16f p11 = outer2(R.sa[1], R.sb[1]);
+      __builtin_amdgcn_s_setprio(0);
+      __builtin_amdgcn_sched_barrier(0);
+      if constexpr (GA) hand_over();
+      __builtin_amdgcn_sched_barrier(0);
+      // ---- Y(g) ----
+      // group g + 1's operands into the registers X(g) read (past the last
+      // group: the last group again, never used)
+      read_raw(smem + (min(g + 1, KG - 1) % D) * C::STAGE, ro, R);
+      asm volatile("" ::: "memory");
+      __builtin_amdgcn_sched_barrier(0);
+      fma16(acc[0][0], c00, p00);
       fma16(acc[0][1], c01, p01);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);
       __builtin_amdgcn_sched_barrier(0);
-      c11 = codes_half(a1, b1);
-      const uint32_t sa1 = R.sa[1], sb1 = R.sb[1];
-      // this group's operand registers are free once its last code product is
-      // issued: the next group's operands are read into them (no copies)
-      read_raw(smem + ((g + 1) % D) * C::STAGE, lane, wr, wc, R);
-      asm volatile("" ::: "memory");   // issue the reads here, ahead of their use
+      {
+        // this wavefront's loads of a later group into a free slot (B at g = 0:
+        // group D - 1 again, the same bytes to the same place)
+        const int gl = GA ? g + D : g + D - 1;
+        p_issue(P, THREE, min(gl, KG - 1), ring_lds + (gl % D) * C::STAGE);
+      }
       __builtin_amdgcn_sched_barrier(0);
-      p11 = outer2(sa1, sb1);
       fma16(acc[1][0], c10, p10);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);
+      fma16(acc[1][1], c11, p11);
       __builtin_amdgcn_sched_barrier(0);
-      a0 = R.a[0];
+      wait_lgkm0();
       b0 = unpack32(R.b[0]);
+      b1 = unpack32(R.b[1]);
+      __builtin_amdgcn_sched_barrier(0);
+      if constexpr (!GA) hand_over();
     }
-    fma16(acc[1][1], c11, p11);
     wait_vm<0>();   // the refills past the end have landed before the ring is reused
   }
 
@@ -549,11 +555,12 @@ __global__ __launch_bounds__(64 * PNW, 1) void dual_gemm_prefill_kernel(GemmArgs
     for (int i = 0; i < 2; i++)
 #pragma unroll
       for (int j = 0; j < 2; j++) acc[i][j] = v16f{0};
-    // the stage-2 operands of this wavefront's two column tiles (L2 blocks
-    // and scales) travel with the first groups of the K loop
-    const uint32_t l2_lds = ring_lds + C::OFF_L2 + wave * C::L2W;
+    // the stage-2 operands of this column pair's two column tiles (L2 blocks
+    // and scales) travel with the first groups of the K loop, loaded by the
+    // wavefront with wr = 0 (published by the K loop's first barrier)
+    const uint32_t l2_lds = ring_lds + C::OFF_L2 + wc * C::L2W;
     auto pre = [&]() {
-      if constexpr (RT > 0) {
+      if (RT > 0 && wr == 0) {
 #pragma unroll
         for (int j = 0; j < 2; j++) {
           const int ct = min(n0 / 32 + 2 * wc + j, ctiles - 1);
@@ -572,7 +579,9 @@ __global__ __launch_bounds__(64 * PNW, 1) void dual_gemm_prefill_kernel(GemmArgs
               l2_lds + 2 * C::RB * 1024);
       }
     };
-    K::main_loop(P, wave == 0, smem, ring_lds, KG, lane, wr, wc, acc, pre);
+    if (wave == 0) K::template main_loop_pp<true, true>(P, smem, ring_lds, KG, lane, wr, wc, acc, pre);
+    else if (wr == 0) K::template main_loop_pp<true, false>(P, smem, ring_lds, KG, lane, wr, wc, acc, pre);
+    else K::template main_loop_pp<false, false>(P, smem, ring_lds, KG, lane, wr, wc, acc, pre);
 
     // ---- stage 2 (Q_H Q(L2)) and the single epilogue ----
     // (the index values are re-derived here, behind an opaque copy, so the
@@ -596,7 +605,7 @@ __global__ __launch_bounds__(64 * PNW, 1) void dual_gemm_prefill_kernel(GemmArgs
             const uint8_t *qrow = QS + (32 * ti + l32e) * C::QSTR + rbk * 64 + (lane_e >> 5) * 32;
             const v8i qa = join(*reinterpret_cast<const u32x4 *>(qrow),
                                 *reinterpret_cast<const u32x4 *>(qrow + 16));
-            const uint8_t *L2S = smem + C::OFF_L2 + wave * C::L2W;
+            const uint8_t *L2S = smem + C::OFF_L2 + wc * C::L2W;
             const v8i lb = unpack32(*reinterpret_cast<const u32x4 *>(
                 L2S + (j * C::RB + rbk) * 1024 + lane_e * 16));
             const float sl2 = half_bits_to_float(*reinterpret_cast<const uint16_t *>(
@@ -664,7 +673,7 @@ hipError_t launch_prefill_rt(const GemmArgs &a, hipStream_t s) {
     case 0: return launch_prefill<0, D>(a, s);
     case 1: return launch_prefill<1, D>(a, s);
     case 2: return launch_prefill<2, D>(a, s);
-    case 4: return launch_prefill<4, 5>(a, s);   // six slots and the stage-2 region overflow the LDS
+    case 4: return launch_prefill<4, D - 1>(a, s);   // the larger Q_H and stage-2 region leave D - 1 slots
     default: return hipErrorInvalidValue;
   }
 }
@@ -672,7 +681,7 @@ hipError_t launch_prefill_rt(const GemmArgs &a, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_dual_gemm_prefill(const GemmArgs &a, hipStream_t s) {
-  return launch_prefill_rt<6>(a, s);
+  return launch_prefill_rt<8>(a, s);
 }
 
 }  // namespace tq
