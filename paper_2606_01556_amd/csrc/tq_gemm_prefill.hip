@@ -306,7 +306,7 @@ struct PKernel {
   // waits until only its loads of groups k + 3 .. k + D - 1 may be in flight
   // (D - 3 groups), so groups <= k + 2 are complete when barrier k opens.  The
   // prologue loads groups 0 .. D - 1; loads past the last group repeat the
-  // last group into its free slot.
+  // last group into a free slot.
   // (THREE: this wavefront also loads the scales, three loads per group; a
   // template parameter, so that the loop body is one basic block)
   template <bool GA, bool THREE, typename Pre>
@@ -331,6 +331,15 @@ struct PKernel {
       wait_lgkm0();
       __syncthreads();
     };
+    // The slots read and loaded in Y(g) advance one slot per group
+    // (wave-uniform; no division in the loop): the read slot holds group
+    // min(g + 1, KG - 1), the load slot (an LDS address) receives group
+    // g + D (A) or g + D - 1 (B).
+    uint32_t ring0 = ring_lds;
+    asm volatile("" : "+s"(ring0));   // a plain scalar from here on
+    const uint32_t ring_end = ring0 + C::RING;
+    uint32_t rd_off = (uint32_t)(min(1, KG - 1) * C::STAGE);
+    uint32_t ld_lds = ring0 + (GA ? 0u : (uint32_t)((D - 1) * C::STAGE));
     for (int g = 0; g < KG; g++) {
       // ---- X(g) ----
       __builtin_amdgcn_sched_barrier(0);
@@ -350,7 +359,11 @@ struct PKernel {
       // ---- Y(g) ----
       // group g + 1's operands into the registers X(g) read (past the last
       // group: the last group again, never used)
-      read_raw(smem + (min(g + 1, KG - 1) % D) * C::STAGE, ro, R);
+      read_raw(smem + rd_off, ro, R);
+      {
+        const uint32_t nx = rd_off + C::STAGE == (uint32_t)C::RING ? 0u : rd_off + C::STAGE;
+        rd_off = g + 2 < KG ? nx : rd_off;
+      }
       asm volatile("" ::: "memory");
       __builtin_amdgcn_sched_barrier(0);
       fma16(acc[0][0], c00, p00);
@@ -360,7 +373,9 @@ struct PKernel {
         // this wavefront's loads of a later group into a free slot (B at g = 0:
         // group D - 1 again, the same bytes to the same place)
         const int gl = GA ? g + D : g + D - 1;
-        p_issue(P, THREE, min(gl, KG - 1), ring_lds + (gl % D) * C::STAGE);
+        p_issue(P, THREE, min(gl, KG - 1), ld_lds);
+        ld_lds += C::STAGE;
+        ld_lds = ld_lds == ring_end ? ring0 : ld_lds;
       }
       __builtin_amdgcn_sched_barrier(0);
       fma16(acc[1][0], c10, p10);
