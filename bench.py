@@ -637,7 +637,7 @@ def rank_overhead():
 
 def kernel_choice():
     """Past 512 tokens tq_dual_gemm picks the large kernel (128 x 256 blocks),
-    the prefill kernel (r > 64 beyond one round of blocks) or the mid kernel
+    the prefill kernel (beyond one round of blocks) or the mid kernel
     (32-token blocks, where the large blocks would leave most CUs idle).  Times
     each of them, forced through tq_dual_gemm_debug, beside the one it picks,
     on LLaMA3 layer shapes (HIP events, rotated weight copies, random-init
@@ -673,8 +673,6 @@ def kernel_choice():
                 picked = tq.dual_gemm_kernel(lay.desc, m)
                 res = {}
                 for kname in ("large", "prefill", "mid"):
-                    if kname == "prefill" and rl <= 64:
-                        continue              # the prefill kernel serves r > 64 only
 
                     def gemm():
                         p = copies[call[0] % ncopy]

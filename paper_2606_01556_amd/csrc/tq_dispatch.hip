@@ -1,16 +1,19 @@
 // Kernel selection for the fused layer by token count: the decode kernel for
 // m <= 16 (bound by the weight bytes; H formed in every work-group), the mid kernel
 // (32-token blocks, H formed per block) up to 512 tokens, then the large
-// kernel (128 x 256 blocks, 16 wavefronts), or for r > 64 once its blocks
-// take more than one round over the CUs the prefill kernel (H shared by runs
-// of column blocks); past 512 tokens the mid kernel again where the large
-// kernel's blocks would leave most CUs idle.
+// kernel (128 x 256 blocks, 16 wavefronts), or once its blocks take more
+// than one round over the CUs the prefill kernel (H shared by runs of column
+// blocks) -- for r <= 64 only where a run is long enough to carry its H pass;
+// past 512 tokens the mid kernel again where the large kernel's blocks would
+// leave most CUs idle.
 #include "tq_kernels.hpp"
 
 namespace tq {
 
 // one round of large-kernel blocks in the mid kernel's cost units
 constexpr int kLargeRound = 28;
+// K-groups per prefill work-group run from which it beats the large kernel at r <= 64
+constexpr int kPrefillMinRun = 256;
 
 int choose_kernel(const GemmArgs &a) {
   if (a.force_kernel >= 0) return a.force_kernel;   // validated by the caller
@@ -19,12 +22,18 @@ int choose_kernel(const GemmArgs &a) {
   if (!act_codes_fp8(a.m)) return kKernelMid;
   // 128 x 256 blocks: the large kernel (16 wavefronts, H formed in the main
   // loop of every block) is faster while its blocks fit in one round over the
-  // 256 CUs, and for ranks up to 64 at any size (its H share is then at most a
-  // quarter of a block's work); beyond, the prefill kernel forms H once per
-  // run of column blocks
-  const int blocks = (a.m + 127) / 128 * ((a.geo.n_pad + 255) / 256);
+  // 256 CUs; beyond, the prefill kernel forms H once per run of column blocks
+  // (one work-group per CU).  For ranks up to 64 the large kernel's H share
+  // is at most a quarter of a block's work, so the prefill kernel wins only
+  // where its run (cpw column blocks of KG groups each) is long -- at least
+  // kPrefillMinRun groups -- for its H pass and per-block fills to amortize.
+  const int m_tiles = (a.m + 127) / 128, n_tiles = (a.geo.n_pad + 255) / 256;
+  const int blocks = m_tiles * n_tiles;
+  const int runs = m_tiles >= 256 ? 1 : 256 / m_tiles;
+  const int cpw = (n_tiles + runs - 1) / runs;
+  const bool long_run = cpw * (a.geo.k / 64) >= kPrefillMinRun;   // 64-wide K-groups
   // (the prefill kernel takes 64-wide groups only)
-  const bool large = blocks <= 256 || a.geo.r_pad32 <= 64 || a.geo.gk != 1;
+  const bool large = blocks <= 256 || (a.geo.r_pad32 <= 64 && !long_run) || a.geo.gk != 1;
   // Few large blocks leave most CUs idle (a round of them costs about as much
   // as kLargeRound tile-group units of the mid kernel, whose 32-token blocks
   // fill the CUs at these sizes too): take the cheaper of the two.

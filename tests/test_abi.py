@@ -283,13 +283,19 @@ def test_kernel_choice(L):
     """tq_dual_gemm_kernel: the decode kernel up to 16 tokens (while their
     activation codes fit its LDS), the mid kernel up to 512, past that the
     large kernel where its 128 x 256 blocks fill the CUs, the mid kernel where
-    they would leave most CUs idle, the prefill kernel for r > 64 beyond one
-    round of blocks; -1 for a bad descriptor or m."""
+    they would leave most CUs idle, the prefill kernel beyond one round of
+    blocks (for r <= 64 only where a work-group's run of column blocks spans
+    at least 256 K-groups); -1 for a bad descriptor or m."""
     d = tq.weight_desc_init(4096, 4096, 64)           # n, k, r
     assert [tq.dual_gemm_kernel(d, m) for m in (1, 16, 17, 512, 2048)] == \
         ["decode", "decode", "mid", "mid", "large"]
     assert tq.dual_gemm_kernel(tq.weight_desc_init(96, 4096, 64), 600) == "mid"
     assert tq.dual_gemm_kernel(tq.weight_desc_init(14336, 4096, 128), 4096) == "prefill"
+    # r = 64 beyond one round: runs of 7 blocks x 64 groups take the prefill
+    # kernel, runs of 2 x 64 stay on the large kernel
+    assert tq.dual_gemm_kernel(tq.weight_desc_init(14336, 4096, 64), 4096) == "prefill"
+    assert tq.dual_gemm_kernel(tq.weight_desc_init(4096, 4096, 64), 4096) == "large"
+    assert tq.dual_gemm_kernel(tq.weight_desc_init(4096, 14336, 64), 4096) == "prefill"
     assert tq.dual_gemm_kernel(tq.weight_desc_init(8192, 28672, 128), 1) == "decode"
     assert tq.dual_gemm_kernel(tq.weight_desc_init(8192, 28672, 128), 8) == "decode"
     assert tq.dual_gemm_kernel(tq.weight_desc_init(8192, 28672, 128), 9) == "mid"
