@@ -86,30 +86,41 @@ __global__ __launch_bounds__(256) void quant_act_kernel(const uint16_t *__restri
   if ((lane & 7) == 0) scales[(int64_t)q0 * m32 + row] = row < m ? s16 : (uint16_t)0;
 }
 
+// Rows of x quantized into TQ4 words in the layout of the packed weight
+// blocks: block (t, g) holds rows 32 t .. 32 t + 31 of K block g, and the
+// scales are group-major with the row count padded to 32 -- the same layout as
+// the packed W_res codes and scales, so the weight packing uses this launch.
+static void launch_quant_rows_tq4(const uint16_t *x, int m, int k, int gk, uint32_t *codes,
+                                  uint16_t *scales, hipStream_t s) {
+  const int m32 = (m + 31) / 32 * 32;
+  const dim3 grid((unsigned)(k / kGroup / gk), (unsigned)(m32 / 32));
+  if (gk == 2) hipLaunchKernelGGL((quant_act_kernel<false, 2>), grid, dim3(256), 0, s, x, m, k, codes, scales);
+  else hipLaunchKernelGGL((quant_act_kernel<false, 1>), grid, dim3(256), 0, s, x, m, k, codes, scales);
+}
+
 hipError_t launch_quant_act(const uint16_t *x, int m, int k, int gk, uint32_t *codes,
                             uint16_t *scales, hipStream_t s) {
-  const int m32 = (m + 31) / 32 * 32;
-  const int KG = k / kGroup;
   // one quantization group per work-group: the kernel is bound by its vector
   // ALU work, and more groups per work-group measured slower at every size
-  const dim3 grid((unsigned)(KG / gk), (unsigned)(m32 / 32));
-  const bool f8 = act_codes_fp8(m);
-  if (gk == 2) {
-    if (f8) hipLaunchKernelGGL((quant_act_kernel<true, 2>), grid, dim3(256), 0, s, x, m, k, codes, scales);
-    else hipLaunchKernelGGL((quant_act_kernel<false, 2>), grid, dim3(256), 0, s, x, m, k, codes, scales);
-  } else {
-    if (f8) hipLaunchKernelGGL((quant_act_kernel<true, 1>), grid, dim3(256), 0, s, x, m, k, codes, scales);
-    else hipLaunchKernelGGL((quant_act_kernel<false, 1>), grid, dim3(256), 0, s, x, m, k, codes, scales);
+  if (!act_codes_fp8(m)) {
+    launch_quant_rows_tq4(x, m, k, gk, codes, scales, s);
+    return hipGetLastError();
   }
+  const int m32 = (m + 31) / 32 * 32;
+  const dim3 grid((unsigned)(k / kGroup / gk), (unsigned)(m32 / 32));
+  if (gk == 2) hipLaunchKernelGGL((quant_act_kernel<true, 2>), grid, dim3(256), 0, s, x, m, k, codes, scales);
+  else hipLaunchKernelGGL((quant_act_kernel<true, 1>), grid, dim3(256), 0, s, x, m, k, codes, scales);
   return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
-// Weight packing: one thread per (vector, group) -- a vector is a row of
-// W_res, a column of L1 or a column of L2 -- quantizes its group and writes
-// the codes into the two 16-byte lane slots of its block plus the scale.
-// Vectors past the real sizes (padding to 32 columns / 64 ranks) get zero
-// codes and zero scales, so every byte of the packed buffer is written.
+// Weight packing.  W_res rows go through the activation quantizer's TQ4 path
+// (launch_quant_rows_tq4), whose output is the packed block layout.  The
+// strided vectors -- columns of L1 and of L2 -- take one thread per (vector,
+// group): it quantizes its group and writes the codes into the two 16-byte
+// lane slots of its block plus the scale.  Vectors past the real sizes
+// (padding to 32 columns / 64 ranks) get zero codes and zero scales, so every
+// byte of the packed buffer is written.
 // ---------------------------------------------------------------------------
 // The fp16 scale of `len` values at src with the given element stride (0 if
 // !present), and the TQ4 words of the 64 of them starting at element e0
@@ -212,9 +223,10 @@ __global__ __launch_bounds__(256) void zero16_kernel(uint8_t *__restrict__ p, in
 hipError_t launch_pack(const Geometry &g, const uint16_t *w, const uint16_t *l1,
                        const uint16_t *l2, uint8_t *packed, hipStream_t s) {
   const int kg = g.k / kGroup, kq = kg / g.gk;   // 64-wide blocks, quantization groups
-  hipLaunchKernelGGL(pack_kgroups_kernel, dim3(nblocks((int64_t)g.n_pad * kq)), dim3(256), 0, s,
-                     w, (int64_t)g.k, (int64_t)1, g.n, g.n_pad, kg, g.gk, packed + g.off_w,
-                     reinterpret_cast<uint16_t *>(packed + g.off_ws));
+  // W_res rows: the quantizer of activation rows writes exactly this block
+  // layout (n_pad = n rounded up to 32; padding rows get zero codes and scales)
+  launch_quant_rows_tq4(w, g.n, g.k, g.gk, reinterpret_cast<uint32_t *>(packed + g.off_w),
+                        reinterpret_cast<uint16_t *>(packed + g.off_ws), s);
   // the slack read past the last K block: 1 KiB of codes, one scale row
   hipLaunchKernelGGL(zero16_kernel, dim3(1), dim3(256), 0, s,
                      packed + g.off_w + (uint64_t)g.n_pad / 32 * kg * 1024, (int64_t)64);
