@@ -184,6 +184,73 @@ def trace_summary(trace_dir, title, cmd):
               f"{float(r['MaxNs']) / 1e3:.2f} | {float(r['TotalDurationNs']) / total * 100:.1f} % |")
 
 
+SIMDS = 1024          # MI355X: 256 CUs x 4 SIMDs
+XCCS = 8
+
+
+def counter_summary(dirs, layer_name, m, cmd):
+    """Markdown summary of rocprofv3 --pmc passes of --kernel-only: the SQ
+    counters of the layer's fused kernel, summed over the chip and averaged
+    over its dispatches, and the unit-busy fractions derived from them."""
+    import paper_2606_01556_amd as tq
+    from tq_synth import WORKLOADS
+    wl = WORKLOADS[HEADLINE]
+    layer = [l for l in wl.layers if l.name == layer_name][0]
+    kname = tq.dual_gemm_kernel(tq.weight_desc_init(layer.N, layer.K, layer.r), m)
+    sym = f"dual_gemm_{kname}_kernel"
+    per = {}
+    for d in dirs:
+        disp = {}
+        for r in _csv_rows(d, "counter_collection.csv"):
+            if sym not in r["Kernel_Name"]:
+                continue
+            key = (r["Dispatch_Id"], r["Counter_Name"])
+            disp[key] = disp.get(key, 0.0) + float(r["Counter_Value"])
+        by_ctr = {}
+        for (_, c), v in disp.items():
+            by_ctr.setdefault(c, []).append(v)
+        for c, vs in by_ctr.items():
+            per[c] = float(np.mean(vs))
+    if not per:
+        raise SystemExit(f"no {sym} dispatch in {dirs}")
+    cyc = per["GRBM_GUI_ACTIVE"] / XCCS          # GPU cycles of one dispatch
+    wave_cyc = per.get("SQ_WAVE_CYCLES", 0.0)    # quad-cycles, summed over waves
+    print(f"# SQ counters: {sym}, {HEADLINE} {layer_name} (K={layer.K}, N={layer.N}, r={layer.r}) at M={m}\n")
+    print("Commands (from the repository root on the GPU box; one rocprofv3 --pmc pass per line):\n")
+    print("```\n" + cmd + "\n```\n")
+    print(f"Kernel source sha256: `{kernel_sha(kname)}`. Values: per dispatch, summed over the chip,")
+    print("averaged over the dispatches of the kernel.\n")
+    print("| counter | value |")
+    print("|---|---|")
+    for c in sorted(per):
+        print(f"| `{c}` | {per[c]:.4g} |")
+    print("\n| derived | value |")
+    print("|---|---|")
+    print(f"| GPU cycles per dispatch (GRBM_GUI_ACTIVE / {XCCS} XCCs) | {cyc:.4g} |")
+    if "SQ_VALU_MFMA_BUSY_CYCLES" in per:
+        print(f"| matrix cores busy, share of SIMD cycles (MFMA_BUSY / (cycles x {SIMDS})) | "
+              f"{per['SQ_VALU_MFMA_BUSY_CYCLES'] / (cyc * SIMDS) * 100:.1f} % |")
+    if wave_cyc:
+        for c, label in (("SQ_ACTIVE_INST_VALU", "vector instructions active"),
+                         ("SQ_ACTIVE_INST_SCA", "scalar instructions active"),
+                         ("SQ_ACTIVE_INST_LDS", "LDS instructions active"),
+                         ("SQ_ACTIVE_INST_ANY", "any instruction active"),
+                         ("SQ_WAIT_INST_ANY", "waiting to issue"),
+                         ("SQ_WAIT_ANY", "waiting on counters / barriers")):
+            if c in per:
+                print(f"| {label}, share of wave cycles | {per[c] / wave_cyc * 100:.1f} % |")
+    if "SQ_WAVES" in per:
+        w = per["SQ_WAVES"]
+        for c in ("SQ_INSTS_MFMA", "SQ_INSTS_LDS", "SQ_INSTS_SALU"):
+            if c in per:
+                print(f"| `{c}` per wavefront | {per[c] / w:.0f} |")
+    if "SQ_INSTS_VALU" in per and "SQ_WAVES" in per:
+        print(f"| `SQ_INSTS_VALU` per wavefront | {per['SQ_INSTS_VALU'] / per['SQ_WAVES']:.0f} |")
+    if "SQ_LDS_BANK_CONFLICT" in per and per.get("SQ_LDS_IDX_ACTIVE"):
+        print(f"| LDS bank-conflict cycles per LDS-active cycle | "
+              f"{per['SQ_LDS_BANK_CONFLICT'] / per['SQ_LDS_IDX_ACTIVE']:.3f} |")
+
+
 # ---------------------------------------------------------------------------
 # the CPU baseline: the oracle on the host cores
 # ---------------------------------------------------------------------------
@@ -707,6 +774,8 @@ def main():
     ap.add_argument("--reps", type=int, default=5)
     ap.add_argument("--traffic-summary", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "LAYER", "M"),
                     help="write the traffic summary of a --kernel-only counter pair under profiles/")
+    ap.add_argument("--counter-summary", nargs="+", metavar="ARG",
+                    help="PASS_DIR... LAYER M: print the SQ counter summary of --kernel-only --pmc passes")
     ap.add_argument("--trace-summary", nargs=2, metavar=("TRACE_DIR", "TITLE"),
                     help="print a markdown summary of a rocprofv3 --kernel-trace --stats run")
     ap.add_argument("--cmd", action="append", default=[],
@@ -722,6 +791,10 @@ def main():
     if args.traffic_summary:
         f, w, layer, m = args.traffic_summary
         traffic_summary(f, w, layer, int(m), args.cmd)
+        return
+    if args.counter_summary:
+        *dirs, layer, m = args.counter_summary
+        counter_summary(dirs, layer, int(m), "\n".join(args.cmd))
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the layer runs on a single MI355X "
