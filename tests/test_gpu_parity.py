@@ -246,12 +246,13 @@ def test_mid_kernel_variants(oracle_mod, ct, M, K, N, r):
 
 @pytest.mark.parametrize("kernel", ["large", "prefill", "mid"])
 @pytest.mark.parametrize("M,K,N,r", [(600, 576, 1000, 64), (1100, 256, 520, 128), (700, 320, 300, 16),
-                                     (900, 128, 2000, 0), (530, 192, 4096, 32)])
+                                     (900, 128, 2000, 0), (530, 192, 4096, 32), (640, 64, 600, 128)])
 def test_large_m_kernels(oracle_mod, kernel, M, K, N, r):
     """m > 512 (fp8 activation codes) on the three kernels that take it: the
     16-wavefront blocks with H in the main loop, the prefill kernel with its
     separate H pass, and the mid kernel's 32-token blocks; ragged token and
-    column counts, odd K-group counts, every rank-tile count."""
+    column counts, odd K-group counts down to a single K-group, every
+    rank-tile count."""
     say(f"{kernel} M={M} K={K} N={N} r={r}")
     d = random_codes_layer(M, K, N, r, seed=M + 3 * N + r)
     full_parity(oracle_mod, d["X"], d["W_res"], d["L1"], d["L2"], kernel=kernel)
