@@ -702,13 +702,13 @@ def rank_overhead():
             print(f"| {name} {Kl}→{Nl} | {m} | {base:.1f} | {cells} |", flush=True)
 
 
-def kernel_choice():
+def kernel_choice(group):
     """Past 512 tokens tq_dual_gemm picks the large kernel (128 x 256 blocks),
     the prefill kernel (beyond one round of blocks) or the mid kernel
     (32-token blocks, where the large blocks would leave most CUs idle).  Times
     each of them, forced through tq_dual_gemm_debug, beside the one it picks,
-    on LLaMA3 layer shapes (HIP events, rotated weight copies, random-init
-    weights).  Prints a markdown table."""
+    on LLaMA3 layer shapes in quantization groups of `group` (HIP events,
+    rotated weight copies, random-init weights).  Prints a markdown table."""
     import torch
     import paper_2606_01556_amd as tq
     dev = torch.device("cuda")
@@ -722,11 +722,11 @@ def kernel_choice():
     for name, Kl, Nl in shapes:
         with torch.cuda.stream(stream):
             W = (torch.randn(Nl, Kl, device=dev) * 0.02).half()
-        for rl in (64, 128):
+        for rl in ((0, 64, 128) if group == 128 else (64, 128)):
             with torch.cuda.stream(stream):
-                L1 = (torch.randn(Kl, rl, device=dev) * 0.05).half()
-                L2 = (torch.randn(rl, Nl, device=dev) * 0.05).half()
-                lay = tq.Layer(W, L1, L2, stream=stream)
+                L1 = (torch.randn(Kl, rl, device=dev) * 0.05).half() if rl else None
+                L2 = (torch.randn(rl, Nl, device=dev) * 0.05).half() if rl else None
+                lay = tq.Layer(W, L1, L2, group=group, stream=stream)
                 ncopy = max(2, int(np.ceil(ROTATE_BYTES / lay.desc.packed_bytes)))
                 copies = [lay.packed] + [lay.packed.clone() for _ in range(ncopy - 1)]
             torch.cuda.synchronize()
@@ -734,9 +734,9 @@ def kernel_choice():
             for m in (576, 1024, 2048, 4096):
                 with torch.cuda.stream(stream):
                     X = torch.randn(m, Kl, device=dev).half()
-                    xc, xs = tq.empty_act(m, Kl, dev)
+                    xc, xs = tq.empty_act(m, Kl, dev, group=group)
                     Y = torch.empty((m, Nl), dtype=torch.float16, device=dev)
-                    tq.quant_act(X, xc, xs, stream=s)
+                    tq.quant_act(X, xc, xs, group, stream=s)
                 picked = tq.dual_gemm_kernel(lay.desc, m)
                 res = {}
                 for kname in ("large", "prefill", "mid"):
@@ -769,6 +769,8 @@ def main():
                     help="the low-rank branch's overhead at ranks 0/32/64/128 (markdown table)")
     ap.add_argument("--kernel-choice", action="store_true",
                     help="the large, prefill and mid kernels past 512 tokens beside the picked one")
+    ap.add_argument("--group", type=int, default=64, choices=(64, 128),
+                    help="quantization group of --kernel-choice")
     ap.add_argument("--kernel-only", nargs=2, metavar=("LAYER", "M"),
                     help="repeat one headline layer call (gate_up or down) after a calibration copy")
     ap.add_argument("--reps", type=int, default=5)
@@ -805,7 +807,7 @@ def main():
     elif args.ranks:
         rank_overhead()
     elif args.kernel_choice:
-        kernel_choice()
+        kernel_choice(args.group)
     elif args.kernel_only:
         kernel_only(args)
     else:

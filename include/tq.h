@@ -188,9 +188,7 @@ int tq_dual_gemm_kernel(const tq_weight_desc *d, int m);
  *   kernel     -1: the kernel tq_dual_gemm would launch; otherwise the
  *              tq_kernel value to run (TQ_KERNEL_DECODE needs a decode-sized
  *              m that fits its LDS, TQ_KERNEL_LARGE / TQ_KERNEL_PREFILL need
- *              m > 512, TQ_KERNEL_MID serves any m; TQ_ERR_SHAPE otherwise;
- *              TQ_KERNEL_PREFILL takes 64-wide groups only, TQ_ERR_GROUP
- *              otherwise -- tq_dual_gemm never picks it for 128-wide ones)
+ *              m > 512, TQ_KERNEL_MID serves any m; TQ_ERR_SHAPE otherwise)
  *   mid_tiles  0: the mid kernel's own choice of 32-column tiles per
  *              work-group; 1, 2 or 4 forces it (TQ_ERR_SHAPE otherwise)
  *   h, sh, qh  all NULL, or all set (r > 0, else TQ_ERR_RANK) to copy the

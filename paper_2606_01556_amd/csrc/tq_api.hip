@@ -211,9 +211,6 @@ static tq_status dual_gemm_impl(const tq_weight_desc *d, const void *packed, con
   a.dbg_qh = static_cast<int8_t *>(c.qh);
   a.force_kernel = c.kernel;
   a.mid_ct = c.mid_ct;
-  // 128-wide groups: every kernel but the prefill kernel takes them, and the
-  // dispatch never picks it for them (only a forced choice can)
-  if (a.geo.gk != 1 && !fq && !tq::serves_group(tq::choose_kernel(a), a.geo.gk)) return TQ_ERR_GROUP;
   const hipStream_t s = static_cast<hipStream_t>(stream);
   if (fq) return hip_status(tq::launch_dual_gemm_decode(a, static_cast<const uint16_t *>(c.x16), s));
   if (c.path == Path::Unfused) return hip_status(tq::launch_dual_gemm_unfused(a, c.scratch, s));

@@ -32,8 +32,12 @@ int choose_kernel(const GemmArgs &a) {
   const int runs = m_tiles >= 256 ? 1 : 256 / m_tiles;
   const int cpw = (n_tiles + runs - 1) / runs;
   const bool long_run = cpw * (a.geo.k / 64) >= kPrefillMinRun;   // 64-wide K-groups
-  // (the prefill kernel takes 64-wide groups only)
-  const bool large = blocks <= 256 || (a.geo.r_pad32 <= 64 && !long_run) || a.geo.gk != 1;
+  // With 128-wide groups the large kernel chains two dependent products per H
+  // tile in its main loop, and the prefill kernel applies half the scale
+  // products per K block: the prefill kernel wins past one round of blocks
+  // at every rank but 0.
+  const bool prefill_wins = a.geo.gk == 1 ? a.geo.r_pad32 > 64 || long_run : a.geo.r_pad32 > 0;
+  const bool large = blocks <= 256 || !prefill_wins;
   // Few large blocks leave most CUs idle (a round of them costs about as much
   // as kLargeRound tile-group units of the mid kernel, whose 32-token blocks
   // fill the CUs at these sizes too): take the cheaper of the two.
@@ -41,11 +45,6 @@ int choose_kernel(const GemmArgs &a) {
   const bool mid = large && dual_gemm_mid_cost(a) < rounds * kLargeRound;
   if (mid) return kKernelMid;
   return large ? kKernelLarge : kKernelPrefill;
-}
-
-bool serves_group(int kernel, int gk) {
-  if (gk == 1) return true;
-  return gk == 2 && kernel != kKernelPrefill;
 }
 
 hipError_t launch_dual_gemm(const GemmArgs &a, hipStream_t s) {

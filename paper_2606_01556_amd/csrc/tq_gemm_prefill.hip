@@ -98,6 +98,13 @@ __device__ __forceinline__ v16f codes_half(v8i a, v8i b) {
                                                          kScale2p9);
 }
 
+// the same added to c: the two 64-wide blocks of a 128-wide group (exact
+// while the sums stay integers below 2^24)
+__device__ __forceinline__ v16f codes_half_acc(v8i a, v8i b, v16f c) {
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, kScale2p9 - 1, 0,
+                                                         kScale2p9);
+}
+
 __device__ __forceinline__ void fma16(v16f &acc, const v16f &c, const v16f &p) {
 #pragma unroll
   for (int v = 0; v < 16; v++) acc[v] = fmaf(c[v], p[v], acc[v]);
@@ -135,25 +142,26 @@ __device__ __forceinline__ const uint8_t *uniform_ptr(const uint8_t *p) {
   return reinterpret_cast<const uint8_t *>(((uint64_t)hi << 32) | lo);
 }
 
-// This wavefront's share of one K-group's loads: two 16-byte-per-lane wave
-// loads (item t reads b[t] + g * inc[t] + v[t] (lane)), and for wavefront 0 a
-// third one, the scales of the group: lane l reads 16 bytes at
-// s3[l] + g * inc3[l].
+// This wavefront's share of one 64-wide K block's loads: two
+// 16-byte-per-lane wave loads (item t reads b[t] + g * inc[t] + v[t] (lane)),
+// and for wavefront 0 a third one, the scales of the block's quantization
+// group (GK blocks per group): lane l reads 16 bytes at s3[l] + (g / GK) * inc3[l].
 struct PPlan {
   const uint8_t *b1, *b2;     // wave-uniform bases of group 0
   uint32_t inc1, inc2;        // bytes per K-group
   uint32_t v1, v2;            // lane offsets
   uint32_t l1, l2;            // LDS offsets within a slot
   const uint8_t *s3;          // lane address of group 0 (wavefront 0)
-  uint32_t inc3;              // lane bytes per K-group
+  uint32_t inc3;              // lane bytes per quantization group
 };
 
+template <int GK>
 __device__ __forceinline__ void p_issue(const PPlan &P, bool three, int g, uint32_t slot_lds) {
-  // the bases are wave-uniform (scalar registers): the group offset is added
+  // the bases are wave-uniform (scalar registers): the block offset is added
   // with scalar instructions
   dma_s(P.v1, P.b1 + (uint32_t)g * P.inc1, slot_lds + P.l1);
   dma_s(P.v2, P.b2 + (uint32_t)g * P.inc2, slot_lds + P.l2);
-  if (three) dma_v(P.s3 + (uint64_t)g * P.inc3, slot_lds + P_SW);
+  if (three) dma_v(P.s3 + (uint64_t)(g / GK) * P.inc3, slot_lds + P_SW);
 }
 
 // activation tile t of the block (clamped to the last tile): its group-0
@@ -200,14 +208,16 @@ __device__ __forceinline__ void plan_main(const GemmArgs &a, int lane, int wave,
 constexpr int H_S = P_SW;
 
 struct HPlan {
-  const uint8_t *base[2];   // lane addresses for group 0
-  uint32_t stride[2];       // lane bytes per group
+  const uint8_t *base[2];   // lane addresses for block 0
+  uint32_t stride[2];       // lane bytes per block (codes) or per quantization group (scales)
   uint32_t lds[2];          // wave-uniform LDS offset within a slot
+  int shift[2];             // block index >> shift: 0 for codes, log2(GK) for scales
 };
 
 __device__ __forceinline__ void h_issue(const HPlan &P, int g, uint32_t slot_lds) {
 #pragma unroll
-  for (int t = 0; t < 2; t++) dma_v(P.base[t] + (uint64_t)g * P.stride[t], slot_lds + P.lds[t]);
+  for (int t = 0; t < 2; t++)
+    dma_v(P.base[t] + (uint64_t)(g >> P.shift[t]) * P.stride[t], slot_lds + P.lds[t]);
 }
 
 // items, in order: the 8 activation halves, RT L1 tiles, one scale item, then
@@ -222,6 +232,7 @@ __device__ __forceinline__ void plan_h(const GemmArgs &a, int lane, int wave, in
   for (int t = 0; t < 2; t++) {
     int it = wave + 8 * t;
     if (it >= nitem) it -= 8;   // a repeat of item it - 8
+    P.shift[t] = 0;
     if (it < 8) {               // half it % 2 of activation tile it / 2
       P.base[t] = act_tile(a, m0, it >> 1) + (it & 1) * 1024 + lane * 16;
       P.stride[t] = 2048;
@@ -240,6 +251,7 @@ __device__ __forceinline__ void plan_h(const GemmArgs &a, int lane, int wave, in
         P.base[t] = a.packed + geo.off_l1s + (int64_t)min(8 * r, geo.r_pad32 - 8) * 2;
         P.stride[t] = (uint32_t)geo.r_pad32 * 2;
       }
+      P.shift[t] = geo.gk - 1;   // one scale row per quantization group
       P.lds[t] = H_S;
     }
   }
@@ -309,16 +321,25 @@ struct PKernel {
   // last group into a free slot.
   // (THREE: this wavefront also loads the scales, three loads per group; a
   // template parameter, so that the loop body is one basic block)
-  template <bool GA, bool THREE, typename Pre>
+  //
+  // 128-wide quantization groups (GK = 2): the ring still moves one 64-wide
+  // block per step, and the steps go in pairs.  X of a group's first block
+  // issues its four code products and holds them; X of the second adds the
+  // second block's code products to them in the matrix core (the exact
+  // integer sum of the whole group) and issues the group's four scale
+  // products; only the second block's Y applies fmas.  Every wait and barrier
+  // is the same per block as for 64-wide groups.
+  template <bool GA, bool THREE, int GK, typename Pre>
   __device__ __forceinline__ static void main_loop_pp(const PPlan &P, uint8_t *smem,
                                                       uint32_t ring_lds, int KG, int lane, int wr,
                                                       int wc, v16f (&acc)[2][2], Pre pre) {
     static_assert(D >= 4, "the hand-over keeps D - 3 groups of loads in flight");
-    constexpr int L = THREE ? 3 : 2;   // loads per group
+    static_assert(GK == 1 || GK == 2, "64- or 128-wide quantization groups");
+    constexpr int L = THREE ? 3 : 2;   // loads per block
     wait_vm<0>();
     pre();
 #pragma unroll
-    for (int s = 0; s < D; s++) p_issue(P, THREE, min(s, KG - 1), ring_lds + s * C::STAGE);
+    for (int s = 0; s < D; s++) p_issue<GK>(P, THREE, min(s, KG - 1), ring_lds + s * C::STAGE);
     wait_vm<L * (D - 3)>();
     __syncthreads();
     const RawOff ro = raw_off(lane, wr, wc);
@@ -331,59 +352,103 @@ struct PKernel {
       wait_lgkm0();
       __syncthreads();
     };
-    // The slots read and loaded in Y(g) advance one slot per group
-    // (wave-uniform; no division in the loop): the read slot holds group
-    // min(g + 1, KG - 1), the load slot (an LDS address) receives group
+    // The slots read and loaded in Y(g) advance one slot per block
+    // (wave-uniform; no division in the loop): the read slot holds block
+    // min(g + 1, KG - 1), the load slot (an LDS address) receives block
     // g + D (A) or g + D - 1 (B).
     uint32_t ring0 = ring_lds;
     asm volatile("" : "+s"(ring0));   // a plain scalar from here on
     const uint32_t ring_end = ring0 + C::RING;
     uint32_t rd_off = (uint32_t)(min(1, KG - 1) * C::STAGE);
     uint32_t ld_lds = ring0 + (GA ? 0u : (uint32_t)((D - 1) * C::STAGE));
-    for (int g = 0; g < KG; g++) {
-      // ---- X(g) ----
+    // Y(g)'s reads and loads: block g + 1's operands into the registers X(g)
+    // read (past the last block: the last block again, never used), and this
+    // wavefront's loads of a later block into a free slot (B at g = 0: block
+    // D - 1 again, the same bytes to the same place)
+    auto y_reads = [&](int g) {
+      read_raw(smem + rd_off, ro, R);
+      const uint32_t nx = rd_off + C::STAGE == (uint32_t)C::RING ? 0u : rd_off + C::STAGE;
+      rd_off = g + 2 < KG ? nx : rd_off;
+      asm volatile("" ::: "memory");
+    };
+    auto y_loads = [&](int g) {
+      const int gl = GA ? g + D : g + D - 1;
+      p_issue<GK>(P, THREE, min(gl, KG - 1), ld_lds);
+      ld_lds += C::STAGE;
+      ld_lds = ld_lds == ring_end ? ring0 : ld_lds;
+    };
+    auto y_expand = [&]() {
+      wait_lgkm0();
+      b0 = unpack32(R.b[0]);
+      b1 = unpack32(R.b[1]);
+    };
+    for (int g = 0; g < KG; g += GK) {
+      v16f c00, c01, c10, c11;
+      if constexpr (GK == 2) {
+        // ---- X(g): the group's first block, held ----
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_setprio(1);
+        c00 = codes_half(R.a[0], b0);
+        c01 = codes_half(R.a[0], b1);
+        c10 = codes_half(R.a[1], b0);
+        c11 = codes_half(R.a[1], b1);
+        __builtin_amdgcn_s_setprio(0);
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (GA) hand_over();
+        __builtin_amdgcn_sched_barrier(0);
+        // ---- Y(g) ----
+        y_reads(g);
+        __builtin_amdgcn_sched_barrier(0);
+        y_loads(g);
+        __builtin_amdgcn_sched_barrier(0);
+        y_expand();
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (!GA) hand_over();
+      }
+      const int gb = g + GK - 1;   // the group's last block
+      // ---- X(gb) ----
       __builtin_amdgcn_sched_barrier(0);
       __builtin_amdgcn_s_setprio(1);
-      const v16f c00 = codes_half(R.a[0], b0);
+      if constexpr (GK == 2) {
+        c00 = codes_half_acc(R.a[0], b0, c00);
+      } else {
+        c00 = codes_half(R.a[0], b0);
+      }
       const v16f p00 = outer2(R.sa[0], R.sb[0]);
-      const v16f c01 = codes_half(R.a[0], b1);
+      if constexpr (GK == 2) {
+        c01 = codes_half_acc(R.a[0], b1, c01);
+      } else {
+        c01 = codes_half(R.a[0], b1);
+      }
       const v16f p01 = outer2(R.sa[0], R.sb[1]);
-      const v16f c10 = codes_half(R.a[1], b0);
+      if constexpr (GK == 2) {
+        c10 = codes_half_acc(R.a[1], b0, c10);
+      } else {
+        c10 = codes_half(R.a[1], b0);
+      }
       const v16f p10 = outer2(R.sa[1], R.sb[0]);
-      const v16f c11 = codes_half(R.a[1], b1);
+      if constexpr (GK == 2) {
+        c11 = codes_half_acc(R.a[1], b1, c11);
+      } else {
+        c11 = codes_half(R.a[1], b1);
+      }
       const v16f p11 = outer2(R.sa[1], R.sb[1]);
       __builtin_amdgcn_s_setprio(0);
       __builtin_amdgcn_sched_barrier(0);
       if constexpr (GA) hand_over();
       __builtin_amdgcn_sched_barrier(0);
-      // ---- Y(g) ----
-      // group g + 1's operands into the registers X(g) read (past the last
-      // group: the last group again, never used)
-      read_raw(smem + rd_off, ro, R);
-      {
-        const uint32_t nx = rd_off + C::STAGE == (uint32_t)C::RING ? 0u : rd_off + C::STAGE;
-        rd_off = g + 2 < KG ? nx : rd_off;
-      }
-      asm volatile("" ::: "memory");
+      // ---- Y(gb) ----
+      y_reads(gb);
       __builtin_amdgcn_sched_barrier(0);
       fma16(acc[0][0], c00, p00);
       fma16(acc[0][1], c01, p01);
       __builtin_amdgcn_sched_barrier(0);
-      {
-        // this wavefront's loads of a later group into a free slot (B at g = 0:
-        // group D - 1 again, the same bytes to the same place)
-        const int gl = GA ? g + D : g + D - 1;
-        p_issue(P, THREE, min(gl, KG - 1), ld_lds);
-        ld_lds += C::STAGE;
-        ld_lds = ld_lds == ring_end ? ring0 : ld_lds;
-      }
+      y_loads(gb);
       __builtin_amdgcn_sched_barrier(0);
       fma16(acc[1][0], c10, p10);
       fma16(acc[1][1], c11, p11);
       __builtin_amdgcn_sched_barrier(0);
-      wait_lgkm0();
-      b0 = unpack32(R.b[0]);
-      b1 = unpack32(R.b[1]);
+      y_expand();
       __builtin_amdgcn_sched_barrier(0);
       if constexpr (!GA) hand_over();
     }
@@ -391,8 +456,11 @@ struct PKernel {
   }
 
   // The stage-1 pass: H tiles of 32 tokens x 32 ranks, accumulated over all
-  // K-groups in ascending order (token tile ti, rank tiles hrt[]), one group
-  // per ring slot and step.
+  // K-groups in ascending order (token tile ti, rank tiles hrt[]), one 64-wide
+  // block per ring slot and step; a 128-wide group (GK = 2) adds its second
+  // block's code products to its first's in the matrix core before its one
+  // scale product.
+  template <int GK>
   __device__ __forceinline__ static void h_loop(const HPlan &P, uint8_t *smem, uint32_t ring_lds,
                                                 int KG, int lane, bool hw, int ti,
                                                 const int (&hrt)[C::HT], v16f (&hacc)[C::HT]) {
@@ -402,32 +470,41 @@ struct PKernel {
     wait_vm<2 * (D - 1)>();
     __syncthreads();
     const int l32 = lane & 31;
-    for (int s = 0; s < KG; s++) {
-      const uint8_t *S = smem + (s % D) * C::STAGE;
-      v8i ra = v8i{0};
-      u32x4 rl[C::HT];
-      uint32_t sa = 0, sl[C::HT];
-      if (hw) {
-        ra = join(*reinterpret_cast<const u32x4 *>(S + P_A + ti * 2048 + lane * 16),
-                  *reinterpret_cast<const u32x4 *>(S + P_A + ti * 2048 + 1024 + lane * 16));
-        sa = *reinterpret_cast<const uint16_t *>(S + H_S + (32 * ti + l32) * 2);
+    for (int s0 = 0; s0 < KG; s0 += GK) {
+      v16f hc[C::HT];
 #pragma unroll
-        for (int h = 0; h < C::HT; h++) {
-          rl[h] = *reinterpret_cast<const u32x4 *>(S + P_B + 1024 * hrt[h] + lane * 16);
-          sl[h] = *reinterpret_cast<const uint16_t *>(S + H_S + 256 + (32 * hrt[h] + l32) * 2);
+      for (int u = 0; u < GK; u++) {
+        const int s = s0 + u;
+        const uint8_t *S = smem + (s % D) * C::STAGE;
+        v8i ra = v8i{0};
+        u32x4 rl[C::HT];
+        uint32_t sa = 0, sl[C::HT];
+        if (hw) {
+          ra = join(*reinterpret_cast<const u32x4 *>(S + P_A + ti * 2048 + lane * 16),
+                    *reinterpret_cast<const u32x4 *>(S + P_A + ti * 2048 + 1024 + lane * 16));
+          sa = *reinterpret_cast<const uint16_t *>(S + H_S + (32 * ti + l32) * 2);
+#pragma unroll
+          for (int h = 0; h < C::HT; h++) {
+            rl[h] = *reinterpret_cast<const u32x4 *>(S + P_B + 1024 * hrt[h] + lane * 16);
+            sl[h] = *reinterpret_cast<const uint16_t *>(S + H_S + 256 + (32 * hrt[h] + l32) * 2);
+          }
         }
-      }
-      // group s + 1 has landed and every wavefront is done with slot s
-      wait_vm<2 * (D - 2)>();
-      wait_lgkm0();
-      __syncthreads();
-      h_issue(P, min(s + D, KG - 1), ring_lds + (s % D) * C::STAGE);
-      if (hw) {
+        // block s + 1 has landed and every wavefront is done with slot s
+        wait_vm<2 * (D - 2)>();
+        wait_lgkm0();
+        __syncthreads();
+        h_issue(P, min(s + D, KG - 1), ring_lds + (s % D) * C::STAGE);
+        if (hw) {
 #pragma unroll
-        for (int h = 0; h < C::HT; h++) {
-          const v16f ch = codes_half(ra, unpack32(rl[h]));
-          const v16f ph = outer2(sa, sl[h]);
-          fma16(hacc[h], ch, ph);
+          for (int h = 0; h < C::HT; h++) {
+            const v8i lb = unpack32(rl[h]);
+            if (u == 0) {
+              hc[h] = codes_half(ra, lb);
+            } else {
+              hc[h] = codes_half_acc(ra, lb, hc[h]);
+            }
+            if (u == GK - 1) fma16(hacc[h], hc[h], outer2(sa, sl[h]));
+          }
         }
       }
     }
@@ -435,12 +512,16 @@ struct PKernel {
   }
 };
 
-template <int RT, int D>
+template <int RT, int D, int GK>
 __global__ __launch_bounds__(64 * PNW, 1) void dual_gemm_prefill_kernel(GemmArgs a, int m_tiles,
                                                                         int n_tiles, int n_chunks,
                                                                         int cpw, int band) {
   using K = PKernel<RT, D>;
   using C = PCfg<RT, D>;
+  // 64-rank blocks per rank group (a 128-rank group in 128-wide groups: 2)
+  // and rank groups
+  constexpr int BPG = GK == 2 && C::RB == 2 ? 2 : 1;
+  constexpr int RG = C::RB / BPG;
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
   const Geometry &geo = a.geo;
   const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31;
@@ -491,7 +572,7 @@ __global__ __launch_bounds__(64 * PNW, 1) void dual_gemm_prefill_kernel(GemmArgs
         v16f hacc[C::HT];
 #pragma unroll
         for (int h = 0; h < C::HT; h++) hacc[h] = v16f{0};
-        K::h_loop(HP, smem, ring_lds, KG, lane, hw, hti, hrt, hacc);
+        K::template h_loop<GK>(HP, smem, ring_lds, KG, lane, hw, hti, hrt, hacc);
         __syncthreads();   // every wavefront is done with the ring
         float *HS = reinterpret_cast<float *>(smem);
         uint8_t *QS = smem + C::OFF_Q;
@@ -584,19 +665,19 @@ __global__ __launch_bounds__(64 * PNW, 1) void dual_gemm_prefill_kernel(GemmArgs
             dma_s(lane * 16, uniform_ptr(l2codes + ((int64_t)ct * C::RB + rbk) * 1024),
                   l2_lds + (j * C::RB + rbk) * 1024);
         }
-        // lane q < 8 RB: 8 scales of column tile j = q / (4 RB), rank group
-        // (q / 4) % RB, columns 8 (q % 4) .. + 8
-        const int q = lane & (8 * C::RB - 1);
-        const int jj = q / (4 * C::RB), rbk = (q / 4) % C::RB;
+        // lane q < 8 RG: 8 scales of column tile j = q / (4 RG), rank group
+        // (q / 4) % RG, columns 8 (q % 4) .. + 8
+        const int q = lane & (8 * RG - 1);
+        const int jj = q / (4 * RG), hg = (q / 4) % RG;
         const int ct = min(n0 / 32 + 2 * wc + jj, ctiles - 1);
-        dma_v(reinterpret_cast<const uint8_t *>(l2scales + (int64_t)rbk * geo.n_pad + ct * 32 +
+        dma_v(reinterpret_cast<const uint8_t *>(l2scales + (int64_t)hg * geo.n_pad + ct * 32 +
                                                 8 * (q & 3)),
               l2_lds + 2 * C::RB * 1024);
       }
     };
-    if (wave == 0) K::template main_loop_pp<true, true>(P, smem, ring_lds, KG, lane, wr, wc, acc, pre);
-    else if (wr == 0) K::template main_loop_pp<true, false>(P, smem, ring_lds, KG, lane, wr, wc, acc, pre);
-    else K::template main_loop_pp<false, false>(P, smem, ring_lds, KG, lane, wr, wc, acc, pre);
+    if (wave == 0) K::template main_loop_pp<true, true, GK>(P, smem, ring_lds, KG, lane, wr, wc, acc, pre);
+    else if (wr == 0) K::template main_loop_pp<true, false, GK>(P, smem, ring_lds, KG, lane, wr, wc, acc, pre);
+    else K::template main_loop_pp<false, false, GK>(P, smem, ring_lds, KG, lane, wr, wc, acc, pre);
 
     // ---- stage 2 (Q_H Q(L2)) and the single epilogue ----
     // (the index values are re-derived here, behind an opaque copy, so the
@@ -615,18 +696,29 @@ __global__ __launch_bounds__(64 * PNW, 1) void dual_gemm_prefill_kernel(GemmArgs
         if constexpr (RT > 0) {
           const uint8_t *QS = smem + C::OFF_Q;
           const float *SHS = reinterpret_cast<const float *>(smem + C::OFF_SH);
+          const uint8_t *L2S = smem + C::OFF_L2 + wc * C::L2W;
+          // one rescale per rank group: a 128-rank group first adds its two
+          // 64-rank blocks' exact integer sums in the matrix core
 #pragma unroll
-          for (int rbk = 0; rbk < C::RB; rbk++) {
-            const uint8_t *qrow = QS + (32 * ti + l32e) * C::QSTR + rbk * 64 + (lane_e >> 5) * 32;
-            const v8i qa = join(*reinterpret_cast<const u32x4 *>(qrow),
-                                *reinterpret_cast<const u32x4 *>(qrow + 16));
-            const uint8_t *L2S = smem + C::OFF_L2 + wc * C::L2W;
-            const v8i lb = unpack32(*reinterpret_cast<const u32x4 *>(
-                L2S + (j * C::RB + rbk) * 1024 + lane_e * 16));
+          for (int hg = 0; hg < RG; hg++) {
+            v16f cbv;
+#pragma unroll
+            for (int bb = 0; bb < BPG; bb++) {
+              const int rbk = hg * BPG + bb;
+              const uint8_t *qrow = QS + (32 * ti + l32e) * C::QSTR + rbk * 64 + (lane_e >> 5) * 32;
+              const v8i qa = join(*reinterpret_cast<const u32x4 *>(qrow),
+                                  *reinterpret_cast<const u32x4 *>(qrow + 16));
+              const v8i lb = unpack32(*reinterpret_cast<const u32x4 *>(
+                  L2S + (j * C::RB + rbk) * 1024 + lane_e * 16));
+              if (bb == 0) {
+                cbv = mfma_codes_32x32x64(qa, lb);
+              } else {
+                cbv = mfma_codes_32x32x64_acc(qa, lb, cbv);
+              }
+            }
             const float sl2 = half_bits_to_float(*reinterpret_cast<const uint16_t *>(
-                L2S + 2 * C::RB * 1024 + ((j * C::RB + rbk) * 32 + l32e) * 2));
-            const v16f cbv = mfma_codes_32x32x64(qa, lb);
-            const float *shrow = SHS + rbk * PBM + 32 * ti + 4 * (lane_e >> 5);
+                L2S + 2 * C::RB * 1024 + ((j * RG + hg) * 32 + l32e) * 2));
+            const float *shrow = SHS + hg * PBM + 32 * ti + 4 * (lane_e >> 5);
 #pragma unroll
             for (int q = 0; q < 4; q++) {
               const v4f sh4 = *reinterpret_cast<const v4f *>(shrow + 8 * q);
@@ -660,7 +752,7 @@ __global__ __launch_bounds__(64 * PNW, 1) void dual_gemm_prefill_kernel(GemmArgs
   }
 }
 
-template <int RT, int D>
+template <int RT, int D, int GK>
 hipError_t launch_prefill(const GemmArgs &a, hipStream_t s) {
   using C = PCfg<RT, D>;
   const int m_tiles = (a.m + PBM - 1) / PBM;
@@ -673,7 +765,7 @@ hipError_t launch_prefill(const GemmArgs &a, hipStream_t s) {
   if (cpw > n_tiles) cpw = n_tiles;
   const int n_chunks = (n_tiles + cpw - 1) / cpw;
   const int band = m_tiles < 8 ? m_tiles : 8;   // token blocks per band of the XCD order
-  auto kern = dual_gemm_prefill_kernel<RT, D>;
+  auto kern = dual_gemm_prefill_kernel<RT, D, GK>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
   if (e != hipSuccess) return e;
@@ -682,13 +774,13 @@ hipError_t launch_prefill(const GemmArgs &a, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int D>
+template <int D, int GK>
 hipError_t launch_prefill_rt(const GemmArgs &a, hipStream_t s) {
   switch (a.geo.r_pad32 / 32) {
-    case 0: return launch_prefill<0, D>(a, s);
-    case 1: return launch_prefill<1, D>(a, s);
-    case 2: return launch_prefill<2, D>(a, s);
-    case 4: return launch_prefill<4, D - 1>(a, s);   // the larger Q_H and stage-2 region leave D - 1 slots
+    case 0: return launch_prefill<0, D, GK>(a, s);
+    case 1: return launch_prefill<1, D, GK>(a, s);
+    case 2: return launch_prefill<2, D, GK>(a, s);
+    case 4: return launch_prefill<4, D - 1, GK>(a, s);   // the larger Q_H and stage-2 region leave D - 1 slots
     default: return hipErrorInvalidValue;
   }
 }
@@ -696,7 +788,11 @@ hipError_t launch_prefill_rt(const GemmArgs &a, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_dual_gemm_prefill(const GemmArgs &a, hipStream_t s) {
-  return launch_prefill_rt<8>(a, s);
+  switch (a.geo.gk) {
+    case 1: return launch_prefill_rt<8, 1>(a, s);
+    case 2: return launch_prefill_rt<8, 2>(a, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace tq

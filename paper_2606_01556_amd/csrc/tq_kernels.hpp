@@ -75,8 +75,6 @@ bool decode_fits(int m, int k);
 // the kernel launch_dual_gemm runs (values of tq_kernel in the C header)
 constexpr int kKernelDecode = 0, kKernelMid = 1, kKernelLarge = 2, kKernelPrefill = 3;
 int choose_kernel(const GemmArgs &a);
-// whether a kernel takes quantization groups of gk 64-wide blocks
-bool serves_group(int kernel, int gk);
 hipError_t launch_dual_gemm_mid(const GemmArgs &a, hipStream_t s);      // mid sizes
 // relative time of the mid kernel's launch: rounds of work-groups over the
 // CUs x tile-groups per work-group and chunk (+3 for its fixed latency)

@@ -284,8 +284,9 @@ def test_kernel_choice(L):
     activation codes fit its LDS), the mid kernel up to 512, past that the
     large kernel where its 128 x 256 blocks fill the CUs, the mid kernel where
     they would leave most CUs idle, the prefill kernel beyond one round of
-    blocks (for r <= 64 only where a work-group's run of column blocks spans
-    at least 256 K-groups); -1 for a bad descriptor or m."""
+    blocks (for r <= 64 in 64-wide groups only where a work-group's run of
+    column blocks spans at least 256 K-groups; in 128-wide groups at every
+    rank but 0); -1 for a bad descriptor or m."""
     d = tq.weight_desc_init(4096, 4096, 64)           # n, k, r
     assert [tq.dual_gemm_kernel(d, m) for m in (1, 16, 17, 512, 2048)] == \
         ["decode", "decode", "mid", "mid", "large"]
@@ -296,6 +297,12 @@ def test_kernel_choice(L):
     assert tq.dual_gemm_kernel(tq.weight_desc_init(14336, 4096, 64), 4096) == "prefill"
     assert tq.dual_gemm_kernel(tq.weight_desc_init(4096, 4096, 64), 4096) == "large"
     assert tq.dual_gemm_kernel(tq.weight_desc_init(4096, 14336, 64), 4096) == "prefill"
+    # 128-wide groups: past one round of blocks the prefill kernel unless r = 0
+    assert tq.dual_gemm_kernel(tq.weight_desc_init(4096, 4096, 64, 128), 4096) == "prefill"
+    assert tq.dual_gemm_kernel(tq.weight_desc_init(4096, 4096, 16, 128), 4096) == "prefill"
+    assert tq.dual_gemm_kernel(tq.weight_desc_init(4096, 4096, 0, 128), 4096) == "large"
+    assert tq.dual_gemm_kernel(tq.weight_desc_init(4096, 4096, 128, 128), 2048) == "large"
+    assert tq.dual_gemm_kernel(tq.weight_desc_init(28672, 8192, 128, 128), 8192) == "prefill"
     assert tq.dual_gemm_kernel(tq.weight_desc_init(8192, 28672, 128), 1) == "decode"
     assert tq.dual_gemm_kernel(tq.weight_desc_init(8192, 28672, 128), 8) == "decode"
     assert tq.dual_gemm_kernel(tq.weight_desc_init(8192, 28672, 128), 9) == "mid"

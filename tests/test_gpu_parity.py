@@ -587,18 +587,17 @@ def test_group128_bf16(oracle_mod, M):
     full_parity(oracle_mod, d["X"], d["W_res"], d["L1"], d["L2"], bf16=True, group=128)
 
 
-def test_group128_rejects_prefill():
-    """The prefill kernel takes 64-wide groups only: forcing it on a 128-wide
-    layer is an argument error, and the dispatch never picks it."""
-    d = random_codes_layer(600, 256, 64, 128, seed=1)
-    lay = tq.Layer(dev(d["W_res"]), dev(d["L1"]), dev(d["L2"]), group=128)
-    for m in (600, 4096, 8192, 65536):
-        assert tq.dual_gemm_kernel(lay.desc, m) != "prefill"
-    xc, xs = tq.empty_act(600, 256, group=128)
-    tq.quant_act(dev(d["X"]), xc, xs, 128)
-    y = torch.empty((600, 64), dtype=torch.float16, device="cuda")
-    with pytest.raises(tq.TQError):
-        tq.dual_gemm_debug(lay.desc, lay.packed, xc, xs, 600, y, kernel="prefill")
+@pytest.mark.parametrize("M,K,N,r", [(600, 1024, 256, 128), (700, 512, 300, 64), (520, 384, 96, 16),
+                                     (1030, 2048, 512, 128), (600, 256, 64, 0), (777, 640, 130, 32),
+                                     (640, 128, 600, 128), (530, 384, 4096, 128)])
+def test_group128_prefill(oracle_mod, M, K, N, r):
+    """The prefill kernel on 128-wide groups (the ring's 64-wide blocks taken
+    in pairs, a 128-rank group's two blocks summed in the matrix core): Y
+    bit-exact, H, s_H and Q_H too; a single group (K = 128), odd group counts,
+    ragged tokens and columns, every rank-tile count."""
+    say(f"group 128 prefill M={M} K={K} N={N} r={r}")
+    d = random_codes_layer(M, K, N, r, seed=7 * M + r)
+    full_parity(oracle_mod, d["X"], d["W_res"], d["L1"], d["L2"], kernel="prefill", group=128)
 
 
 @pytest.mark.parametrize("M,K,N,r,group", [(5, 256, 96, 64, 64), (600, 384, 64, 128, 128),
