@@ -301,10 +301,12 @@ struct PKernel {
   // SIMD run out of step, so that one issues matrix-core work while the other
   // issues vector work:
   //   X(g): the eight matrix-core products of group g (code and scale products
-  //         of tiles 00, 01, 10, 11);
+  //         of tiles 00, 01, 10, 11), with this wavefront's loads of a later
+  //         group interleaved between them (their scalar address arithmetic
+  //         issues while the matrix core works);
   //   Y(g): the LDS reads of group g + 1, the 64 rescaling fmas of group g (on
-  //         products that X(g) has finished), this wavefront's loads of a later
-  //         group and the expansion of the weight operands of group g + 1.
+  //         products that X(g) has finished) and the expansion of the weight
+  //         operands of group g + 1.
   // Every wavefront runs X(0) Y(0) X(1) Y(1) ... with one workgroup barrier per
   // group, placed after X(g) on wavefronts 0-3 (GA) and after Y(g) on
   // wavefronts 4-7 (each SIMD holds one of each), so between barriers k - 1 and
@@ -314,10 +316,10 @@ struct PKernel {
   // the barrier that opens it must publish groups <= k + 1; slot s is free
   // once both readers of its group have passed the barrier after their reads.
   // Each wavefront issues its loads of group k + D - 1 into slot (k - 1) % D
-  // during interval k (A from Y(k - 1), B from Y(k)), and before barrier k
+  // in X(k), which lies in interval k for A and B alike, and before barrier k
   // waits until only its loads of groups k + 3 .. k + D - 1 may be in flight
   // (D - 3 groups), so groups <= k + 2 are complete when barrier k opens.  The
-  // prologue loads groups 0 .. D - 1; loads past the last group repeat the
+  // prologue loads groups 0 .. D - 2; loads past the last group repeat the
   // last group into a free slot.
   // (THREE: this wavefront also loads the scales, three loads per group; a
   // template parameter, so that the loop body is one basic block)
@@ -339,7 +341,7 @@ struct PKernel {
     wait_vm<0>();
     pre();
 #pragma unroll
-    for (int s = 0; s < D; s++) p_issue<GK>(P, THREE, min(s, KG - 1), ring_lds + s * C::STAGE);
+    for (int s = 0; s < D - 1; s++) p_issue<GK>(P, THREE, min(s, KG - 1), ring_lds + s * C::STAGE);
     wait_vm<L * (D - 3)>();
     __syncthreads();
     const RawOff ro = raw_off(lane, wr, wc);
@@ -352,28 +354,26 @@ struct PKernel {
       wait_lgkm0();
       __syncthreads();
     };
-    // The slots read and loaded in Y(g) advance one slot per block
+    // The slots read in Y(g) and loaded in X(g) advance one slot per block
     // (wave-uniform; no division in the loop): the read slot holds block
     // min(g + 1, KG - 1), the load slot (an LDS address) receives block
-    // g + D (A) or g + D - 1 (B).
+    // g + D - 1.
     uint32_t ring0 = ring_lds;
     asm volatile("" : "+s"(ring0));   // a plain scalar from here on
     const uint32_t ring_end = ring0 + C::RING;
     uint32_t rd_off = (uint32_t)(min(1, KG - 1) * C::STAGE);
-    uint32_t ld_lds = ring0 + (GA ? 0u : (uint32_t)((D - 1) * C::STAGE));
-    // Y(g)'s reads and loads: block g + 1's operands into the registers X(g)
-    // read (past the last block: the last block again, never used), and this
-    // wavefront's loads of a later block into a free slot (B at g = 0: block
-    // D - 1 again, the same bytes to the same place)
+    uint32_t ld_lds = ring0 + (uint32_t)((D - 1) * C::STAGE);
+    // Y(g)'s reads: block g + 1's operands into the registers X(g) read (past
+    // the last block: the last block again, never used); X(g)'s loads: this
+    // wavefront's share of block g + D - 1 into the slot that block g - 1 left
     auto y_reads = [&](int g) {
       read_raw(smem + rd_off, ro, R);
       const uint32_t nx = rd_off + C::STAGE == (uint32_t)C::RING ? 0u : rd_off + C::STAGE;
       rd_off = g + 2 < KG ? nx : rd_off;
       asm volatile("" ::: "memory");
     };
-    auto y_loads = [&](int g) {
-      const int gl = GA ? g + D : g + D - 1;
-      p_issue<GK>(P, THREE, min(gl, KG - 1), ld_lds);
+    auto x_loads = [&](int g) {
+      p_issue<GK>(P, THREE, min(g + D - 1, KG - 1), ld_lds);
       ld_lds += C::STAGE;
       ld_lds = ld_lds == ring_end ? ring0 : ld_lds;
     };
@@ -392,14 +392,21 @@ struct PKernel {
         c01 = codes_half(R.a[0], b1);
         c10 = codes_half(R.a[1], b0);
         c11 = codes_half(R.a[1], b1);
+        x_loads(g);
+#pragma unroll
+        for (int i = 0; i < 4; i++) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x004, 6, 0);
+          __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
         __builtin_amdgcn_s_setprio(0);
         __builtin_amdgcn_sched_barrier(0);
         if constexpr (GA) hand_over();
         __builtin_amdgcn_sched_barrier(0);
         // ---- Y(g) ----
         y_reads(g);
-        __builtin_amdgcn_sched_barrier(0);
-        y_loads(g);
         __builtin_amdgcn_sched_barrier(0);
         y_expand();
         __builtin_amdgcn_sched_barrier(0);
@@ -433,6 +440,17 @@ struct PKernel {
         c11 = codes_half(R.a[1], b1);
       }
       const v16f p11 = outer2(R.sa[1], R.sb[1]);
+      x_loads(gb);
+      // one product, then a few of the loads' scalar, memory and address
+      // instructions, in the shadow of the product
+#pragma unroll
+      for (int i = 0; i < 8; i++) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x004, 3, 0);
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
       __builtin_amdgcn_s_setprio(0);
       __builtin_amdgcn_sched_barrier(0);
       if constexpr (GA) hand_over();
@@ -442,8 +460,6 @@ struct PKernel {
       __builtin_amdgcn_sched_barrier(0);
       fma16(acc[0][0], c00, p00);
       fma16(acc[0][1], c01, p01);
-      __builtin_amdgcn_sched_barrier(0);
-      y_loads(gb);
       __builtin_amdgcn_sched_barrier(0);
       fma16(acc[1][0], c10, p10);
       fma16(acc[1][1], c11, p11);
