@@ -157,7 +157,9 @@ struct ResSlot {
   uint32_t swa[CTW], swb[CTW];   // fp16 weight scales (TOK8: the lane's own group in swa)
 };
 
-template <int MODE, int CT, bool FQ>
+// GK: 64-wide K blocks per quantization group (1 or 2, the layer's geo.gk),
+// or 0: read from geo.gk at run time
+template <int MODE, int CT, bool FQ, int GK>
 __global__ __launch_bounds__(64 * DW) void dual_gemm_decode_kernel(GemmArgs a,
                                                                    const uint16_t *__restrict__ xh) {
   using MD = DMode<MODE>;
@@ -213,7 +215,7 @@ __global__ __launch_bounds__(64 * DW) void dual_gemm_decode_kernel(GemmArgs a,
   // Scale rows: one per quantization group, so a pair of 64-wide blocks spans
   // two rows (64-wide groups) or one (128-wide groups, gk = 2), and group B's
   // row is the next one or the same.
-  const int gk = geo.gk;
+  const int gk = GK ? GK : geo.gk;
   const uint32_t l1s_pair = (uint32_t)geo.r_pad32 * 4 / gk, ws_pair = (uint32_t)geo.n_pad * 4 / gk;
   const uint32_t l1s_b = gk == 1 ? (uint32_t)geo.r_pad32 * 2 : 0u, ws_b = gk == 1 ? (uint32_t)geo.n_pad * 2 : 0u;
   const uint8_t *l1sb = reinterpret_cast<const uint8_t *>(l1scales);
@@ -412,12 +414,21 @@ __global__ __launch_bounds__(64 * DW) void dual_gemm_decode_kernel(GemmArgs a,
 #pragma unroll
     for (int v = 0; v < MV; v++) {
       const float ib = MD::TOK8 ? upper_half(P.I[v]) : P.I2[v];
-      // a 128-wide group: its two halves' sums add exactly (|I| < 2^13) and
-      // the second step adds +0, which leaves the (never negative-zero) h as is
-      const float i1 = gk == 2 ? P.I[v] + ib : P.I[v];
-      const float i2 = gk == 2 ? 0.0f : ib;
-      hacc[v] = fmaf(i1 * P.sxa[v], (float)sla, hacc[v]);
-      hacc[v] = fmaf(i2 * P.sxb[v], (float)slb, hacc[v]);
+      if constexpr (GK == 2) {
+        // a 128-wide group: its two halves' sums add exactly (|I| < 2^13)
+        // into the group's one step
+        hacc[v] = fmaf((P.I[v] + ib) * P.sxa[v], (float)sla, hacc[v]);
+      } else if constexpr (GK == 1) {
+        hacc[v] = fmaf(P.I[v] * P.sxa[v], (float)sla, hacc[v]);
+        hacc[v] = fmaf(ib * P.sxb[v], (float)slb, hacc[v]);
+      } else {
+        // the same, chosen at run time: for a 128-wide group the second step
+        // adds +0, which leaves the (never negative-zero) h as is
+        const float i1 = gk == 2 ? P.I[v] + ib : P.I[v];
+        const float i2 = gk == 2 ? 0.0f : ib;
+        hacc[v] = fmaf(i1 * P.sxa[v], (float)sla, hacc[v]);
+        hacc[v] = fmaf(i2 * P.sxb[v], (float)slb, hacc[v]);
+      }
     }
   };
   auto residual = [&](const ResSlot<CTW> &Sl, int p) {
@@ -457,18 +468,34 @@ __global__ __launch_bounds__(64 * DW) void dual_gemm_decode_kernel(GemmArgs a,
     // slot s holds pair i0 + s; it is refilled after pair i's chain step
     S1Lds lds2 = s1_lds(min(1, NP - 1));
     S1Prod prod = s1_mfma(s1_lds(0), S1[0]);
-    for (int i0 = 0; i0 < NP; i0 += D1) {
+    auto s1_step = [&](int i, int s) {
+      const S1Lds lds_next = s1_lds(min(i + 2, NP - 1));
+      const S1Prod prod_next = s1_mfma(lds2, S1[(s + 1) % D1]);
+      s1_chain(prod, S1[s]);
+      prod = prod_next;
+      lds2 = lds_next;
+    };
+    int i0 = 0;
+    if constexpr (MV <= 2) {
+      // whole rounds of the ring with no per-pair test, so that the
+      // pipeline's registers rotate by renaming inside a round (a per-pair
+      // test splits the round into blocks joined by register copies), then
+      // the last NP % D1 pairs.  (With four rows per lane the longer-lived
+      // operands do not fit 128 registers that way: those layouts keep the
+      // tested loop.)
+      for (; i0 + D1 <= NP; i0 += D1) {
+#pragma unroll
+        for (int s = 0; s < D1; s++) {
+          s1_step(i0 + s, s);
+          load_s1(S1[s], min(i0 + s + D1, NP - 1));
+        }
+      }
+    }
+    for (; i0 < NP; i0 += D1) {
 #pragma unroll
       for (int s = 0; s < D1; s++) {
-        const int i = i0 + s;
-        if (i < NP) {
-          const S1Lds lds_next = s1_lds(min(i + 2, NP - 1));
-          const S1Prod prod_next = s1_mfma(lds2, S1[(s + 1) % D1]);
-          s1_chain(prod, S1[s]);
-          prod = prod_next;
-          lds2 = lds_next;
-        }
-        load_s1(S1[s], min(i + D1, NP - 1));
+        if (i0 + s < NP) s1_step(i0 + s, s);
+        load_s1(S1[s], min(i0 + s + D1, NP - 1));
       }
     }
   } else {
@@ -630,7 +657,13 @@ template <int MODE, int CT, bool FQ>
 hipError_t launch_decode(const GemmArgs &a, const uint16_t *xh, hipStream_t s) {
   const DLayout LY = decode_layout<MODE, CT>(a.geo.k / kGroup, a.geo.r);
   const int tiles16 = a.geo.n_pad / 16;
-  auto kern = dual_gemm_decode_kernel<MODE, CT, FQ>;
+  if (a.geo.gk != 1 && a.geo.gk != 2) return hipErrorInvalidValue;
+  // the group width is a compile-time constant where the registers allow it
+  // (64-wide groups up to two rows per lane, 128-wide groups at one row): the
+  // chain then takes one or two steps per pair without a per-pair choice
+  constexpr int MV = DMode<MODE>::MV;
+  auto kern = a.geo.gk == 1 ? dual_gemm_decode_kernel<MODE, CT, FQ, MV <= 2 ? 1 : 0>
+                            : dual_gemm_decode_kernel<MODE, CT, FQ, MV == 1 ? 2 : 0>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, LY.total);
   if (e != hipSuccess) return e;
