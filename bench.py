@@ -595,6 +595,14 @@ def main_bench(args):
         # the paper's default configuration (group 128, rank 128) on the same shape
         L3 = LayerBench(wl2, wl2.layers[0], wl2.Ms, stream, group=128, rank=128)
         rows += detail_rows(L3, wl2.Ms, stream, DETAIL_EXTRA + "-g128-r128")
+        del L3
+        torch.cuda.empty_cache()
+        # and at the headline's prefill point (gate_up, r = 128, the largest M)
+        gate_up = [l for l in wl.layers if l.name == "gate_up"][0]
+        L4 = LayerBench(wl, gate_up, (max(HEAD_MS),), stream, group=128)
+        rows += detail_rows(L4, (max(HEAD_MS),), stream, HEADLINE + "-g128")
+        del L4
+        torch.cuda.empty_cache()
         out["per_m"] = rows
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(step_flops)
