@@ -444,6 +444,7 @@ def detail_rows(L, ms, stream, wl_name):
             tq.dual_gemm_unfused(L.desc, L.packed[i % L.ncopy], xc, xs, m, L.Y[m][i % len(L.Y[m])],
                                  scratch, stream=s)
 
+        timed(stream, lambda: L.call(m, s), reps)   # warm-up: the clocks after the host-side set-up
         us_layer = timed(stream, lambda: L.call(m, s), reps)
         us_two = timed(stream, lambda: L.call(m, s, fused_quant=False), reps)
         us_gemm = timed(stream, gemm, reps)
