@@ -189,14 +189,16 @@ def test_ragged_shapes(oracle_mod, M, K, N, r):
     (1, 4096, 64, 8), (1, 28672, 512, 128), (2, 320, 4096, 16), (2, 8256, 1000, 64),
     (3, 4160, 512, 64), (4, 128, 8192, 64), (7, 64, 8, 0), (8, 28672, 256, 128),
     (9, 192, 16384, 128), (12, 14336, 300, 32), (16, 64, 16416, 32), (16, 8256, 256, 128),
-    (1, 1984, 33000, 0), (5, 704, 20000, 64),
+    (1, 1984, 33000, 0), (5, 704, 20000, 64), (1, 2560, 512, 64), (2, 1280, 300, 128),
+    (1, 1152, 96, 16),
 ])
 def test_decode_kernel_variants(oracle_mod, M, K, N, r):
     """m <= 16 in every token layout of the decode kernel (one token, two,
     up to 8 with two K-groups per product, up to 16), with 1, 2, 4 and 8
     column tiles per work-group and more work-groups than CUs, odd K-group
-    counts, K at the largest size whose activation codes fit its LDS, and
-    every rank-tile count."""
+    counts, K at the largest size whose activation codes fit its LDS, every
+    rank-tile count, and stage-1 loops of whole ring rounds only (K-group
+    pairs a multiple of the ring depth of 10), with a tail, or a tail only."""
     say(f"decode M={M} K={K} N={N} r={r}")
     d = random_codes_layer(M, K, N, r, seed=N + r)
     g, _ = full_parity(oracle_mod, d["X"], d["W_res"], d["L1"], d["L2"])
