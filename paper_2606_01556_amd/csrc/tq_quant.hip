@@ -12,7 +12,8 @@ namespace tq {
 
 // ---------------------------------------------------------------------------
 // Activations: one work-group of 4 wavefronts per quantization group (GK
-// consecutive 1 KiB matrix-core blocks) of one token tile.  Wavefront
+// consecutive 1 KiB matrix-core blocks) of one token tile, or per QPW
+// consecutive groups (the fp8 output of 64-wide groups).  Wavefront
 // w takes tokens 8 w .. 8 w + 7 of the tile; for each of the GK blocks, lane
 // 8 j + 4 h + l quantizes codes 32 h + 8 l .. + 7 of the group for token
 // 8 w + j (16 bytes of the row) into one TQ4 word, and the 8 lanes of a token
@@ -31,59 +32,66 @@ namespace tq {
 // (max8_dpp and quant8_fp8, the per-lane quantizer step, are in tq_device.hpp:
 // the decode kernel quantizes fp16 activations with the same code.)
 
-template <bool FP8, int GK>
+template <bool FP8, int GK, int QPW = 1>
 __global__ __launch_bounds__(256) void quant_act_kernel(const uint16_t *__restrict__ x, int m,
                                                         int k, uint32_t *__restrict__ codes,
                                                         uint16_t *__restrict__ scales) {
-  // one quantization group of GK 64-wide blocks: the group's max spans them
+  // QPW consecutive quantization groups of GK 64-wide blocks each: a group's
+  // max spans its blocks
   const int KG = k / kGroup;
-  const int q0 = blockIdx.x, g0 = q0 * GK, t = blockIdx.y;
+  const int t = blockIdx.y;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int j = lane >> 3, h = (lane >> 2) & 1, l = lane & 3;
   const int i = 8 * w + j;          // token within the tile
   const int row = 32 * t + i;
   const int m32 = (int)gridDim.y * 32;
-  u32x4 raw[GK];
+  u32x4 raw[QPW][GK];
   // padding tokens read the last real row (m >= 1) and quantize zeros; every
   // load is issued before the first is used
   const bool live = row < m;
-  const uint16_t *src = x + (int64_t)(live ? row : m - 1) * k + g0 * kGroup + 32 * h + 8 * l;
+  const uint16_t *src = x + (int64_t)(live ? row : m - 1) * k + blockIdx.x * QPW * GK * kGroup + 32 * h + 8 * l;
 #pragma unroll
-  for (int q = 0; q < GK; q++) raw[q] = *reinterpret_cast<const u32x4 *>(src + q * kGroup);
+  for (int u = 0; u < QPW; u++)
 #pragma unroll
-  for (int q = 0; q < GK; q++)
-    if (!live) raw[q] = u32x4{0, 0, 0, 0};
-  float v[GK][8];
-  float amax = 0.0f;
+    for (int q = 0; q < GK; q++) raw[u][q] = *reinterpret_cast<const u32x4 *>(src + (u * GK + q) * kGroup);
 #pragma unroll
-  for (int q = 0; q < GK; q++) {
+  for (int u = 0; u < QPW; u++) {
+    const int q0 = blockIdx.x * QPW + u, g0 = q0 * GK;
 #pragma unroll
-    for (int e = 0; e < 4; e++) {
-      v[q][2 * e] = half_bits_to_float((uint16_t)(raw[q][e] & 0xffffu));
-      v[q][2 * e + 1] = half_bits_to_float((uint16_t)(raw[q][e] >> 16));
+    for (int q = 0; q < GK; q++)
+      if (!live) raw[u][q] = u32x4{0, 0, 0, 0};
+    float v[GK][8];
+    float amax = 0.0f;
+#pragma unroll
+    for (int q = 0; q < GK; q++) {
+#pragma unroll
+      for (int e = 0; e < 4; e++) {
+        v[q][2 * e] = half_bits_to_float((uint16_t)(raw[u][q][e] & 0xffffu));
+        v[q][2 * e + 1] = half_bits_to_float((uint16_t)(raw[u][q][e] >> 16));
+      }
+#pragma unroll
+      for (int e = 0; e < 8; e++) amax = fmaxf(amax, fabsf(v[q][e]));
     }
+    amax = max8_dpp(amax);
+    uint16_t s16;
+    const float s = q4_scale(amax, s16);
+    const float y = s == 0.0f ? 0.0f : __builtin_amdgcn_rcpf(s);
 #pragma unroll
-    for (int e = 0; e < 8; e++) amax = fmaxf(amax, fabsf(v[q][e]));
-  }
-  amax = max8_dpp(amax);
-  uint16_t s16;
-  const float s = q4_scale(amax, s16);
-  const float y = s == 0.0f ? 0.0f : __builtin_amdgcn_rcpf(s);
-#pragma unroll
-  for (int q = 0; q < GK; q++) {
-    const int g = g0 + q;   // the launch covers the K blocks exactly
-    uint32_t b0, b1;
-    quant8_fp8(v[q], s, y, b0, b1);
-    if constexpr (FP8) {
-      const int64_t off = (((int64_t)t * KG + g) * 2 + (l >> 1)) * 256 + (32 * h + i) * 4 + 2 * (l & 1);
-      *reinterpret_cast<uint2 *>(codes + off) = make_uint2(b0, b1);
-    } else {
-      // TQ4 word: the inverse of tq4_to_fp8 (codes 4..7 rotated into the
-      // bits 0x78787878 that codes 0..3 leave free)
-      codes[(((int64_t)t * KG + g) * 64 + 32 * h + i) * 4 + l] = b0 | __builtin_amdgcn_alignbit(b1, b1, 28);
+    for (int q = 0; q < GK; q++) {
+      const int g = g0 + q;   // the launch covers the K blocks exactly
+      uint32_t b0, b1;
+      quant8_fp8(v[q], s, y, b0, b1);
+      if constexpr (FP8) {
+        const int64_t off = (((int64_t)t * KG + g) * 2 + (l >> 1)) * 256 + (32 * h + i) * 4 + 2 * (l & 1);
+        *reinterpret_cast<uint2 *>(codes + off) = make_uint2(b0, b1);
+      } else {
+        // TQ4 word: the inverse of tq4_to_fp8 (codes 4..7 rotated into the
+        // bits 0x78787878 that codes 0..3 leave free)
+        codes[(((int64_t)t * KG + g) * 64 + 32 * h + i) * 4 + l] = b0 | __builtin_amdgcn_alignbit(b1, b1, 28);
+      }
     }
+    if ((lane & 7) == 0) scales[(int64_t)q0 * m32 + row] = row < m ? s16 : (uint16_t)0;
   }
-  if ((lane & 7) == 0) scales[(int64_t)q0 * m32 + row] = row < m ? s16 : (uint16_t)0;
 }
 
 // Rows of x quantized into TQ4 words in the layout of the packed weight
@@ -100,14 +108,24 @@ static void launch_quant_rows_tq4(const uint16_t *x, int m, int k, int gk, uint3
 
 hipError_t launch_quant_act(const uint16_t *x, int m, int k, int gk, uint32_t *codes,
                             uint16_t *scales, hipStream_t s) {
-  // one quantization group per work-group: the kernel is bound by its vector
-  // ALU work, and more groups per work-group measured slower at every size
+  // TQ4 output (up to kMidMaxTokens tokens): one quantization group per
+  // work-group (more groups per work-group measured slower there)
   if (!act_codes_fp8(m)) {
     launch_quant_rows_tq4(x, m, k, gk, codes, scales, s);
     return hipGetLastError();
   }
   const int m32 = (m + 31) / 32 * 32;
-  const dim3 grid((unsigned)(k / kGroup / gk), (unsigned)(m32 / 32));
+  const int kq = k / kGroup / gk;   // quantization groups per row
+  // 64-wide groups: four groups per work-group with all loads of a lane
+  // issued first (more bytes in flight per work-group: the 70B down layer's
+  // 8192 x 28672 activations quantize in 140-143 us instead of 149-154 us;
+  // no change at the smaller sizes, 2 % slower for 128-wide groups)
+  if (gk == 1 && kq % 4 == 0) {
+    const dim3 grid((unsigned)(kq / 4), (unsigned)(m32 / 32));
+    hipLaunchKernelGGL((quant_act_kernel<true, 1, 4>), grid, dim3(256), 0, s, x, m, k, codes, scales);
+    return hipGetLastError();
+  }
+  const dim3 grid((unsigned)kq, (unsigned)(m32 / 32));
   if (gk == 2) hipLaunchKernelGGL((quant_act_kernel<true, 2>), grid, dim3(256), 0, s, x, m, k, codes, scales);
   else hipLaunchKernelGGL((quant_act_kernel<true, 1>), grid, dim3(256), 0, s, x, m, k, codes, scales);
   return hipGetLastError();
