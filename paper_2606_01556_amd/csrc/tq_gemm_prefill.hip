@@ -20,9 +20,10 @@
 // (global_load_lds_dwordx4) into a D-slot ring; the loads of a group are
 // spread over the 8 wavefronts, and one workgroup barrier per group hands
 // slots over.  A wavefront's group step has a matrix-core phase (the eight
-// products of the group) and a vector phase (the rescaling fmas of those
-// products, the next group's LDS reads and operand expansion, its share of
-// the loads).  The two wavefronts of a SIMD run these phases out of step --
+// products of the group, with its share of the loads of a later group in
+// their shadow) and a vector phase (the rescaling fmas of those products, the
+// next group's LDS reads and operand expansion).  The two wavefronts of a
+// SIMD run these phases out of step --
 // their barrier sits after the matrix-core phase on one and after the vector
 // phase on the other -- so one issues matrix-core work while the other issues
 // vector work: on gfx950 a wavefront that interleaves both itself overlaps
@@ -35,7 +36,9 @@
 // placed in k = 0 and k = 4 (twice the product), and one fma adds their
 // product -- exactly I * s_x * s_w -- to the fp32 accumulator in ascending
 // group order, the oracle's order for H and for the residual, so Y is
-// bit-identical to the oracle's rounded result.
+// bit-identical to the oracle's rounded result.  128-wide groups (Sec. 5.1)
+// keep the 64-wide operand blocks: a group's two blocks add their integer
+// sums in the matrix core (its accumulator input) before the one rescale.
 
 #include <type_traits>
 
@@ -200,11 +203,12 @@ __device__ __forceinline__ void plan_main(const GemmArgs &a, int lane, int wave,
   }
 }
 
-// H pass.  A step covers one K-group, laid out in a slot as: the activation
-// tiles at P_A (as in the main loop), L1 rank tile t at P_B + 1024 t, and at
-// H_S the activation scales of the 128 tokens (256 B) followed by the L1
-// scales (256 B).  Every item is a wave load whose lane l reads 16 bytes at
-// base[l] + g * stride[l].
+// H pass.  A step covers one 64-wide K block, laid out in a slot as: the
+// activation tiles at P_A (as in the main loop), L1 rank tile t at
+// P_B + 1024 t, and at H_S the activation scales of the 128 tokens (256 B)
+// followed by the L1 scales (256 B) of the block's quantization group.  Every
+// item is a wave load whose lane l reads 16 bytes at base[l] + (g >> shift)
+// * stride[l].
 constexpr int H_S = P_SW;
 
 struct HPlan {
