@@ -318,9 +318,10 @@ __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, i
       fb[k] = m_uniform(H ? l1codes + ((int64_t)wave * KG + item_gi(k)) * 1024
                           : wcodes + ((int64_t)min(cb * CT + item_tile(k), ct32 - 1) * KG + item_gi(k)) * 1024);
     uint32_t islot = 0;   // ring offset of the next chunk to issue
-    auto issue = [&](int c) {
+    // (full: the chunk is known to lie within K)
+    auto issue = [&](int c, auto full) {
       const uint32_t slot = lds0 + islot;
-      if (MCG * (c + 1) <= KG) {
+      if (decltype(full)::value || MCG * (c + 1) <= KG) {
         mdma(sh_addr, slot + sl0.dst);
         if constexpr (FP8) mdma(sh_addr1, slot + sl1.dst);
 #pragma unroll
@@ -348,21 +349,25 @@ __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, i
     mwait_vm<0>();
     stage2_loads();
     for (int s = 0; s < D - 1; s++)
-      if (s < NCH) issue(s);
+      if (s < NCH) issue(s, std::false_type{});
     if (D - 1 <= NCH) mwait_vm<(D - 2) * PER>();   // chunk 0 has landed
     else mwait_vm<0>();
     __syncthreads();
     expand(0, 0);
     uint32_t rslot = 0;   // ring offset of chunk c
-    for (int c = 0; c < NCH; c++) {
+    // One chunk.  steady: chunk c + D - 1 is issued and lies within K (so
+    // chunks c and c + 1 do too): no test of the chunk index, and so no
+    // branch in the chunk (the chunks before the last D are all such).
+    auto chunk = [&](int c, auto steady_c) {
+      constexpr bool steady = decltype(steady_c)::value;
       // chunk c + 1 has landed for its expansion (fp8: chunk c, read as
       // loaded); near the end of K nothing is issued past the last chunk, so
       // everything issued is waited for
-      if (c + D - 1 <= NCH) mwait_vm<(FP8 ? D - 2 : D - 3) * PER>();
+      if (steady || c + D - 1 <= NCH) mwait_vm<(FP8 ? D - 2 : D - 3) * PER>();
       else mwait_vm<0>();
       __syncthreads();             // chunk c's operands are visible; chunk c - 1 is consumed
-      if (c + D - 1 < NCH) issue(c + D - 1);   // into chunk c - 1's slot
-      if (c + 1 < NCH) expand(c + 1, rslot + C::SLOT == D * C::SLOT ? 0 : rslot + C::SLOT);
+      if (steady || c + D - 1 < NCH) issue(c + D - 1, steady_c);   // into chunk c - 1's slot
+      if (steady || c + 1 < NCH) expand(c + 1, rslot + C::SLOT == D * C::SLOT ? 0 : rslot + C::SLOT);
       if constexpr (NF > 0) {
         const uint8_t *S = smem + rslot;
         const uint8_t *XE = smem + C::OFF_XE + (c & 1) * C::XEB;
@@ -381,7 +386,7 @@ __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, i
           }
           bv[k] = *reinterpret_cast<const u32x4 *>(S + C::S_FR + item_frag(k) * 1024 + lane * 16);
           const uint32_t s_a = *reinterpret_cast<const uint16_t *>(S + C::S_SC + (gi * 32 + l32) * 2);
-          sa[k] = MCG * c + gi < KG ? s_a : 0u;   // a group past K adds exactly zero
+          sa[k] = steady || MCG * c + gi < KG ? s_a : 0u;   // a group past K adds exactly zero
           const int so = H ? (C::NPX + C::NPW) * 16 + (gi * 32 * RT + 32 * wave + l32) * 2
                            : C::NPX * 16 + (gi * 32 * CT + 32 * item_tile(k) + l32) * 2;
           sb[k] = *reinterpret_cast<const uint16_t *>(S + C::S_SC + so);
@@ -399,7 +404,7 @@ __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, i
             for (int v = 0; v < 16; v++) acc[0][v] = fmaf(cg[v], pg[v], acc[0][v]);
           }
           rslot = rslot + C::SLOT == D * C::SLOT ? 0 : rslot + C::SLOT;
-          continue;
+          return;
         }
         // Every operand of the chunk is read before the first product; then
         // item k's two products go to the matrix core while the vector ALU
@@ -435,7 +440,10 @@ __global__ __launch_bounds__(64 * MW, 1) void dual_gemm_mid_kernel(GemmArgs a, i
         }
       }
       rslot = rslot + C::SLOT == D * C::SLOT ? 0 : rslot + C::SLOT;
-    }
+    };
+    int c = 0;
+    for (; MCG * (c + D) <= KG; c++) chunk(c, std::true_type{});
+    for (; c < NCH; c++) chunk(c, std::false_type{});
   };
 
   constexpr int NACC = C::NF_MAX > 1 ? C::NF_MAX : 1;
