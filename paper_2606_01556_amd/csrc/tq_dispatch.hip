@@ -10,8 +10,11 @@
 
 namespace tq {
 
-// one round of large-kernel blocks in the mid kernel's cost units
-constexpr int kLargeRound = 28;
+// one round of large-kernel blocks in the mid kernel's cost units, for 64-
+// and 128-wide groups (fitted to measured mid and large times: 164 layer
+// shapes with K 4096-28672, N 1024-14336, r 0-128, M 576-4096, and the
+// LLaMA3 shapes of both group widths)
+constexpr int kLargeRound64 = 34, kLargeRound128 = 28;
 // K-groups per prefill work-group run from which it beats the large kernel at r <= 64
 constexpr int kPrefillMinRun = 256;
 
@@ -39,10 +42,12 @@ int choose_kernel(const GemmArgs &a) {
   const bool prefill_wins = a.geo.gk == 1 ? a.geo.r_pad32 > 64 || long_run : a.geo.r_pad32 > 0;
   const bool large = blocks <= 256 || !prefill_wins;
   // Few large blocks leave most CUs idle (a round of them costs about as much
-  // as kLargeRound tile-group units of the mid kernel, whose 32-token blocks
-  // fill the CUs at these sizes too): take the cheaper of the two.
+  // as kLargeRound64 / kLargeRound128 tile-group units of the mid kernel,
+  // whose 32-token blocks fill the CUs at these sizes too): take the cheaper
+  // of the two.
   const int rounds = (blocks + 255) / 256;
-  const bool mid = large && dual_gemm_mid_cost(a) < rounds * kLargeRound;
+  const int large_round = a.geo.gk == 1 ? kLargeRound64 : kLargeRound128;
+  const bool mid = large && dual_gemm_mid_cost(a) < rounds * large_round;
   if (mid) return kKernelMid;
   return large ? kKernelLarge : kKernelPrefill;
 }
