@@ -303,6 +303,12 @@ def test_kernel_choice(L):
     assert tq.dual_gemm_kernel(tq.weight_desc_init(4096, 4096, 0, 128), 4096) == "large"
     assert tq.dual_gemm_kernel(tq.weight_desc_init(4096, 4096, 128, 128), 2048) == "large"
     assert tq.dual_gemm_kernel(tq.weight_desc_init(28672, 8192, 128, 128), 8192) == "prefill"
+    # the mid kernel's threshold over the large kernel is lower for 128-wide
+    # groups (28 against 34 of its cost units per round of large blocks)
+    assert tq.dual_gemm_kernel(tq.weight_desc_init(4096, 4096, 0), 1024) == "mid"
+    assert tq.dual_gemm_kernel(tq.weight_desc_init(4096, 4096, 0, 128), 1024) == "large"
+    assert tq.dual_gemm_kernel(tq.weight_desc_init(4096, 14336, 128), 576) == "mid"
+    assert tq.dual_gemm_kernel(tq.weight_desc_init(4096, 14336, 128, 128), 576) == "large"
     assert tq.dual_gemm_kernel(tq.weight_desc_init(8192, 28672, 128), 1) == "decode"
     assert tq.dual_gemm_kernel(tq.weight_desc_init(8192, 28672, 128), 8) == "decode"
     assert tq.dual_gemm_kernel(tq.weight_desc_init(8192, 28672, 128), 9) == "mid"
