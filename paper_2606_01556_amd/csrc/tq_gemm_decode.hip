@@ -59,7 +59,10 @@ struct DMode {
   static constexpr int XB = XFP8 ? 64 : 32;   // bytes per (group, token)
   // pairs of operands in flight per stage-1 wavefront, and the residual
   // ring's budget in 16-byte fragments (what fits 128 registers unspilled)
-  static constexpr int D1 = MODE == 16 ? 8 : 10;
+  static constexpr int D1 = MODE == 16 ? 8 : (MODE == 1 ? 9 : 10);
+  // one token: the two L1 scale rows of a pair arrive by one load (group A's
+  // row in lanes 0-31, group B's in lanes 32-63)
+  static constexpr bool MS = MODE == 1;
   static constexpr int RF = MODE == 1 ? 10 : 8;
 };
 
@@ -149,7 +152,9 @@ __device__ __forceinline__ float hi_half(uint32_t w) { return half_bits_to_float
 // CT weight fragments with their scales.
 struct S1Slot {
   u32x4 l1;
-  uint32_t sla, slb;  // fp16 L1 scales of groups A and B (the lane's rank)
+  // fp16 L1 scales of the lane's rank for groups A and B; for one token a
+  // single load, the lane's own group's row (sla only)
+  uint32_t sla, slb;
 };
 template <int CTW>
 struct ResSlot {
@@ -220,11 +225,16 @@ __global__ __launch_bounds__(64 * DW) void dual_gemm_decode_kernel(GemmArgs a,
   const uint32_t l1s_b = gk == 1 ? (uint32_t)geo.r_pad32 * 2 : 0u, ws_b = gk == 1 ? (uint32_t)geo.n_pad * 2 : 0u;
   const uint8_t *l1sb = reinterpret_cast<const uint8_t *>(l1scales);
   const uint8_t *wsb = reinterpret_cast<const uint8_t *>(wscales);
+  const uint32_t l1s_own = l1s_lane + gq * l1s_b;   // the lane's own group's row
   auto load_s1 = [&](S1Slot &S, int p) {
     S.l1 = *reinterpret_cast<const u32x4 *>(l1codes + (uint32_t)(p * 2048) + l1_lane);
     const uint8_t *sb = l1sb + (uint32_t)p * l1s_pair;
-    S.sla = *reinterpret_cast<const uint16_t *>(sb + l1s_lane);
-    S.slb = *reinterpret_cast<const uint16_t *>(sb + l1s_b + l1s_lane);
+    if constexpr (MD::MS) {
+      S.sla = *reinterpret_cast<const uint16_t *>(sb + l1s_own);
+    } else {
+      S.sla = *reinterpret_cast<const uint16_t *>(sb + l1s_lane);
+      S.slb = *reinterpret_cast<const uint16_t *>(sb + l1s_b + l1s_lane);
+    }
   };
   uint32_t w_lane[CTW], ws_lane[CTW];
   const uint32_t ws_gq = gq * ws_b;   // the lane's own block's group (TOK8)
@@ -382,6 +392,7 @@ __global__ __launch_bounds__(64 * DW) void dual_gemm_decode_kernel(GemmArgs a,
     v4f I;           // integer sums (TOK8: group A in lanes 0-31, B in 32-63)
     v4f I2;          // 16-token layout: group B's sums
     v4f sxa, sxb;
+    uint32_t sla, slb;   // one token: the L1 scales of groups A and B for lanes 0-31
   };
   auto s1_lds = [&](int p) -> S1Lds {
     S1Lds r;
@@ -402,6 +413,10 @@ __global__ __launch_bounds__(64 * DW) void dual_gemm_decode_kernel(GemmArgs a,
     }
     r.sxa = A.sxa;
     r.sxb = A.sxb;
+    // group B's scale comes from lanes 32-63, as its sums do (with 128-wide
+    // groups both halves read the same row and only sla is used)
+    r.sla = Sl.sla;
+    r.slb = MD::MS && GK != 2 ? __builtin_bit_cast(uint32_t, upper_half(__builtin_bit_cast(float, Sl.sla))) : 0u;
     return r;
   };
   // One chain step per group: h = fma(I s_x, s_L1, h).  I s_x is exact in
@@ -409,8 +424,8 @@ __global__ __launch_bounds__(64 * DW) void dual_gemm_decode_kernel(GemmArgs a,
   // same exact value I s_x s_L1 + h once, as fma(I, s_x s_L1, h) does; the
   // fp16 scale enters the fma without a separate conversion.
   auto s1_chain = [&](const S1Prod &P, const S1Slot &Sl) {
-    const _Float16 sla = __builtin_bit_cast(_Float16, (uint16_t)Sl.sla);
-    const _Float16 slb = __builtin_bit_cast(_Float16, (uint16_t)Sl.slb);
+    const _Float16 sla = __builtin_bit_cast(_Float16, (uint16_t)(MD::MS ? P.sla : Sl.sla));
+    const _Float16 slb = __builtin_bit_cast(_Float16, (uint16_t)(MD::MS ? P.slb : Sl.slb));
 #pragma unroll
     for (int v = 0; v < MV; v++) {
       const float ib = MD::TOK8 ? upper_half(P.I[v]) : P.I2[v];
